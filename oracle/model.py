@@ -1,0 +1,306 @@
+"""Oracle model: DLCL pre-norm encoder and incremental pre-norm decoder (NumPy).
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+What is computed, following the paper:
+
+* Encoder, Sec. 2.1 Eq. 1-2 (dynamic linear combination of layers, DLCL): the input
+  of layer l+1 is sum_{k<=l} W^(l+1)_k LN(y_k), with y_0 the embedding output and
+  y_k the k-th layer's output.  Deep encoder, shallow decoder: Sec. 3.2.
+* Tied embeddings: one matrix E is the source embedding, the target embedding and
+  the output projection (Sec. 2.2).
+* Caching (Sec. 4.1): the decoder keeps the key/value projections of every earlier
+  step (self-attention) and of the encoder output (cross-attention, computed once).
+
+Readings of what the paper leaves open (each is also listed in the design notes):
+
+* W is one scalar per (row, entry) pair: a lower-triangular (L+1)x(L+1) matrix.
+* Each history entry k has its own LayerNorm, applied once when y_k is produced.
+  ``hist_norm=False`` replaces it with the identity (used to check that one-hot W
+  reduces to the plain pre-norm stack).
+* Every layer (encoder and decoder) is pre-norm; the decoder has no DLCL.
+* Encoder output: enc = LN_out(sum_{k<=L} W[L+1,k] h_k).
+* Embedding: y_0 = sqrt(d) E[id] + PE(pos), PE interleaved sin/cos from position 0.
+* Attention scale 1/sqrt(d_head); ReLU FFN; biases on every projection except the
+  tied output projection; LayerNorm with biased variance and eps = 1e-5.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+import synth
+
+
+# ---------------------------------------------------------------------------
+# Primitives
+# ---------------------------------------------------------------------------
+def layer_norm(x, gamma, beta, eps=1e-5):
+    """LN(u) = gamma * (u - mean) / sqrt(var + eps) + beta over the last axis (biased var)."""
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + eps) * gamma + beta
+
+
+def positional_encoding(positions, d, dtype=np.float64):
+    """Sinusoidal encoding: PE(p, 2m) = sin(p / 10000^(2m/d)), PE(p, 2m+1) = cos(same)."""
+    pos = np.asarray(positions, dtype=np.float64)[:, None]
+    m = np.arange(d // 2, dtype=np.float64)[None, :]
+    ang = pos / np.power(10000.0, 2.0 * m / d)
+    pe = np.empty((pos.shape[0], d), dtype=np.float64)
+    pe[:, 0::2] = np.sin(ang)
+    pe[:, 1::2] = np.cos(ang)
+    return pe.astype(dtype)
+
+
+def softmax(x, axis=-1):
+    m = np.max(x, axis=axis, keepdims=True)
+    e = np.exp(x - m)
+    return e / e.sum(axis=axis, keepdims=True)
+
+
+def logsumexp(x, axis=-1):
+    m = np.max(x, axis=axis, keepdims=True)
+    return (m + np.log(np.exp(x - m).sum(axis=axis, keepdims=True))).squeeze(axis)
+
+
+def attention(q, k, v, n_heads, allowed=None):
+    """Multi-head scaled dot-product attention on already-projected q [Tq,d], k/v [Tk,d].
+
+    Head h uses columns h*dh..(h+1)*dh.  ``allowed`` [Tq,Tk] (bool) masks keys with -inf.
+    Returns the concatenated head outputs [Tq, d] (before the output projection).
+    """
+    tq, d = q.shape
+    dh = d // n_heads
+    out = np.empty((tq, d), dtype=q.dtype)
+    scale = 1.0 / math.sqrt(dh)
+    for h in range(n_heads):
+        sl = slice(h * dh, (h + 1) * dh)
+        s = (q[:, sl] @ k[:, sl].T) * q.dtype.type(scale)
+        if allowed is not None:
+            s = np.where(allowed, s, -np.inf)
+        out[:, sl] = softmax(s, axis=-1) @ v[:, sl]
+    return out
+
+
+def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> np.ndarray:
+    """Return a copy of the fp32 blob whose *matrices* (E and every W_*) are rounded to
+    fp16 or bf16 (round to nearest even) and widened back.  Biases, LayerNorm and DLCL
+    scalars keep fp32: that is what a half-precision model stores in half precision.
+    """
+    if precision == "f32":
+        return blob.copy()
+    out = blob.copy()
+    off = 0
+    for e in synth.weight_layout(shape):
+        if e.name == "E" or ".W_" in e.name:
+            seg = out[off:off + e.size]
+            if precision == "f16":
+                seg[:] = seg.astype(np.float16).astype(np.float32)
+            elif precision == "bf16":
+                u = seg.view(np.uint32).astype(np.uint64)
+                u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+                seg[:] = u.astype(np.uint32).view(np.float32)
+            else:
+                raise ValueError(precision)
+        off += e.size
+    return out
+
+
+def param_count_formula(V, d, F, L, Ld):
+    """Matrix parameters of a tied-embedding Transformer with L encoder / Ld decoder layers:
+    V*d + L*(4 d^2 + 2 d F) + Ld*(8 d^2 + 2 d F)."""
+    return V * d + L * (4 * d * d + 2 * d * F) + Ld * (8 * d * d + 2 * d * F)
+
+
+# ---------------------------------------------------------------------------
+# Model
+# ---------------------------------------------------------------------------
+class OracleModel:
+    """The full model on one sentence at a time.
+
+    ``blob`` is the canonical fp32 weight vector; ``precision`` rounds its matrices as
+    the GPU stores them ("f32", "f16", "bf16"); arithmetic is done in ``dtype``.
+    """
+
+    def __init__(self, shape: synth.ModelShape, blob: np.ndarray, dtype=np.float64,
+                 precision: str = "f32", hist_norm: bool = True, eps: float = 1e-5):
+        self.shape = shape
+        self.dtype = np.dtype(dtype)
+        self.hist_norm = hist_norm
+        self.eps = eps
+        named = synth.unpack(shape, round_weights(blob, shape, precision))
+        self.p = {k: v.astype(self.dtype) for k, v in named.items()}
+        self.d = shape.d_model
+        self.H = shape.n_heads
+        self.scale_emb = self.dtype.type(math.sqrt(self.d))
+
+    # -- pieces ---------------------------------------------------------------
+    def ln(self, x, prefix):
+        return layer_norm(x, self.p[prefix + ".gamma"], self.p[prefix + ".beta"], self.eps)
+
+    def embed(self, ids, positions):
+        ids = np.asarray(ids, dtype=np.int64)
+        return self.scale_emb * self.p["E"][ids] + positional_encoding(positions, self.d, self.dtype)
+
+    def hist_entry(self, y, k):
+        """N_k(y_k): the k-th history LayerNorm of Eq. 2, or the identity."""
+        return self.ln(y, f"hist_ln.{k}") if self.hist_norm else y
+
+    def dlcl_row(self, l):
+        """W[l, 0..l-1] for row l (1-based)."""
+        return self.p[f"dlcl.{l}"]
+
+    def enc_layer(self, x, i):
+        """One pre-norm encoder layer: a = x + MHA(LN1 x); y = a + FFN(LN2 a)."""
+        p = f"enc.{i}."
+        d = self.d
+        u = self.ln(x, p + "ln1")
+        qkv = u @ self.p[p + "W_qkv"] + self.p[p + "b_qkv"]
+        att = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], self.H)
+        a = x + att @ self.p[p + "W_o"] + self.p[p + "b_o"]
+        u = self.ln(a, p + "ln2")
+        f = np.maximum(u @ self.p[p + "W_1"] + self.p[p + "b_1"], 0)
+        return a + f @ self.p[p + "W_2"] + self.p[p + "b_2"]
+
+    # -- encoder (Eq. 1-2) ----------------------------------------------------
+    def encode(self, src, return_history=False):
+        """DLCL encoder over one unpadded sentence; returns enc [S, d]."""
+        L = self.shape.n_enc
+        src = np.asarray(src)
+        y = self.embed(src, np.arange(len(src)))
+        hist = [self.hist_entry(y, 0)]
+        for l in range(1, L + 1):
+            w = self.dlcl_row(l)
+            x = sum(w[k] * hist[k] for k in range(l))
+            y = self.enc_layer(x, l - 1)
+            hist.append(self.hist_entry(y, l))
+        w = self.dlcl_row(L + 1)
+        x = sum(w[k] * hist[k] for k in range(L + 1))
+        enc = self.ln(x, "enc_out_ln")
+        return (enc, hist) if return_history else enc
+
+    def cross_kv(self, enc):
+        """Encoder-decoder K/V of every decoder layer, computed once per sentence."""
+        d = self.d
+        out = []
+        for j in range(self.shape.n_dec):
+            kv = enc @ self.p[f"dec.{j}.W_kv"] + self.p[f"dec.{j}.b_kv"]
+            out.append((kv[:, :d], kv[:, d:]))
+        return out
+
+    # -- decoder ----------------------------------------------------------------
+    def dec_layer_step(self, z, j, cache_k, cache_v, cross):
+        """Incremental decoder layer for one row z [d] at the newest position.
+
+        cache_k/cache_v: the row's earlier self-attention keys/values [t, d] of this
+        layer (t may be 0).  Returns (z', k_new, v_new)."""
+        p = f"dec.{j}."
+        d = self.d
+        u = self.ln(z[None, :], p + "ln1")
+        qkv = u @ self.p[p + "W_qkv"] + self.p[p + "b_qkv"]
+        k_all = np.concatenate([cache_k, qkv[:, d:2 * d]], axis=0)
+        v_all = np.concatenate([cache_v, qkv[:, 2 * d:]], axis=0)
+        att = attention(qkv[:, :d], k_all, v_all, self.H)
+        z = z + (att @ self.p[p + "W_o"] + self.p[p + "b_o"])[0]
+        u = self.ln(z[None, :], p + "ln2")
+        q = u @ self.p[p + "W_q"] + self.p[p + "b_q"]
+        att = attention(q, cross[j][0], cross[j][1], self.H)
+        z = z + (att @ self.p[p + "W_oc"] + self.p[p + "b_oc"])[0]
+        u = self.ln(z[None, :], p + "ln3")
+        f = np.maximum(u @ self.p[p + "W_1"] + self.p[p + "b_1"], 0)
+        z = z + (f @ self.p[p + "W_2"] + self.p[p + "b_2"])[0]
+        return z, qkv[0, d:2 * d], qkv[0, 2 * d:]
+
+    def output_logits(self, z):
+        """logits = LN_dec(z) E^T (tied projection, no bias)."""
+        return self.ln(z, "dec_out_ln") @ self.p["E"].T
+
+    def decode_full(self, cross, tokens):
+        """Full recompute: decoder over [BOS] + tokens with a causal mask.
+
+        Returns logits [len(tokens)+1, V]; row t predicts the token after position t."""
+        d, n = self.d, len(tokens) + 1
+        inp = np.concatenate([[synth.BOS_ID], np.asarray(tokens, dtype=np.int64)]).astype(np.int64)
+        z = self.embed(inp, np.arange(n))
+        causal = np.tril(np.ones((n, n), dtype=bool))
+        for j in range(self.shape.n_dec):
+            p = f"dec.{j}."
+            u = self.ln(z, p + "ln1")
+            qkv = u @ self.p[p + "W_qkv"] + self.p[p + "b_qkv"]
+            att = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], self.H, causal)
+            z = z + att @ self.p[p + "W_o"] + self.p[p + "b_o"]
+            u = self.ln(z, p + "ln2")
+            q = u @ self.p[p + "W_q"] + self.p[p + "b_q"]
+            z = z + attention(q, cross[j][0], cross[j][1], self.H) @ self.p[p + "W_oc"] + self.p[p + "b_oc"]
+            u = self.ln(z, p + "ln3")
+            f = np.maximum(u @ self.p[p + "W_1"] + self.p[p + "b_1"], 0)
+            z = z + f @ self.p[p + "W_2"] + self.p[p + "b_2"]
+        return self.output_logits(z)
+
+    def teacher_forced_logits(self, src, tokens, incremental=True):
+        """Logits of every step when the decoder is fed ``tokens`` (BOS first)."""
+        cross = self.cross_kv(self.encode(src))
+        if not incremental:
+            return self.decode_full(cross, tokens)
+        sc = IncrementalScorer(self, src, cross=cross)
+        rows = []
+        prefix: list = []
+        for t in range(len(tokens) + 1):
+            logits, _ = sc([prefix])
+            rows.append(logits[0])
+            if t < len(tokens):
+                prefix = prefix + [int(tokens[t])]
+        return np.stack(rows)
+
+
+class IncrementalScorer:
+    """Next-token logits for a set of target prefixes, with cached keys/values.
+
+    Called once per step with every live prefix of length t (all of the same length);
+    the caches of the previous step's prefixes are looked up by the prefix minus its
+    last token, extended by one slot, and kept for the next step only.  Returns
+    (logits [n, V], lse [n])."""
+
+    def __init__(self, model: OracleModel, src, cross=None):
+        self.m = model
+        self.cross = cross if cross is not None else model.cross_kv(model.encode(src))
+        Ld, d = model.shape.n_dec, model.d
+        empty = np.zeros((0, d), dtype=model.dtype)
+        self.caches = {(): [(empty, empty) for _ in range(Ld)]}
+        self.t = 0
+
+    def __call__(self, prefixes):
+        m = self.m
+        t = len(prefixes[0]) if prefixes else 0
+        new_caches = {}
+        logits = []
+        for pre in prefixes:
+            pre = tuple(int(x) for x in pre)
+            assert len(pre) == t
+            parent = self.caches[pre[:-1]] if t > 0 else self.caches[()]
+            token = pre[-1] if t > 0 else synth.BOS_ID
+            z = m.embed([token], [t])[0]
+            layer_caches = []
+            for j in range(m.shape.n_dec):
+                ck, cv = parent[j]
+                z, k_new, v_new = m.dec_layer_step(z, j, ck, cv, self.cross)
+                layer_caches.append((np.concatenate([ck, k_new[None]]), np.concatenate([cv, v_new[None]])))
+            new_caches[pre] = layer_caches
+            logits.append(m.output_logits(z[None, :])[0])
+        self.caches = new_caches
+        logits = np.stack(logits)
+        return logits, logsumexp(logits, axis=-1)
+
+
+class FullRecomputeScorer:
+    """Same interface as IncrementalScorer, recomputing the whole prefix every call."""
+
+    def __init__(self, model: OracleModel, src, cross=None):
+        self.m = model
+        self.cross = cross if cross is not None else model.cross_kv(model.encode(src))
+
+    def __call__(self, prefixes):
+        logits = np.stack([self.m.decode_full(self.cross, list(p))[-1] for p in prefixes])
+        return logits, logsumexp(logits, axis=-1)
