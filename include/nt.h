@@ -1,0 +1,223 @@
+/*
+ * nt.h -- C ABI of the MI355X (gfx950) deep-encoder / shallow-decoder translation library.
+ *
+ * The library translates batches of token-ID sentences with a Transformer whose encoder
+ * combines layers dynamically (DLCL, Sec. 2.1 Eq. 1-2: the input of layer l+1 is
+ * sum_{k<=l} W_k^(l+1) LN(y_k), y_0 being the embedding) and whose decoder runs one
+ * step at a time over cached self-attention keys/values and encoder-decoder
+ * keys/values computed once per batch (Sec. 4.1 "Caching").  Around the model sit the
+ * decoding optimisations of Sec. 4: greedy search (Sec. 4.4), beam search with the
+ * early-stop rule (Sec. 4.1 "Faster Beam Search"), batch pruning (Sec. 4.1), dynamic
+ * batching by a token budget (Sec. 4.2), FP16 inference with fp32 reductions (Sec. 4.2)
+ * and one memory pool per call (Sec. 4.4 "Profile-guided optimization").
+ *
+ * Conventions shared by every entry point
+ *  - Handles are opaque; device pointers are plain HIP device addresses (for example
+ *    torch tensors' data_ptr()); `stream` is a hipStream_t passed as void* (NULL = the
+ *    null stream).  All device work is enqueued on that stream.
+ *  - The caller owns every buffer it passes in.  The library owns only the small host
+ *    structs nt_model and nt_dec_state (freed by nt_free_model / nt_free_state) and never
+ *    frees caller memory.
+ *  - Every function returns an nt_status and, on failure, sets a thread-local message
+ *    readable with nt_last_error().  Nothing throws across the ABI and nothing aborts.
+ *  - Special token IDs: PAD = 0, BOS = 1, EOS = 2 (UNK = 3 is an ordinary word).
+ *  - Output tokens exclude BOS and EOS.  Outputs of nt_translate are in input order
+ *    (Sec. 4.3 and Sec. 5: inputs are sorted by length and the original order restored).
+ */
+#ifndef NT_H_
+#define NT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  NT_OK = 0,
+  NT_E_INVALID = 1,      /* bad argument: null pointer, empty input, ID out of range, size */
+  NT_E_UNSUPPORTED = 2,  /* a shape or option the kernels do not implement */
+  NT_E_WORKSPACE = 3,    /* workspace too small; the message states the bytes required */
+  NT_E_DEVICE = 4,       /* a HIP runtime error */
+  NT_E_STATE = 5,        /* a call that does not fit the state (e.g. a step after the end) */
+  NT_E_NUMERIC = 6       /* reserved: NaN/Inf detected by a debug check */
+} nt_status;
+
+typedef enum { NT_F32 = 0, NT_F16 = 1, NT_BF16 = 2 } nt_dtype;
+
+typedef struct nt_model nt_model;
+typedef struct nt_dec_state nt_dec_state;
+
+/* Model shape and numeric mode.
+ *  d_model % n_heads == 0, d_head = d_model / n_heads in {32, 64, 128}, d_model % 64 == 0,
+ *  d_ffn % 64 == 0.  max_positions bounds source and target positions (1024 in Sec. 2.2).
+ *  dtype: storage type of matrices and activations.  NT_F32 is true fp32 end to end;
+ *  NT_F16 / NT_BF16 store weights and activations in 16 bits and keep every
+ *  accumulation, LayerNorm, softmax, log-sum-exp, DLCL sum and search score in fp32
+ *  (Sec. 4.2 "FP16 Inference": reductions run in a wider type to avoid overflow).
+ *  dlcl_hist_norm: 1 = each history entry is LayerNorm'd as in Eq. 2 (the default);
+ *  0 = identity, so that one-hot DLCL weights give the plain pre-norm stack.
+ *  ln_eps: LayerNorm epsilon (1e-5). */
+typedef struct {
+  int32_t d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_positions;
+  int32_t pad_id, bos_id, eos_id;
+  int32_t dtype;
+  int32_t dlcl_hist_norm;
+  float ln_eps;
+} nt_model_cfg;
+
+/* Search and batching options.
+ *  beam: 1 = greedy (Sec. 4.4), 2..16 = beam search (Sec. 4.1).
+ *  len_penalty: alpha of lp(n) = ((5+n)/6)^alpha applied to finished/final scores; 0 = raw.
+ *  max target tokens of sentence i (EOS counted) = floor(max_len_a * len_i) + max_len_b.
+ *  token_budget: dynamic batching (Sec. 4.2) packs sentences, longest first, while
+ *    n_sentences * longest_length <= token_budget (padded source tokens).
+ *  max_batch_sents: 0 = no cap; otherwise at most this many sentences per batch.
+ *  early_stop: 1 = stop a sentence's beam once its best finished hypothesis scores at
+ *    least every live one (Sec. 4.1); 0 = run to the length limit.
+ *  prune: 1 = drop finished sentences from the decoder's batch every step (Sec. 4.1
+ *    "Batch Pruning"); 0 = keep computing them (results are identical). */
+typedef struct {
+  int32_t beam;
+  float len_penalty;
+  float max_len_a;
+  int32_t max_len_b;
+  int32_t token_budget;
+  int32_t max_batch_sents;
+  int32_t early_stop;
+  int32_t prune;
+} nt_search_cfg;
+
+/* ---- weights --------------------------------------------------------------------------
+ * The host weight blob is one fp32 vector in this canonical order (matrices row-major
+ * "in x out", y = x W):
+ *   E [V,d] (tied: source embedding, target embedding and output projection, Sec. 2.2);
+ *   hist_ln[k].{gamma,beta} [d] for k = 0..L  (the LN of Eq. 2, one per history entry);
+ *   DLCL W: rows l = 1..L+1, row l holding W[l,0..l-1] (Eq. 2, one scalar per pair);
+ *   per encoder layer: ln1.{g,b}, W_qkv [d,3d] (columns Q|K|V, head h at h*dh within
+ *     each), b_qkv [3d], W_o [d,d], b_o, ln2.{g,b}, W_1 [d,F], b_1 [F], W_2 [F,d], b_2;
+ *   enc_out_ln.{g,b};
+ *   per decoder layer: ln1.{g,b}, W_qkv, b_qkv, W_o, b_o, ln2.{g,b}, W_q [d,d], b_q,
+ *     W_kv [d,2d] (columns K|V), b_kv, W_oc [d,d], b_oc, ln3.{g,b}, W_1, b_1, W_2, b_2;
+ *   dec_out_ln.{g,b}.
+ */
+
+/* Sizes for a model: host_floats = length of the fp32 blob; device_bytes = size of the
+ * device buffer nt_load_weights needs.  Returns NT_E_INVALID / NT_E_UNSUPPORTED for a
+ * shape the library cannot run. */
+nt_status nt_weights_size(const nt_model_cfg* cfg, size_t* host_floats, size_t* device_bytes);
+
+/* Converts the host blob into the device layout: matrices rounded (nearest even) to the
+ * model dtype and stored transposed ([out][in]) for the GEMMs, vectors kept in fp32, a
+ * sinusoidal position table computed once.  device_buf (>= device_bytes, 256-byte
+ * aligned) is borrowed for the model's lifetime.  The host blob may be freed on return.
+ * Synchronises `stream` before returning. */
+nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, size_t host_floats,
+                          void* device_buf, size_t device_bytes, void* stream, nt_model** out);
+void nt_free_model(nt_model* m);
+
+/* ---- workspace (the memory pool) -------------------------------------------------------
+ * Bytes of workspace needed to encode and decode one batch of up to max_sents sentences
+ * padded to max_src tokens under `search` (beam width and length limits). */
+nt_status nt_workspace_size(const nt_model* m, const nt_search_cfg* search, int32_t max_sents,
+                            int32_t max_src, size_t* bytes);
+
+/* Bytes of workspace nt_translate needs for this exact input: the maximum over the
+ * batches that dynamic batching forms from it. */
+nt_status nt_translate_workspace_size(const nt_model* m, const nt_search_cfg* search,
+                                      const int64_t* h_src_off, int32_t n_sent, size_t* bytes);
+
+/* ---- step-level entry points -----------------------------------------------------------
+ * nt_encode runs the DLCL encoder (Eq. 1-2) on a padded batch and computes the
+ * encoder-decoder keys/values of every decoder layer once (Sec. 4.1), then sets up the
+ * decoder state.  d_src: [B,S] int32 device IDs, row-major, PAD-padded; d_len: [B] int32
+ * device lengths (1..S).  IDs must lie in [0, vocab): nt_translate checks them on the
+ * host; here an ID outside the range is read as the nearest valid ID.  d_ws / ws_bytes: workspace,
+ * borrowed until nt_free_state.  Asynchronous except for a small host->device copy of
+ * per-sentence length limits, which reads h_len if given (else copies d_len back). */
+nt_status nt_encode(nt_model* m, const int32_t* d_src, const int32_t* d_len, const int32_t* h_len,
+                    int32_t B, int32_t S, const nt_search_cfg* search, void* d_ws, size_t ws_bytes,
+                    void* stream, nt_dec_state** st);
+
+/* One decoder step for every live hypothesis: embedding, Ld pre-norm layers with the
+ * cached self-attention keys/values (the new key/value is appended at slot t) and the
+ * cached encoder-decoder keys/values, the tied output projection, then selection (greedy
+ * argmax with log-sum-exp, or beam top-2K) and the search update; with pruning on, the
+ * finished sentences leave the batch.
+ *  d_forced: NULL, or [B*beam] int32 device tokens (greedy only): teacher forcing --
+ *    row r emits d_forced[r] instead of its argmax (its log-prob is still recorded);
+ *    an ID outside [0, V) is replaced by EOS.
+ *  d_logits: NULL, or [B*beam, V] fp32 device buffer receiving this step's logits of
+ *    the live rows (rows of finished sentences are left untouched).
+ *  h_alive: NULL, or host int32 receiving the number of sentences still decoding; asking
+ *    for it synchronises the stream.
+ * Returns NT_E_STATE once every sentence has finished. */
+nt_status nt_decode_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, int32_t* h_alive,
+                         void* stream);
+
+/* Results of a finished batch, one row per sentence in batch order:
+ *  h_tokens [B, max_tgt] int32 (row i valid up to h_lens[i]), h_lens [B],
+ *  h_scores [B] (normalised score; with alpha = 0 the sum of log-probs including EOS),
+ *  h_token_logp [B, max_tgt] fp32 log-prob of each output token.  Any pointer may be
+ *  NULL.  max_tgt is reported by nt_dec_state_info.  NT_E_STATE if a sentence is still
+ *  decoding.  Synchronises the stream. */
+nt_status nt_dec_state_read(nt_dec_state* st, int32_t* h_tokens, int32_t* h_lens, float* h_scores,
+                            float* h_token_logp, void* stream);
+
+/* Shape of a state: batch size, padded source length, beam, max target tokens, steps
+ * taken, sentences still decoding (as of the last step that reported it). */
+nt_status nt_dec_state_info(const nt_dec_state* st, int32_t* B, int32_t* S, int32_t* beam,
+                            int32_t* max_tgt, int32_t* steps, int32_t* alive);
+
+/* Copies the encoder output LN_out(x_{L+1}) [B,S,d] to host fp32 (rows of padding
+ * included).  Synchronises the stream.  For tests. */
+nt_status nt_dec_state_encoder_out(nt_dec_state* st, float* h_enc, void* stream);
+
+void nt_free_state(nt_dec_state* st);
+
+/* ---- whole-job entry point -------------------------------------------------------------
+ * Translates n_sent sentences given in CSR form on the host (h_src: concatenated IDs,
+ * h_src_off: [n_sent+1] offsets, every sentence 1..max_positions IDs in [0, V)).
+ * Sentences are sorted by descending length, packed into batches under the token budget,
+ * encoded and decoded batch by batch in the workspace, and written back in input order:
+ * h_out receives the concatenated output tokens (capacity out_cap; the sum of every
+ * sentence's max target length always suffices), h_out_off [n_sent+1] the offsets,
+ * h_score [n_sent] (or NULL) the scores, h_tok_logp [out_cap] (or NULL) each output
+ * token's log-prob.  Returns when the outputs are in host memory. */
+nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* h_src,
+                       const int64_t* h_src_off, int32_t n_sent, int32_t* h_out, int64_t out_cap,
+                       int64_t* h_out_off, float* h_score, float* h_tok_logp, void* d_ws,
+                       size_t ws_bytes, void* stream);
+
+/* Thread-local message of the last failing call on this thread ("" if none). */
+const char* nt_last_error(void);
+
+/* ---- kernel timing ---------------------------------------------------------------------
+ * When enabled for a kernel class, the library brackets each launch of that class with
+ * HIP events on the launch stream and records the launch's algorithmic bytes and flops
+ * (the data the method must move or compute, not what the kernel happens to touch). */
+typedef enum {
+  NT_K_GEMM_ENC = 0,    /* encoder projections (QKV, O, FFN1, FFN2) and the cross-K/V GEMM */
+  NT_K_GEMM_DEC = 1,    /* decoder-step projections */
+  NT_K_GEMM_VOCAB = 2,  /* tied output projection (logits) */
+  NT_K_DLCL = 3,        /* fused history LayerNorm + DLCL combination (+ next LN) */
+  NT_K_LN = 4,          /* plain LayerNorm (and the decoder embedding) */
+  NT_K_ATTN_ENC = 5,    /* encoder self-attention */
+  NT_K_ATTN_SELF = 6,   /* decoder self-attention over the step cache */
+  NT_K_ATTN_CROSS = 7,  /* decoder encoder-decoder attention */
+  NT_K_SELECT = 8,      /* argmax / top-2K with log-sum-exp */
+  NT_K_SEARCH = 9,      /* search update, compaction, finalisation */
+  NT_K_COUNT = 10
+} nt_kernel_class;
+
+nt_status nt_prof_enable(uint32_t class_mask);   /* bit i enables class i; 0 disables */
+nt_status nt_prof_reset(void);
+/* Totals since the last reset for one class; synchronises on the recorded events. */
+nt_status nt_prof_get(int32_t kernel_class, int64_t* launches, double* total_ms, double* alg_bytes,
+                      double* alg_flops);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NT_H_ */

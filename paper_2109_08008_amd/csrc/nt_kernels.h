@@ -1,0 +1,167 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher enqueues on `s` and
+// returns hipGetLastError() of the launch.  Shapes are validated by the runtime
+// (nt_runtime.cpp) before any launch; launchers assume them.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace nt {
+
+enum class DT : int { F32 = 0, F16 = 1, BF16 = 2 };
+inline size_t dt_bytes(DT t) { return t == DT::F32 ? 4 : 2; }
+
+// ---------------------------------------------------------------------------------
+// GEMM: C[M,N] = A[M,K] . Bt[N,K]^T  (+ epilogue), fp32 accumulation on MFMA.
+// A row stride lda (elements), Bt is [N][K] contiguous (weights stored "out x in").
+enum EpiMode : int {
+  EPI_STORE = 0,      // out = acc + bias
+  EPI_RELU = 1,       // out = max(acc + bias, 0)
+  EPI_RESID = 2,      // out = resid + acc + bias  (resid may alias out)
+  EPI_SELF_QKV = 3,   // decoder: cols [0,d) -> q out; [d,3d) -> K/V cache slot t of phys row
+  EPI_CROSS_KV = 4,   // encoder: cols of [Ld][K|V][d] -> cross cache [Ld][2][B][H][S][dh]
+};
+
+struct GemmEpi {
+  int mode = EPI_STORE;
+  const float* bias = nullptr;   // [N] fp32 or null
+  const void* resid = nullptr;   // [M][ldc], same type as out
+  void* out = nullptr;           // [M][ldc]
+  int ldc = 0;
+  int out_f32 = 0;               // 1: out is fp32 (logits); else the model dtype
+  // EPI_SELF_QKV
+  const int* sent_list = nullptr;  // logical sentence -> batch sentence
+  int beam = 1;
+  void* kcache = nullptr;          // [R][H][Tcap][dh] of this layer
+  void* vcache = nullptr;
+  int t = 0, Tcap = 0;
+  // EPI_SELF_QKV / EPI_CROSS_KV
+  int d = 0, H = 0, dh = 0;
+  // EPI_CROSS_KV
+  void* cross = nullptr;           // [Ld][2][B][H][S][dh]
+  int B = 0, S = 0;
+};
+
+hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
+                hipStream_t s);
+
+// ---------------------------------------------------------------------------------
+// Normalisation / embedding kernels (one wave per row of d = 64*EPL elements).
+struct DlclArgs {
+  int l;                    // combination row l = 1..L+1; produces history entry l-1
+  const void* y_prev;       // [rows][d] model dtype, or null for l = 1 (embedding)
+  const int* ids;           // l = 1: [rows] token ids
+  const int* lens;          // l = 1: [rows / S] sentence lengths (positions >= len are PAD)
+  int S;                    // l = 1: padded length (position = row % S)
+  const void* E;            // l = 1: [V][d] embedding
+  int V;                    // l = 1: IDs are clamped to [0, V) so bad input cannot read past E
+  const float* pe;          // l = 1: [max_pos][d] position table
+  float emb_scale;          // sqrt(d)
+  void* hist;               // history base; entry k at hist + k*hist_stride elements
+  size_t hist_stride;
+  const float* hist_ln;     // [2][d] gamma|beta of history entry l-1
+  int hist_norm;
+  const float* w;           // W[l][0..l-1]
+  void* x_out;              // [rows][d] or null
+  const float* ln;          // [2][d] LN applied to x (ln1 of layer l, or the output LN)
+  void* u_out;              // [rows][d]
+  int rows, d;
+  float eps;
+};
+hipError_t dlcl_combine(DT dt, const DlclArgs& a, hipStream_t s);
+
+// y = LN(x) row-wise; gamma|beta at ln[0..d), ln[d..2d).
+hipError_t layernorm(DT dt, const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s);
+
+// Decoder step input: z[r] = emb_scale*E[tok[phys(r)]] + pe[t]; u[r] = LN(z[r]).
+hipError_t dec_embed_ln(DT dt, const int* cur_tok, const int* sent_list, int beam, const void* E,
+                        const float* pe, int t, float emb_scale, const float* ln, void* z, void* u,
+                        int rows, int d, float eps, hipStream_t s);
+
+// Weight packing: dst[n][k] = (T) src[k][n] (src fp32 [K][N] row-major).
+hipError_t pack_transpose(DT dt, const float* src, void* dst, int K, int N, hipStream_t s);
+// dst[i] = (T) src[i].
+hipError_t pack_convert(DT dt, const float* src, void* dst, size_t n, hipStream_t s);
+
+// ---------------------------------------------------------------------------------
+// Attention.
+// Grouped multi-head attention over keys stored per (group, head): group g has
+// nq(g) queries and len(g) valid keys.  Used for encoder self-attention (group =
+// sentence, queries = its tokens) and decoder encoder-decoder attention (group =
+// live sentence, queries = its beam rows).
+struct MhaArgs {
+  const void* q; int q_ld;       // query row r at q + r*q_ld + h*dh
+  const void* k; const void* v;  // key (b,h,s) at k + b*kb + h*kh + s*ks
+  long long kb, kh, ks;
+  void* out; int out_ld;         // out row r at out + r*out_ld + h*dh
+  const int* group_map;          // logical group -> b (null: identity)
+  const int* lens;               // [b] valid keys (and valid queries for self-attention)
+  int q_per_group;               // queries of group g are rows g*q_per_group + i
+  int self_queries;              // 1: query i valid only if i < lens[b] (padded rows -> 0)
+  int n_groups, H, dh;
+  float scale;
+};
+hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s);
+
+// Decoder self-attention of each live row over its cached slots 0..t.
+struct SelfAttnArgs {
+  const void* q;              // [rows][d]
+  const void* kcache; const void* vcache;  // [R][H][Tcap][dh]
+  const int* sent_list; int beam;
+  const int* anc;             // [R][Tcap] physical row holding slot s (null: own row)
+  void* out;                  // [rows][d]
+  int rows, H, dh, t, Tcap;
+  float scale;
+};
+hipError_t self_attn(DT dt, const SelfAttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------------
+// Search.
+struct SearchState {
+  int B, beam, V, eos, Tcap;
+  float alpha;
+  int early_stop;
+  const int* sent_list;   // live sentences (logical order)
+  int n_live;             // entries in sent_list
+  float* score;           // [R] raw hypothesis scores
+  int* cur_tok;           // [R] next input token
+  int* tok_hist;          // [Tcap][R]
+  int* par_hist;          // [Tcap][R]
+  float* lp_hist;         // [Tcap][R]
+  const int* anc_cur;     // [R][Tcap]
+  int* anc_next;
+  int* done;              // [B]
+  const int* maxlen;      // [B]
+  float* best_score;      // [B] normalised
+  float* best_raw;        // [B]
+  int* best_step;         // [B]
+  int* best_row;          // [B]
+  int* best_nout;         // [B]
+};
+
+// Greedy: per live row, argmax (lowest ID on ties) and log-sum-exp over V logits, then
+// the update (token, log-prob, EOS / length stop).  forced: [R] (by phys row) or null.
+hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, int t, hipStream_t s);
+
+// Beam: per live row, log-sum-exp and the 2K largest logits; then per live sentence the
+// candidate ranking, the walk, the stop rule and the ancestor-table update.
+hipError_t beam_select(const float* logits, int rows, int V, int k2, float* topv, int* topi, float* lse,
+                       hipStream_t s);
+hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, int t,
+                       hipStream_t s);
+
+// Compaction: new_list = [b in list if !done[b]] in order; count -> *n_out (device).
+hipError_t compact(const int* list, int n, const int* done, int* new_list, int* n_out, hipStream_t s);
+
+// Backtrack every sentence's best hypothesis into out_tok/out_lp [B][Tcap], out_len/out_score [B].
+hipError_t finalize(const SearchState& st, int* out_tok, float* out_lp, int* out_len, float* out_score,
+                    hipStream_t s);
+
+// Initialise per-batch search state (scores 0 / -inf, BOS, best = -inf, done = 0, identity list).
+hipError_t search_init(const SearchState& st, int* list, int bos, hipStream_t s);
+
+// Scatter rows of the compact logits [rows][V] to dst[phys(r)][V].
+hipError_t scatter_logits(const float* logits, const int* sent_list, int beam, int rows, int V, float* dst,
+                          hipStream_t s);
+
+}  // namespace nt

@@ -1,0 +1,1184 @@
+// Host runtime of the translation library: the C ABI declared in include/nt.h.
+//
+//  * model: validates the shape, lays the weights out on the device (matrices
+//    transposed to [out][in] in the model dtype, vectors fp32, a sinusoidal position
+//    table) and converts the caller's fp32 blob there with packing kernels;
+//  * workspace arena: one caller-owned device buffer per batch is carved into every
+//    tensor the encoder and decoder need (the memory pool of Sec. 4.4; nothing is
+//    allocated during decoding); encoder temporaries and decoder buffers share space,
+//    since the encoder is finished before the first decoder step;
+//  * encoder (Eq. 1-2), decoder steps with cached keys/values (Sec. 4.1), greedy and
+//    beam search, batch pruning (Sec. 4.1) and dynamic batching (Sec. 4.2);
+//  * optional per-kernel-class event timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "../../include/nt.h"
+#include "nt_kernels.h"
+
+using nt::DT;
+
+// --------------------------------------------------------------------------------------
+// errors
+namespace {
+thread_local std::string g_err;
+
+nt_status fail(nt_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define NT_HIP(expr)                                                                          \
+  do {                                                                                        \
+    hipError_t e_ = (expr);                                                                   \
+    if (e_ != hipSuccess) return fail(NT_E_DEVICE, "%s: %s (%s:%d)", #expr, hipGetErrorString(e_), __FILE__, __LINE__); \
+  } while (0)
+
+#define NT_TRY(expr)                    \
+  do {                                  \
+    nt_status s_ = (expr);              \
+    if (s_ != NT_OK) return s_;         \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// --------------------------------------------------------------------------------------
+// kernel timing
+struct ProfRec {
+  int cls;
+  hipEvent_t a, b;
+  double bytes, flops;
+};
+std::mutex g_prof_mu;
+uint32_t g_prof_mask = 0;
+std::vector<ProfRec> g_prof;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename F>
+hipError_t timed(int cls, hipStream_t s, double bytes, double flops, F&& launch) {
+  if (!(g_prof_mask & (1u << cls))) return launch();
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  hipEvent_t a = prof_event(), b = prof_event();
+  if (!a || !b) return hipErrorOutOfMemory;
+  hipError_t e = hipEventRecord(a, s);
+  if (e != hipSuccess) return e;
+  e = launch();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(b, s);
+  g_prof.push_back({cls, a, b, bytes, flops});
+  return e;
+}
+
+}  // namespace
+
+// --------------------------------------------------------------------------------------
+// model
+struct EncLayerW {
+  const float *ln1, *bqkv, *bo, *ln2, *b1, *b2;
+  const void *Wqkv, *Wo, *W1, *W2;
+};
+struct DecLayerW {
+  const float *ln1, *bqkv, *bo, *ln2, *bq, *boc, *ln3, *b1, *b2;
+  const void *Wqkv, *Wo, *Wq, *Woc, *W1, *W2;
+};
+
+struct nt_model {
+  nt_model_cfg cfg;
+  DT dt;
+  size_t eb;
+  int d, H, dh, F, L, Ld, V;
+  const void* E;
+  const float* pe;
+  const float* hist_ln;   // [L+1][2][d]
+  const float* dlcl;      // row l (1-based) at dlcl + l(l-1)/2
+  std::vector<EncLayerW> enc;
+  const float* enc_out_ln;
+  std::vector<DecLayerW> dec;
+  const void* Wkv_all;    // [Ld*2d][d]
+  const float* bkv_all;   // [Ld*2d]
+  const float* dec_out_ln;
+};
+
+namespace {
+
+nt_status validate_cfg(const nt_model_cfg* c) {
+  if (!c) return fail(NT_E_INVALID, "null model config");
+  if (c->d_model <= 0 || c->n_heads <= 0 || c->d_ffn <= 0 || c->n_enc < 0 || c->n_dec <= 0 || c->vocab <= 0 ||
+      c->max_positions <= 0)
+    return fail(NT_E_INVALID, "model sizes must be positive (n_enc >= 0)");
+  if (c->vocab < 4) return fail(NT_E_INVALID, "vocab must hold PAD, BOS, EOS and a word (>= 4)");
+  for (int id : {c->pad_id, c->bos_id, c->eos_id})
+    if (id < 0 || id >= c->vocab) return fail(NT_E_INVALID, "special token id %d outside [0, %d)", id, c->vocab);
+  if (c->dtype < NT_F32 || c->dtype > NT_BF16) return fail(NT_E_INVALID, "unknown dtype %d", c->dtype);
+  if (c->d_model % 64 != 0) return fail(NT_E_UNSUPPORTED, "d_model %% 64 != 0 (d_model=%d)", c->d_model);
+  const int e = c->d_model / 64;
+  if (e != 1 && e != 2 && e != 4 && e != 6 && e != 8 && e != 12 && e != 16)
+    return fail(NT_E_UNSUPPORTED, "d_model=%d not in {64,128,256,384,512,768,1024}", c->d_model);
+  if (c->d_model % c->n_heads != 0) return fail(NT_E_UNSUPPORTED, "d_model %% n_heads != 0");
+  const int dh = c->d_model / c->n_heads;
+  if (dh != 32 && dh != 64 && dh != 128) return fail(NT_E_UNSUPPORTED, "head size %d not in {32,64,128}", dh);
+  if (c->d_ffn % 64 != 0) return fail(NT_E_UNSUPPORTED, "d_ffn %% 64 != 0 (d_ffn=%d)", c->d_ffn);
+  if (c->max_positions > 1024) return fail(NT_E_UNSUPPORTED, "max_positions > 1024");
+  if (!(c->ln_eps > 0.f)) return fail(NT_E_INVALID, "ln_eps must be > 0");
+  return NT_OK;
+}
+
+// Offsets of the device layout (bytes) and of the host blob (floats).
+struct ModelLayout {
+  size_t total = 0;
+  size_t E, pe, hist_ln, dlcl, enc_out_ln, Wkv_all, bkv_all, dec_out_ln;
+  struct Enc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2; };
+  struct Dec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Woc, boc, ln3, W1, b1, W2, b2; };
+  std::vector<Enc> enc;
+  std::vector<Dec> dec;
+  // host blob (fp32) offsets
+  size_t hE, hhist, hdlcl, henc_out, hdec_out, host_floats;
+  struct HEnc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2; };
+  struct HDec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Wkv, bkv, Woc, boc, ln3, W1, b1, W2, b2; };
+  std::vector<HEnc> henc;
+  std::vector<HDec> hdec;
+};
+
+ModelLayout layout_of(const nt_model_cfg& c) {
+  ModelLayout Lo;
+  const size_t d = c.d_model, F = c.d_ffn, V = c.vocab, L = c.n_enc, Ld = c.n_dec;
+  const size_t eb = c.dtype == NT_F32 ? 4 : 2;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  Lo.E = take(V * d * eb);
+  Lo.pe = take((size_t)c.max_positions * d * 4);
+  Lo.hist_ln = take((L + 1) * 2 * d * 4);
+  Lo.dlcl = take((L + 1) * (L + 2) / 2 * 4);
+  for (size_t i = 0; i < L; ++i) {
+    ModelLayout::Enc e;
+    e.ln1 = take(2 * d * 4);
+    e.Wqkv = take(3 * d * d * eb);
+    e.bqkv = take(3 * d * 4);
+    e.Wo = take(d * d * eb);
+    e.bo = take(d * 4);
+    e.ln2 = take(2 * d * 4);
+    e.W1 = take(F * d * eb);
+    e.b1 = take(F * 4);
+    e.W2 = take(d * F * eb);
+    e.b2 = take(d * 4);
+    Lo.enc.push_back(e);
+  }
+  Lo.enc_out_ln = take(2 * d * 4);
+  for (size_t j = 0; j < Ld; ++j) {
+    ModelLayout::Dec e;
+    e.ln1 = take(2 * d * 4);
+    e.Wqkv = take(3 * d * d * eb);
+    e.bqkv = take(3 * d * 4);
+    e.Wo = take(d * d * eb);
+    e.bo = take(d * 4);
+    e.ln2 = take(2 * d * 4);
+    e.Wq = take(d * d * eb);
+    e.bq = take(d * 4);
+    e.Woc = take(d * d * eb);
+    e.boc = take(d * 4);
+    e.ln3 = take(2 * d * 4);
+    e.W1 = take(F * d * eb);
+    e.b1 = take(F * 4);
+    e.W2 = take(d * F * eb);
+    e.b2 = take(d * 4);
+    Lo.dec.push_back(e);
+  }
+  Lo.Wkv_all = take(Ld * 2 * d * d * eb);
+  Lo.bkv_all = take(Ld * 2 * d * 4);
+  Lo.dec_out_ln = take(2 * d * 4);
+  Lo.total = off;
+
+  // host blob, canonical order (see include/nt.h)
+  size_t h = 0;
+  Lo.hE = h; h += V * d;
+  Lo.hhist = h; h += (L + 1) * 2 * d;
+  Lo.hdlcl = h; h += (L + 1) * (L + 2) / 2;
+  for (size_t i = 0; i < L; ++i) {
+    ModelLayout::HEnc e;
+    e.ln1 = h; h += 2 * d;
+    e.Wqkv = h; h += d * 3 * d;
+    e.bqkv = h; h += 3 * d;
+    e.Wo = h; h += d * d;
+    e.bo = h; h += d;
+    e.ln2 = h; h += 2 * d;
+    e.W1 = h; h += d * F;
+    e.b1 = h; h += F;
+    e.W2 = h; h += F * d;
+    e.b2 = h; h += d;
+    Lo.henc.push_back(e);
+  }
+  Lo.henc_out = h; h += 2 * d;
+  for (size_t j = 0; j < Ld; ++j) {
+    ModelLayout::HDec e;
+    e.ln1 = h; h += 2 * d;
+    e.Wqkv = h; h += d * 3 * d;
+    e.bqkv = h; h += 3 * d;
+    e.Wo = h; h += d * d;
+    e.bo = h; h += d;
+    e.ln2 = h; h += 2 * d;
+    e.Wq = h; h += d * d;
+    e.bq = h; h += d;
+    e.Wkv = h; h += d * 2 * d;
+    e.bkv = h; h += 2 * d;
+    e.Woc = h; h += d * d;
+    e.boc = h; h += d;
+    e.ln3 = h; h += 2 * d;
+    e.W1 = h; h += d * F;
+    e.b1 = h; h += F;
+    e.W2 = h; h += F * d;
+    e.b2 = h; h += d;
+    Lo.hdec.push_back(e);
+  }
+  Lo.hdec_out = h; h += 2 * d;
+  Lo.host_floats = h;
+  return Lo;
+}
+
+// --------------------------------------------------------------------------------------
+// workspace arena of one batch
+struct WsPlan {
+  size_t total = 0;
+  // persistent through the batch
+  size_t src, len, maxlen, enc_out, cross;
+  size_t kself, vself, score, cur_tok, tok_hist, par_hist, lp_hist, anc, done, best_score, best_raw, best_step,
+      best_row, best_nout, list, count, out_tok, out_lp, out_len, out_score;
+  // encoder temporaries (union with the decoder buffers below)
+  size_t hist, x, u, qkv, att, a, f, y;
+  // decoder buffers
+  size_t z, du, dq, datt, df, logits, topv, topi, lse;
+};
+
+WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
+  WsPlan p;
+  const size_t T = (size_t)B * S, R = (size_t)B * K, d = m.d, eb = m.eb;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + std::max<size_t>(bytes, 1));
+    return o;
+  };
+  p.src = take(T * 4);
+  p.len = take(B * 4);
+  p.maxlen = take(B * 4);
+  p.enc_out = take(T * d * eb);
+  p.cross = take((size_t)m.Ld * 2 * T * d * eb);
+  p.kself = take((size_t)m.Ld * R * Tcap * d * eb);
+  p.vself = take((size_t)m.Ld * R * Tcap * d * eb);
+  p.score = take(R * 4);
+  p.cur_tok = take(R * 4);
+  p.tok_hist = take((size_t)Tcap * R * 4);
+  p.par_hist = take((size_t)Tcap * R * 4);
+  p.lp_hist = take((size_t)Tcap * R * 4);
+  p.anc = take(K > 1 ? 2 * R * Tcap * 4 : 0);
+  p.done = take(B * 4);
+  p.best_score = take(B * 4);
+  p.best_raw = take(B * 4);
+  p.best_step = take(B * 4);
+  p.best_row = take(B * 4);
+  p.best_nout = take(B * 4);
+  p.list = take(2 * (size_t)B * 4);
+  p.count = take(16);
+  p.out_tok = take((size_t)B * Tcap * 4);
+  p.out_lp = take((size_t)B * Tcap * 4);
+  p.out_len = take(B * 4);
+  p.out_score = take(B * 4);
+  const size_t base = off;
+  // encoder temporaries
+  p.hist = take((size_t)(m.L + 1) * T * d * eb);
+  p.x = take(T * d * eb);
+  p.u = take(T * d * eb);
+  p.qkv = take(T * 3 * d * eb);
+  p.att = take(T * d * eb);
+  p.a = take(T * d * eb);
+  p.f = take(T * m.F * eb);
+  p.y = take(T * d * eb);
+  const size_t enc_end = off;
+  // decoder buffers reuse the same space
+  off = base;
+  p.z = take(R * d * eb);
+  p.du = take(R * d * eb);
+  p.dq = take(R * d * eb);
+  p.datt = take(R * d * eb);
+  p.df = take(R * m.F * eb);
+  p.logits = take(R * m.V * 4);
+  p.topv = take(R * 2 * K * 4);
+  p.topi = take(R * 2 * K * 4);
+  p.lse = take(R * 4);
+  p.total = std::max(enc_end, off);
+  return p;
+}
+
+int max_tgt_of(const nt_search_cfg& s, int len) {
+  return (int)std::floor((double)s.max_len_a * (double)len) + s.max_len_b;
+}
+
+nt_status validate_search(const nt_model& m, const nt_search_cfg* s) {
+  if (!s) return fail(NT_E_INVALID, "null search config");
+  if (s->beam < 1) return fail(NT_E_INVALID, "beam must be >= 1");
+  if (s->beam > 16) return fail(NT_E_UNSUPPORTED, "beam %d > 16", s->beam);
+  if (s->max_len_a < 0.f || !std::isfinite(s->max_len_a)) return fail(NT_E_INVALID, "max_len_a must be >= 0");
+  if (s->token_budget < 0 || s->max_batch_sents < 0) return fail(NT_E_INVALID, "negative budget / sentence cap");
+  if (!std::isfinite(s->len_penalty)) return fail(NT_E_INVALID, "len_penalty must be finite");
+  (void)m;
+  return NT_OK;
+}
+
+}  // namespace
+
+// --------------------------------------------------------------------------------------
+// decoder state
+struct nt_dec_state {
+  nt_model* m;
+  nt_search_cfg sc;
+  int B, S, K, Tcap;
+  int t = 0;
+  int n_live = 0;     // entries of the current live list
+  int n_alive = 0;    // sentences not finished
+  int list_cur = 0;   // which half of the list buffer is current
+  int anc_cur = 0;
+  bool finished = false;
+  WsPlan plan;
+  char* ws;
+  int* h_count = nullptr;   // pinned 4-byte mailbox
+  template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+  int* list(int which) const { return at<int>(plan.list) + (size_t)which * B; }
+  int* anc(int which) const { return at<int>(plan.anc) + (size_t)which * B * K * Tcap; }
+  nt::SearchState search() const {
+    nt::SearchState s;
+    s.B = B;
+    s.beam = K;
+    s.V = m->V;
+    s.eos = m->cfg.eos_id;
+    s.Tcap = Tcap;
+    s.alpha = sc.len_penalty;
+    s.early_stop = sc.early_stop;
+    s.sent_list = list(list_cur);
+    s.n_live = n_live;
+    s.score = at<float>(plan.score);
+    s.cur_tok = at<int>(plan.cur_tok);
+    s.tok_hist = at<int>(plan.tok_hist);
+    s.par_hist = at<int>(plan.par_hist);
+    s.lp_hist = at<float>(plan.lp_hist);
+    s.anc_cur = K > 1 ? anc(anc_cur) : nullptr;
+    s.anc_next = K > 1 ? anc(anc_cur ^ 1) : nullptr;
+    s.done = at<int>(plan.done);
+    s.maxlen = at<int>(plan.maxlen);
+    s.best_score = at<float>(plan.best_score);
+    s.best_raw = at<float>(plan.best_raw);
+    s.best_step = at<int>(plan.best_step);
+    s.best_row = at<int>(plan.best_row);
+    s.best_nout = at<int>(plan.best_nout);
+    return s;
+  }
+};
+
+namespace {
+
+// ---- encoder (Eq. 1-2) ---------------------------------------------------------------
+nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
+  const nt_model& m = *st->m;
+  const int B = st->B, S = st->S, d = m.d, L = m.L;
+  const int T = B * S;
+  const double eb = (double)m.eb;
+  auto at = [&](size_t o) { return st->ws + o; };
+  const WsPlan& p = st->plan;
+  const size_t hist_stride = (size_t)T * d;
+  const float eps = m.cfg.ln_eps;
+
+  auto gemm_enc = [&](const void* A, int lda, const void* W, int N, int K, const nt::GemmEpi& e) -> hipError_t {
+    const double bytes = ((double)T * K + (double)N * K) * eb + (double)T * N * eb * (e.mode == nt::EPI_RESID ? 2 : 1);
+    return timed(NT_K_GEMM_ENC, s, bytes, 2.0 * T * N * K, [&] { return nt::gemm(m.dt, A, lda, W, T, N, K, e, s); });
+  };
+
+  for (int l = 1; l <= L + 1; ++l) {
+    nt::DlclArgs a{};
+    a.l = l;
+    a.y_prev = l == 1 ? nullptr : at(p.y);
+    a.ids = st->at<int>(p.src);
+    a.lens = st->at<int>(p.len);
+    a.S = S;
+    a.E = m.E;
+    a.V = m.V;
+    a.pe = m.pe;
+    a.emb_scale = std::sqrt((float)d);
+    a.hist = at(p.hist);
+    a.hist_stride = hist_stride;
+    a.hist_ln = m.hist_ln + (size_t)(l - 1) * 2 * d;
+    a.hist_norm = m.cfg.dlcl_hist_norm;
+    a.w = m.dlcl + (size_t)l * (l - 1) / 2;
+    a.x_out = l <= L ? at(p.x) : nullptr;
+    a.ln = l <= L ? m.enc[l - 1].ln1 : m.enc_out_ln;
+    a.u_out = l <= L ? at(p.u) : at(p.enc_out);
+    a.rows = T;
+    a.d = d;
+    a.eps = eps;
+    const double bytes = (double)T * d * eb * (l + (l <= L ? 3 : 2));
+    NT_HIP(timed(NT_K_DLCL, s, bytes, 2.0 * T * d * l, [&] { return nt::dlcl_combine(m.dt, a, s); }));
+    if (l > L) break;
+    const EncLayerW& w = m.enc[l - 1];
+
+    nt::GemmEpi e{};
+    e.mode = nt::EPI_STORE;
+    e.bias = w.bqkv;
+    e.out = at(p.qkv);
+    e.ldc = 3 * d;
+    NT_HIP(gemm_enc(at(p.u), d, w.Wqkv, 3 * d, d, e));
+
+    nt::MhaArgs ma{};
+    ma.q = at(p.qkv);
+    ma.q_ld = 3 * d;
+    ma.k = at(p.qkv) + (size_t)d * m.eb;
+    ma.v = at(p.qkv) + (size_t)2 * d * m.eb;
+    ma.kb = (long long)S * 3 * d;
+    ma.kh = m.dh;
+    ma.ks = 3 * d;
+    ma.out = at(p.att);
+    ma.out_ld = d;
+    ma.group_map = nullptr;
+    ma.lens = st->at<int>(p.len);
+    ma.q_per_group = S;
+    ma.self_queries = 1;
+    ma.n_groups = B;
+    ma.H = m.H;
+    ma.dh = m.dh;
+    ma.scale = 1.0f / std::sqrt((float)m.dh);
+    NT_HIP(timed(NT_K_ATTN_ENC, s, 4.0 * T * d * eb, 4.0 * B * (double)S * S * d, [&] { return nt::mha(m.dt, ma, s); }));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RESID;
+    e.bias = w.bo;
+    e.resid = at(p.x);
+    e.out = at(p.a);
+    e.ldc = d;
+    NT_HIP(gemm_enc(at(p.att), d, w.Wo, d, d, e));
+
+    NT_HIP(timed(NT_K_LN, s, 2.0 * T * d * eb, 8.0 * T * d,
+                 [&] { return nt::layernorm(m.dt, at(p.a), w.ln2, at(p.u), T, d, eps, s); }));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RELU;
+    e.bias = w.b1;
+    e.out = at(p.f);
+    e.ldc = m.F;
+    NT_HIP(gemm_enc(at(p.u), d, w.W1, m.F, d, e));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RESID;
+    e.bias = w.b2;
+    e.resid = at(p.a);
+    e.out = at(p.y);
+    e.ldc = d;
+    NT_HIP(gemm_enc(at(p.f), m.F, w.W2, d, m.F, e));
+  }
+
+  // encoder-decoder keys/values of every decoder layer, once per batch (Sec. 4.1)
+  nt::GemmEpi e{};
+  e.mode = nt::EPI_CROSS_KV;
+  e.bias = m.bkv_all;
+  e.cross = at(p.cross);
+  e.d = d;
+  e.H = m.H;
+  e.dh = m.dh;
+  e.B = B;
+  e.S = S;
+  NT_HIP(gemm_enc(at(p.enc_out), d, m.Wkv_all, 2 * d * m.Ld, d, e));
+  return NT_OK;
+}
+
+// ---- one decoder step ------------------------------------------------------------------
+nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, hipStream_t s) {
+  const nt_model& m = *st->m;
+  const WsPlan& p = st->plan;
+  const int K = st->K, d = m.d, R = st->n_live * K, t = st->t;
+  const size_t Rp = (size_t)st->B * K;
+  const double eb = (double)m.eb;
+  const float eps = m.cfg.ln_eps;
+  auto at = [&](size_t o) { return st->ws + o; };
+  const int* list = st->list(st->list_cur);
+
+  auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
+    const double ob = e.out_f32 ? 4.0 : eb;
+    const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
+    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, R, N, Kd, e, s); });
+  };
+
+  NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
+    return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, t, std::sqrt((float)d), m.dec[0].ln1,
+                            at(p.z), at(p.du), R, d, eps, s);
+  }));
+
+  for (int j = 0; j < m.Ld; ++j) {
+    const DecLayerW& w = m.dec[j];
+    char* kc = at(p.kself) + (size_t)j * Rp * st->Tcap * d * m.eb;
+    char* vc = at(p.vself) + (size_t)j * Rp * st->Tcap * d * m.eb;
+
+    nt::GemmEpi e{};
+    e.mode = nt::EPI_SELF_QKV;
+    e.bias = w.bqkv;
+    e.out = at(p.dq);
+    e.ldc = d;
+    e.sent_list = list;
+    e.beam = K;
+    e.kcache = kc;
+    e.vcache = vc;
+    e.t = t;
+    e.Tcap = st->Tcap;
+    e.d = d;
+    e.H = m.H;
+    e.dh = m.dh;
+    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wqkv, 3 * d, d, e));
+
+    nt::SelfAttnArgs sa{};
+    sa.q = at(p.dq);
+    sa.kcache = kc;
+    sa.vcache = vc;
+    sa.sent_list = list;
+    sa.beam = K;
+    sa.anc = K > 1 ? st->anc(st->anc_cur) : nullptr;
+    sa.out = at(p.datt);
+    sa.rows = R;
+    sa.H = m.H;
+    sa.dh = m.dh;
+    sa.t = t;
+    sa.Tcap = st->Tcap;
+    sa.scale = 1.0f / std::sqrt((float)m.dh);
+    NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * (2.0 + 2.0 * (t + 1)), 4.0 * R * (t + 1) * (double)d,
+                 [&] { return nt::self_attn(m.dt, sa, s); }));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RESID;
+    e.bias = w.bo;
+    e.resid = at(p.z);
+    e.out = at(p.z);
+    e.ldc = d;
+    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Wo, d, d, e));
+
+    NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), R, d, eps, s); }));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_STORE;
+    e.bias = w.bq;
+    e.out = at(p.dq);
+    e.ldc = d;
+    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wq, d, d, e));
+
+    const size_t cross_layer = (size_t)2 * st->B * st->S * d;   // elements per layer (K and V)
+    nt::MhaArgs ma{};
+    ma.q = at(p.dq);
+    ma.q_ld = d;
+    ma.k = at(p.cross) + (size_t)j * cross_layer * m.eb;
+    ma.v = at(p.cross) + ((size_t)j * cross_layer + (size_t)st->B * st->S * d) * m.eb;
+    ma.kb = (long long)m.H * st->S * m.dh;
+    ma.kh = (long long)st->S * m.dh;
+    ma.ks = m.dh;
+    ma.out = at(p.datt);
+    ma.out_ld = d;
+    ma.group_map = list;
+    ma.lens = st->at<int>(p.len);
+    ma.q_per_group = K;
+    ma.self_queries = 0;
+    ma.n_groups = st->n_live;
+    ma.H = m.H;
+    ma.dh = m.dh;
+    ma.scale = 1.0f / std::sqrt((float)m.dh);
+    NT_HIP(timed(NT_K_ATTN_CROSS, s, ((double)st->n_live * 2 * st->S * d + 2.0 * R * d) * eb,
+                 4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s); }));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RESID;
+    e.bias = w.boc;
+    e.resid = at(p.z);
+    e.out = at(p.z);
+    e.ldc = d;
+    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Woc, d, d, e));
+
+    NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), R, d, eps, s); }));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RELU;
+    e.bias = w.b1;
+    e.out = at(p.df);
+    e.ldc = m.F;
+    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.W1, m.F, d, e));
+
+    e = nt::GemmEpi{};
+    e.mode = nt::EPI_RESID;
+    e.bias = w.b2;
+    e.resid = at(p.z);
+    e.out = at(p.z);
+    e.ldc = d;
+    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.df), m.F, w.W2, d, m.F, e));
+
+    const float* next_ln = j + 1 < m.Ld ? m.dec[j + 1].ln1 : m.dec_out_ln;
+    NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                 [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), R, d, eps, s); }));
+  }
+
+  // tied output projection: logits = LN_dec(z) E^T  (fp32 logits)
+  nt::GemmEpi e{};
+  e.mode = nt::EPI_STORE;
+  e.out = at(p.logits);
+  e.ldc = m.V;
+  e.out_f32 = 1;
+  NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+  if (d_logits) NT_HIP(nt::scatter_logits(st->at<float>(p.logits), list, K, R, m.V, d_logits, s));
+
+  nt::SearchState ss = st->search();
+  if (K == 1) {
+    NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V,
+                 [&] { return nt::greedy_step(st->at<float>(p.logits), d_forced, ss, t, s); }));
+  } else {
+    NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V, [&] {
+      return nt::beam_select(st->at<float>(p.logits), R, m.V, 2 * K, st->at<float>(p.topv), st->at<int>(p.topi),
+                             st->at<float>(p.lse), s);
+    }));
+    NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
+      return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, t, s);
+    }));
+    st->anc_cur ^= 1;
+  }
+  int* cnt = st->at<int>(p.count);
+  NT_HIP(timed(NT_K_SEARCH, s, (double)st->n_live * 8, 0.0, [&] {
+    return nt::compact(list, st->n_live, st->at<int>(p.done), st->list(st->list_cur ^ 1), cnt, s);
+  }));
+  NT_HIP(hipMemcpyAsync(st->h_count, cnt, sizeof(int), hipMemcpyDeviceToHost, s));
+  NT_HIP(hipStreamSynchronize(s));
+  st->t = t + 1;
+  st->n_alive = *st->h_count;
+  if (st->sc.prune) {
+    st->list_cur ^= 1;
+    st->n_live = st->n_alive;
+  }
+  if (st->n_alive == 0) st->finished = true;
+  if (!st->finished && st->t >= st->Tcap)
+    return fail(NT_E_STATE, "internal: %d sentences alive after %d steps", st->n_alive, st->t);
+  return NT_OK;
+}
+
+nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, const int32_t* h_len, int B, int S,
+                      const nt_search_cfg* sc, void* d_ws, size_t ws_bytes, hipStream_t s, nt_dec_state** out) {
+  if (!m || !d_src || !d_len || !out || !d_ws) return fail(NT_E_INVALID, "null argument to nt_encode");
+  NT_TRY(validate_search(*m, sc));
+  if (B <= 0 || S <= 0) return fail(NT_E_INVALID, "empty batch (B=%d, S=%d)", B, S);
+  if (S > m->cfg.max_positions) return fail(NT_E_INVALID, "S=%d > max_positions=%d", S, m->cfg.max_positions);
+  std::vector<int> lens(B);
+  if (h_len) {
+    std::memcpy(lens.data(), h_len, sizeof(int) * B);
+  } else {
+    NT_HIP(hipMemcpyAsync(lens.data(), d_len, sizeof(int) * B, hipMemcpyDeviceToHost, s));
+    NT_HIP(hipStreamSynchronize(s));
+  }
+  int Tcap = 0;
+  std::vector<int> maxlen(B);
+  for (int b = 0; b < B; ++b) {
+    if (lens[b] < 1 || lens[b] > S) return fail(NT_E_INVALID, "sentence %d has length %d outside [1, %d]", b, lens[b], S);
+    maxlen[b] = max_tgt_of(*sc, lens[b]);
+    if (maxlen[b] < 1) return fail(NT_E_INVALID, "max target length %d < 1", maxlen[b]);
+    Tcap = std::max(Tcap, maxlen[b]);
+  }
+  if (Tcap > m->cfg.max_positions)
+    return fail(NT_E_INVALID, "max target length %d > max_positions %d", Tcap, m->cfg.max_positions);
+  const WsPlan plan = ws_plan(*m, B, S, sc->beam, Tcap);
+  if (ws_bytes < plan.total)
+    return fail(NT_E_WORKSPACE, "workspace too small: %zu bytes given, %zu required", ws_bytes, plan.total);
+  if ((reinterpret_cast<uintptr_t>(d_ws) & (kAlign - 1)) != 0) return fail(NT_E_INVALID, "workspace must be 256-byte aligned");
+
+  nt_dec_state* st = new nt_dec_state();
+  st->m = m;
+  st->sc = *sc;
+  st->B = B;
+  st->S = S;
+  st->K = sc->beam;
+  st->Tcap = Tcap;
+  st->plan = plan;
+  st->ws = static_cast<char*>(d_ws);
+  st->n_live = B;
+  st->n_alive = B;
+  if (hipHostMalloc((void**)&st->h_count, sizeof(int), hipHostMallocDefault) != hipSuccess) {
+    delete st;
+    return fail(NT_E_DEVICE, "hipHostMalloc failed");
+  }
+  auto bail = [&](nt_status code) {
+    (void)hipHostFree(st->h_count);
+    delete st;
+    return code;
+  };
+  auto chk = [&](hipError_t e, const char* what) -> nt_status {
+    if (e == hipSuccess) return NT_OK;
+    return bail(fail(NT_E_DEVICE, "%s: %s", what, hipGetErrorString(e)));
+  };
+  nt_status r;
+  if (d_src != st->at<int>(plan.src) &&
+      (r = chk(hipMemcpyAsync(st->at<int>(plan.src), d_src, sizeof(int) * (size_t)B * S, hipMemcpyDeviceToDevice, s),
+               "copy src")) != NT_OK)
+    return r;
+  if (d_len != st->at<int>(plan.len) &&
+      (r = chk(hipMemcpyAsync(st->at<int>(plan.len), d_len, sizeof(int) * B, hipMemcpyDeviceToDevice, s), "copy len")) != NT_OK)
+    return r;
+  if ((r = chk(hipMemcpyAsync(st->at<int>(plan.maxlen), maxlen.data(), sizeof(int) * B, hipMemcpyHostToDevice, s),
+               "copy maxlen")) != NT_OK)
+    return r;
+  if (st->K > 1 &&
+      (r = chk(hipMemsetAsync(st->at<int>(plan.anc), 0, sizeof(int) * 2 * (size_t)B * st->K * Tcap, s), "clear anc")) != NT_OK)
+    return r;
+  if ((r = run_encoder(st, s)) != NT_OK) return bail(r);
+  if ((r = chk(nt::search_init(st->search(), st->list(0), m->cfg.bos_id, s), "search init")) != NT_OK) return r;
+  // the host copy of maxlen must not be freed before the copy has run
+  if ((r = chk(hipStreamSynchronize(s), "sync")) != NT_OK) return r;
+  *out = st;
+  return NT_OK;
+}
+
+nt_status read_impl(nt_dec_state* st, int32_t* h_tokens, int32_t* h_lens, float* h_scores, float* h_token_logp,
+                    hipStream_t s) {
+  if (!st) return fail(NT_E_INVALID, "null state");
+  if (!st->finished) return fail(NT_E_STATE, "%d sentences are still decoding", st->n_alive);
+  const WsPlan& p = st->plan;
+  NT_HIP(nt::finalize(st->search(), st->at<int>(p.out_tok), st->at<float>(p.out_lp), st->at<int>(p.out_len),
+                      st->at<float>(p.out_score), s));
+  const size_t n = (size_t)st->B * st->Tcap;
+  if (h_tokens) NT_HIP(hipMemcpyAsync(h_tokens, st->at<int>(p.out_tok), n * 4, hipMemcpyDeviceToHost, s));
+  if (h_token_logp) NT_HIP(hipMemcpyAsync(h_token_logp, st->at<float>(p.out_lp), n * 4, hipMemcpyDeviceToHost, s));
+  if (h_lens) NT_HIP(hipMemcpyAsync(h_lens, st->at<int>(p.out_len), st->B * 4, hipMemcpyDeviceToHost, s));
+  if (h_scores) NT_HIP(hipMemcpyAsync(h_scores, st->at<float>(p.out_score), st->B * 4, hipMemcpyDeviceToHost, s));
+  NT_HIP(hipStreamSynchronize(s));
+  return NT_OK;
+}
+
+void free_state(nt_dec_state* st) {
+  if (!st) return;
+  if (st->h_count) (void)hipHostFree(st->h_count);
+  delete st;
+}
+
+// ---- dynamic batching (Sec. 4.2) ----------------------------------------------------------
+struct Batch {
+  int first, count, S, Tcap;   // a run of the length-sorted order
+};
+
+std::vector<Batch> plan_batches(const std::vector<int>& order, const std::vector<int>& lens, const nt_search_cfg& sc) {
+  std::vector<Batch> out;
+  const int n = (int)order.size();
+  int i = 0;
+  while (i < n) {
+    const int S = lens[order[i]];
+    int cnt = 1;
+    while (i + cnt < n) {
+      if (sc.token_budget > 0 && (long long)(cnt + 1) * S > sc.token_budget) break;
+      if (sc.max_batch_sents > 0 && cnt + 1 > sc.max_batch_sents) break;
+      ++cnt;
+    }
+    out.push_back({i, cnt, S, max_tgt_of(sc, S)});
+    i += cnt;
+  }
+  return out;
+}
+
+nt_status validate_sources(const nt_model& m, const nt_search_cfg& sc, const int32_t* h_src, const int64_t* off,
+                           int n_sent, std::vector<int>& lens, bool check_ids) {
+  if (!off || n_sent <= 0) return fail(NT_E_INVALID, "n_sent must be > 0 with offsets");
+  if (off[0] != 0) return fail(NT_E_INVALID, "h_src_off[0] must be 0");
+  lens.resize(n_sent);
+  for (int i = 0; i < n_sent; ++i) {
+    const int64_t L = off[i + 1] - off[i];
+    if (L <= 0) return fail(NT_E_INVALID, "sentence %d is empty", i);
+    if (L > m.cfg.max_positions) return fail(NT_E_INVALID, "sentence %d has %lld tokens > max_positions %d", i, (long long)L, m.cfg.max_positions);
+    lens[i] = (int)L;
+    const int mt = max_tgt_of(sc, (int)L);
+    if (mt < 1 || mt > m.cfg.max_positions)
+      return fail(NT_E_INVALID, "sentence %d: max target length %d outside [1, max_positions=%d]", i, mt, m.cfg.max_positions);
+  }
+  if (check_ids) {
+    if (!h_src) return fail(NT_E_INVALID, "null h_src");
+    for (int64_t k = 0; k < off[n_sent]; ++k)
+      if (h_src[k] < 0 || h_src[k] >= m.V)
+        return fail(NT_E_INVALID, "token id %d at position %lld outside [0, %d)", h_src[k], (long long)k, m.V);
+  }
+  return NT_OK;
+}
+
+std::vector<int> length_order(const std::vector<int>& lens) {
+  std::vector<int> order(lens.size());
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return lens[a] > lens[b]; });
+  return order;
+}
+
+}  // namespace
+
+// ======================================================================================
+// C ABI
+extern "C" {
+
+const char* nt_last_error(void) { return g_err.c_str(); }
+
+nt_status nt_weights_size(const nt_model_cfg* cfg, size_t* host_floats, size_t* device_bytes) {
+  g_err.clear();
+  NT_TRY(validate_cfg(cfg));
+  const ModelLayout Lo = layout_of(*cfg);
+  if (host_floats) *host_floats = Lo.host_floats;
+  if (device_bytes) *device_bytes = Lo.total;
+  return NT_OK;
+}
+
+nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, size_t host_floats, void* device_buf,
+                          size_t device_bytes, void* stream, nt_model** out) {
+  g_err.clear();
+  NT_TRY(validate_cfg(cfg));
+  if (!host_weights || !device_buf || !out) return fail(NT_E_INVALID, "null argument to nt_load_weights");
+  const ModelLayout Lo = layout_of(*cfg);
+  if (host_floats != Lo.host_floats)
+    return fail(NT_E_INVALID, "weight blob has %zu floats, the model needs %zu", host_floats, Lo.host_floats);
+  if (device_bytes < Lo.total) return fail(NT_E_WORKSPACE, "weight buffer too small: %zu bytes given, %zu required", device_bytes, Lo.total);
+  if ((reinterpret_cast<uintptr_t>(device_buf) & (kAlign - 1)) != 0) return fail(NT_E_INVALID, "weight buffer must be 256-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const DT dt = static_cast<DT>(cfg->dtype);
+  const int d = cfg->d_model, F = cfg->d_ffn, V = cfg->vocab, L = cfg->n_enc, Ld = cfg->n_dec;
+  char* base = static_cast<char*>(device_buf);
+
+  float* staging = nullptr;
+  NT_HIP(hipMalloc((void**)&staging, Lo.host_floats * sizeof(float)));
+  struct Guard {
+    float* p;
+    ~Guard() { if (p) (void)hipFree(p); }
+  } guard{staging};
+  NT_HIP(hipMemcpyAsync(staging, host_weights, Lo.host_floats * sizeof(float), hipMemcpyHostToDevice, s));
+
+  auto vec = [&](size_t dev_off, size_t host_off, size_t n) -> hipError_t {
+    return hipMemcpyAsync(base + dev_off, staging + host_off, n * 4, hipMemcpyDeviceToDevice, s);
+  };
+  auto mat = [&](size_t dev_off, size_t host_off, int in, int outn) -> hipError_t {
+    return nt::pack_transpose(dt, staging + host_off, base + dev_off, in, outn, s);
+  };
+  NT_HIP(nt::pack_convert(dt, staging + Lo.hE, base + Lo.E, (size_t)V * d, s));
+  NT_HIP(vec(Lo.hist_ln, Lo.hhist, (size_t)(L + 1) * 2 * d));
+  NT_HIP(vec(Lo.dlcl, Lo.hdlcl, (size_t)(L + 1) * (L + 2) / 2));
+  for (int i = 0; i < L; ++i) {
+    const auto& D = Lo.enc[i];
+    const auto& Hh = Lo.henc[i];
+    NT_HIP(vec(D.ln1, Hh.ln1, 2 * d));
+    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d));
+    NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
+    NT_HIP(mat(D.Wo, Hh.Wo, d, d));
+    NT_HIP(vec(D.bo, Hh.bo, d));
+    NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
+    NT_HIP(mat(D.W1, Hh.W1, d, F));
+    NT_HIP(vec(D.b1, Hh.b1, F));
+    NT_HIP(mat(D.W2, Hh.W2, F, d));
+    NT_HIP(vec(D.b2, Hh.b2, d));
+  }
+  NT_HIP(vec(Lo.enc_out_ln, Lo.henc_out, 2 * d));
+  const size_t eb = dt == DT::F32 ? 4 : 2;
+  for (int j = 0; j < Ld; ++j) {
+    const auto& D = Lo.dec[j];
+    const auto& Hh = Lo.hdec[j];
+    NT_HIP(vec(D.ln1, Hh.ln1, 2 * d));
+    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d));
+    NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
+    NT_HIP(mat(D.Wo, Hh.Wo, d, d));
+    NT_HIP(vec(D.bo, Hh.bo, d));
+    NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
+    NT_HIP(mat(D.Wq, Hh.Wq, d, d));
+    NT_HIP(vec(D.bq, Hh.bq, d));
+    NT_HIP(mat(D.Woc, Hh.Woc, d, d));
+    NT_HIP(vec(D.boc, Hh.boc, d));
+    NT_HIP(vec(D.ln3, Hh.ln3, 2 * d));
+    NT_HIP(mat(D.W1, Hh.W1, d, F));
+    NT_HIP(vec(D.b1, Hh.b1, F));
+    NT_HIP(mat(D.W2, Hh.W2, F, d));
+    NT_HIP(vec(D.b2, Hh.b2, d));
+    // cross K/V projections of all layers stacked into one [Ld*2d][d] matrix
+    NT_HIP(nt::pack_transpose(dt, staging + Hh.Wkv, base + Lo.Wkv_all + (size_t)j * 2 * d * d * eb, d, 2 * d, s));
+    NT_HIP(vec(Lo.bkv_all + (size_t)j * 2 * d * 4, Hh.bkv, 2 * d));
+  }
+  NT_HIP(vec(Lo.dec_out_ln, Lo.hdec_out, 2 * d));
+
+  // sinusoidal positions, PE(p, 2i) = sin(p / 10000^(2i/d)), PE(p, 2i+1) = cos(same)
+  std::vector<float> pe((size_t)cfg->max_positions * d);
+  for (int pos = 0; pos < cfg->max_positions; ++pos)
+    for (int i = 0; i < d / 2; ++i) {
+      const double ang = pos / std::pow(10000.0, 2.0 * i / d);
+      pe[(size_t)pos * d + 2 * i] = (float)std::sin(ang);
+      pe[(size_t)pos * d + 2 * i + 1] = (float)std::cos(ang);
+    }
+  NT_HIP(hipMemcpyAsync(base + Lo.pe, pe.data(), pe.size() * 4, hipMemcpyHostToDevice, s));
+  NT_HIP(hipStreamSynchronize(s));
+
+  nt_model* m = new nt_model();
+  m->cfg = *cfg;
+  m->dt = dt;
+  m->eb = eb;
+  m->d = d;
+  m->H = cfg->n_heads;
+  m->dh = d / cfg->n_heads;
+  m->F = F;
+  m->L = L;
+  m->Ld = Ld;
+  m->V = V;
+  auto fp = [&](size_t o) { return reinterpret_cast<const float*>(base + o); };
+  m->E = base + Lo.E;
+  m->pe = fp(Lo.pe);
+  m->hist_ln = fp(Lo.hist_ln);
+  m->dlcl = fp(Lo.dlcl);
+  for (int i = 0; i < L; ++i) {
+    const auto& D = Lo.enc[i];
+    m->enc.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.b1), fp(D.b2), base + D.Wqkv, base + D.Wo,
+                      base + D.W1, base + D.W2});
+  }
+  m->enc_out_ln = fp(Lo.enc_out_ln);
+  for (int j = 0; j < Ld; ++j) {
+    const auto& D = Lo.dec[j];
+    m->dec.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.bq), fp(D.boc), fp(D.ln3), fp(D.b1), fp(D.b2),
+                      base + D.Wqkv, base + D.Wo, base + D.Wq, base + D.Woc, base + D.W1, base + D.W2});
+  }
+  m->Wkv_all = base + Lo.Wkv_all;
+  m->bkv_all = fp(Lo.bkv_all);
+  m->dec_out_ln = fp(Lo.dec_out_ln);
+  *out = m;
+  return NT_OK;
+}
+
+void nt_free_model(nt_model* m) { delete m; }
+
+nt_status nt_workspace_size(const nt_model* m, const nt_search_cfg* search, int32_t max_sents, int32_t max_src,
+                            size_t* bytes) {
+  g_err.clear();
+  if (!m || !bytes) return fail(NT_E_INVALID, "null argument to nt_workspace_size");
+  NT_TRY(validate_search(*m, search));
+  if (max_sents <= 0 || max_src <= 0) return fail(NT_E_INVALID, "max_sents and max_src must be > 0");
+  const int Tcap = std::max(1, max_tgt_of(*search, max_src));
+  *bytes = ws_plan(*m, max_sents, max_src, search->beam, Tcap).total;
+  return NT_OK;
+}
+
+nt_status nt_translate_workspace_size(const nt_model* m, const nt_search_cfg* search, const int64_t* h_src_off,
+                                      int32_t n_sent, size_t* bytes) {
+  g_err.clear();
+  if (!m || !bytes) return fail(NT_E_INVALID, "null argument to nt_translate_workspace_size");
+  NT_TRY(validate_search(*m, search));
+  std::vector<int> lens;
+  NT_TRY(validate_sources(*m, *search, nullptr, h_src_off, n_sent, lens, false));
+  const auto order = length_order(lens);
+  size_t need = 0;
+  for (const Batch& b : plan_batches(order, lens, *search))
+    need = std::max(need, ws_plan(*m, b.count, b.S, search->beam, b.Tcap).total);
+  *bytes = need;
+  return NT_OK;
+}
+
+nt_status nt_encode(nt_model* m, const int32_t* d_src, const int32_t* d_len, const int32_t* h_len, int32_t B, int32_t S,
+                    const nt_search_cfg* search, void* d_ws, size_t ws_bytes, void* stream, nt_dec_state** st) {
+  g_err.clear();
+  return encode_impl(m, d_src, d_len, h_len, B, S, search, d_ws, ws_bytes, static_cast<hipStream_t>(stream), st);
+}
+
+nt_status nt_decode_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, int32_t* h_alive, void* stream) {
+  g_err.clear();
+  if (!st) return fail(NT_E_INVALID, "null state");
+  if (st->finished) return fail(NT_E_STATE, "every sentence has finished");
+  if (d_forced && st->K != 1) return fail(NT_E_UNSUPPORTED, "teacher forcing needs beam 1");
+  NT_TRY(run_step(st, d_forced, d_logits, static_cast<hipStream_t>(stream)));
+  if (h_alive) *h_alive = st->n_alive;
+  return NT_OK;
+}
+
+nt_status nt_dec_state_read(nt_dec_state* st, int32_t* h_tokens, int32_t* h_lens, float* h_scores, float* h_token_logp,
+                            void* stream) {
+  g_err.clear();
+  return read_impl(st, h_tokens, h_lens, h_scores, h_token_logp, static_cast<hipStream_t>(stream));
+}
+
+nt_status nt_dec_state_info(const nt_dec_state* st, int32_t* B, int32_t* S, int32_t* beam, int32_t* max_tgt,
+                            int32_t* steps, int32_t* alive) {
+  g_err.clear();
+  if (!st) return fail(NT_E_INVALID, "null state");
+  if (B) *B = st->B;
+  if (S) *S = st->S;
+  if (beam) *beam = st->K;
+  if (max_tgt) *max_tgt = st->Tcap;
+  if (steps) *steps = st->t;
+  if (alive) *alive = st->n_alive;
+  return NT_OK;
+}
+
+nt_status nt_dec_state_encoder_out(nt_dec_state* st, float* h_enc, void* stream) {
+  g_err.clear();
+  if (!st || !h_enc) return fail(NT_E_INVALID, "null argument");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const nt_model& m = *st->m;
+  const size_t n = (size_t)st->B * st->S * m.d;
+  std::vector<char> raw(n * m.eb);
+  NT_HIP(hipMemcpyAsync(raw.data(), st->ws + st->plan.enc_out, raw.size(), hipMemcpyDeviceToHost, s));
+  NT_HIP(hipStreamSynchronize(s));
+  for (size_t i = 0; i < n; ++i) {
+    if (m.dt == DT::F32) {
+      h_enc[i] = reinterpret_cast<const float*>(raw.data())[i];
+    } else if (m.dt == DT::F16) {
+      h_enc[i] = (float)reinterpret_cast<const _Float16*>(raw.data())[i];
+    } else {
+      uint32_t u = (uint32_t)reinterpret_cast<const uint16_t*>(raw.data())[i] << 16;
+      std::memcpy(&h_enc[i], &u, 4);
+    }
+  }
+  return NT_OK;
+}
+
+void nt_free_state(nt_dec_state* st) { free_state(st); }
+
+nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* h_src, const int64_t* h_src_off,
+                       int32_t n_sent, int32_t* h_out, int64_t out_cap, int64_t* h_out_off, float* h_score,
+                       float* h_tok_logp, void* d_ws, size_t ws_bytes, void* stream) {
+  g_err.clear();
+  if (!m || !h_out || !h_out_off || !d_ws) return fail(NT_E_INVALID, "null argument to nt_translate");
+  NT_TRY(validate_search(*m, search));
+  std::vector<int> lens;
+  NT_TRY(validate_sources(*m, *search, h_src, h_src_off, n_sent, lens, true));
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const auto order = length_order(lens);
+  const auto batches = plan_batches(order, lens, *search);
+  size_t need = 0;
+  int maxB = 0, maxBS = 0, maxBT = 0;
+  for (const Batch& b : batches) {
+    need = std::max(need, ws_plan(*m, b.count, b.S, search->beam, b.Tcap).total);
+    maxB = std::max(maxB, b.count);
+    maxBS = std::max(maxBS, b.count * b.S);
+    maxBT = std::max(maxBT, b.count * b.Tcap);
+  }
+  if (ws_bytes < need) return fail(NT_E_WORKSPACE, "workspace too small: %zu bytes given, %zu required", ws_bytes, need);
+
+  // pinned staging for one batch's inputs and outputs
+  struct Pinned {
+    void* p = nullptr;
+    ~Pinned() { if (p) (void)hipHostFree(p); }
+  } pin;
+  const size_t pin_bytes = (size_t)maxBS * 4 + (size_t)maxB * 4 * 3 + (size_t)maxBT * 8;
+  NT_HIP(hipHostMalloc(&pin.p, pin_bytes, hipHostMallocDefault));
+  int* p_src = static_cast<int*>(pin.p);
+  int* p_len = p_src + maxBS;
+  int* p_olen = p_len + maxB;
+  float* p_oscore = reinterpret_cast<float*>(p_olen + maxB);
+  int* p_otok = reinterpret_cast<int*>(p_oscore + maxB);
+  float* p_olp = reinterpret_cast<float*>(p_otok + maxBT);
+
+  std::vector<std::vector<int>> res_tok(n_sent);
+  std::vector<std::vector<float>> res_lp(n_sent);
+  std::vector<float> res_score(n_sent);
+  char* ws = static_cast<char*>(d_ws);
+
+  for (const Batch& bt : batches) {
+    const int B = bt.count, S = bt.S;
+    for (int i = 0; i < B; ++i) {
+      const int sid = order[bt.first + i];
+      const int L = lens[sid];
+      p_len[i] = L;
+      std::memcpy(p_src + (size_t)i * S, h_src + h_src_off[sid], sizeof(int) * L);
+      std::fill(p_src + (size_t)i * S + L, p_src + (size_t)(i + 1) * S, m->cfg.pad_id);
+    }
+    // inputs go straight into the workspace slots nt_encode copies them to
+    const WsPlan plan = ws_plan(*m, B, S, search->beam, bt.Tcap);
+    NT_HIP(hipMemcpyAsync(ws + plan.src, p_src, sizeof(int) * (size_t)B * S, hipMemcpyHostToDevice, s));
+    NT_HIP(hipMemcpyAsync(ws + plan.len, p_len, sizeof(int) * B, hipMemcpyHostToDevice, s));
+    nt_dec_state* st = nullptr;
+    NT_TRY(encode_impl(m, reinterpret_cast<int*>(ws + plan.src), reinterpret_cast<int*>(ws + plan.len), p_len, B, S,
+                       search, d_ws, ws_bytes, s, &st));
+    nt_status r = NT_OK;
+    while (!st->finished && r == NT_OK) r = run_step(st, nullptr, nullptr, s);
+    if (r == NT_OK) r = read_impl(st, p_otok, p_olen, p_oscore, p_olp, s);
+    const int Tcap = st->Tcap;
+    free_state(st);
+    if (r != NT_OK) return r;
+    for (int i = 0; i < B; ++i) {
+      const int sid = order[bt.first + i];
+      res_tok[sid].assign(p_otok + (size_t)i * Tcap, p_otok + (size_t)i * Tcap + p_olen[i]);
+      res_lp[sid].assign(p_olp + (size_t)i * Tcap, p_olp + (size_t)i * Tcap + p_olen[i]);
+      res_score[sid] = p_oscore[i];
+    }
+  }
+
+  int64_t total = 0;
+  for (int i = 0; i < n_sent; ++i) total += (int64_t)res_tok[i].size();
+  if (total > out_cap) return fail(NT_E_INVALID, "out_cap %lld too small: %lld output tokens", (long long)out_cap, (long long)total);
+  int64_t o = 0;
+  h_out_off[0] = 0;
+  for (int i = 0; i < n_sent; ++i) {
+    std::copy(res_tok[i].begin(), res_tok[i].end(), h_out + o);
+    if (h_tok_logp) std::copy(res_lp[i].begin(), res_lp[i].end(), h_tok_logp + o);
+    o += (int64_t)res_tok[i].size();
+    h_out_off[i + 1] = o;
+    if (h_score) h_score[i] = res_score[i];
+  }
+  return NT_OK;
+}
+
+nt_status nt_prof_enable(uint32_t class_mask) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_mask = class_mask & ((1u << NT_K_COUNT) - 1);
+  return NT_OK;
+}
+
+nt_status nt_prof_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto& r : g_prof) {
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+  }
+  g_prof.clear();
+  return NT_OK;
+}
+
+nt_status nt_prof_get(int32_t kernel_class, int64_t* launches, double* total_ms, double* alg_bytes, double* alg_flops) {
+  g_err.clear();
+  if (kernel_class < 0 || kernel_class >= NT_K_COUNT) return fail(NT_E_INVALID, "kernel class %d", kernel_class);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  int64_t n = 0;
+  double ms = 0, by = 0, fl = 0;
+  for (auto& r : g_prof) {
+    if (r.cls != kernel_class) continue;
+    NT_HIP(hipEventSynchronize(r.b));
+    float e = 0.f;
+    NT_HIP(hipEventElapsedTime(&e, r.a, r.b));
+    ++n;
+    ms += e;
+    by += r.bytes;
+    fl += r.flops;
+  }
+  if (launches) *launches = n;
+  if (total_ms) *total_ms = ms;
+  if (alg_bytes) *alg_bytes = by;
+  if (alg_flops) *alg_flops = fl;
+  return NT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,481 @@
+// Search kernels: greedy and beam selection over the fp32 logits, the per-sentence
+// search update, batch compaction and the final backtrack.
+//
+// Greedy (Sec. 4.4): argmax of the logits (ties -> lowest ID) in the same pass as an
+// online log-sum-exp, so the chosen token's log-prob is logit - LSE without a
+// log_softmax over the vocabulary (Sec. 4.4 drops it for greedy search).
+// Beam: each live row keeps its 2K largest logits and its LSE; per sentence the K*2K
+// candidates c = score_h + logit - LSE_h are ranked by (c desc, h*V + w asc), the first
+// 2K walked: EOS candidates finish (score c / ((5+n)/6)^alpha, n tokens incl. EOS), the
+// first K others form the next beam.  A sentence stops once its best finished score is
+// at least every live score (Sec. 4.1 "Faster Beam Search") or at its length limit.
+// Finished sentences leave the batch by compaction (Sec. 4.1 "Batch Pruning"): the
+// list of live sentences is rebuilt and every per-row kernel indexes through it, so
+// no cache row is ever copied.
+#include <limits.h>
+
+#include "nt_common.h"
+#include "nt_kernels.h"
+
+namespace nt {
+namespace {
+
+constexpr int SEL_THREADS = 256;
+
+struct MaxSum {
+  float m, s;
+};
+__device__ __forceinline__ MaxSum ms_merge(MaxSum a, MaxSum b) {
+  if (b.m == -INFINITY) return a;
+  if (a.m == -INFINITY) return b;
+  const float m = fmaxf(a.m, b.m);
+  return {m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
+}
+// (value desc, index asc)
+__device__ __forceinline__ bool better(float v1, int i1, float v2, int i2) {
+  return v1 > v2 || (v1 == v2 && i1 < i2);
+}
+
+// Per-thread online max/sum and argmax over a row; returns block-wide results in
+// every thread.  Elements are visited in increasing index per thread.
+__device__ void row_lse_argmax(const float* __restrict__ x, int V, float& lse, float& best, int& bidx) {
+  __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave], sb[SEL_THREADS / kWave];
+  __shared__ int si[SEL_THREADS / kWave];
+  const int tid = threadIdx.x;
+  MaxSum acc{-INFINITY, 0.f};
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  const bool vec = (V % 4) == 0 && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
+  if (vec) {
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    for (int i = tid; i < V / 4; i += SEL_THREADS) {
+      const float4 v = x4[i];
+      const float mx = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
+      if (mx > acc.m) {
+        acc.s = acc.m == -INFINITY ? 0.f : acc.s * expf(acc.m - mx);
+        acc.m = mx;
+      }
+      acc.s += expf(v.x - acc.m) + expf(v.y - acc.m) + expf(v.z - acc.m) + expf(v.w - acc.m);
+      if (v.x > bv) { bv = v.x; bi = 4 * i; }
+      if (v.y > bv) { bv = v.y; bi = 4 * i + 1; }
+      if (v.z > bv) { bv = v.z; bi = 4 * i + 2; }
+      if (v.w > bv) { bv = v.w; bi = 4 * i + 3; }
+    }
+  } else {
+    for (int i = tid; i < V; i += SEL_THREADS) {
+      const float v = x[i];
+      if (v > acc.m) {
+        acc.s = acc.m == -INFINITY ? 0.f : acc.s * expf(acc.m - v);
+        acc.m = v;
+      }
+      acc.s += expf(v - acc.m);
+      if (v > bv) { bv = v; bi = i; }
+    }
+  }
+  // wave reduction
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    MaxSum other{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)};
+    acc = ms_merge(acc, other);
+    const float ov = __shfl_xor(bv, o, kWave);
+    const int oi = __shfl_xor(bi, o, kWave);
+    if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+  }
+  const int wave = tid / kWave, lane = tid % kWave;
+  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; sb[wave] = bv; si[wave] = bi; }
+  __syncthreads();
+  MaxSum tot{sm[0], ss[0]};
+  float fb = sb[0];
+  int fi = si[0];
+#pragma unroll
+  for (int w = 1; w < SEL_THREADS / kWave; ++w) {
+    tot = ms_merge(tot, MaxSum{sm[w], ss[w]});
+    if (better(sb[w], si[w], fb, fi)) { fb = sb[w]; fi = si[w]; }
+  }
+  lse = tot.m + logf(tot.s);
+  best = fb;
+  bidx = fi;
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __restrict__ logits,
+                                                             const int* __restrict__ forced, SearchState st, int t) {
+  const int r = blockIdx.x;
+  const int b = st.sent_list[r];
+  const int p = b;                      // beam 1: physical row = sentence
+  const float* x = logits + (size_t)r * st.V;
+  float lse, best;
+  int bidx;
+  row_lse_argmax(x, st.V, lse, best, bidx);
+  if (threadIdx.x != 0 || st.done[b]) return;
+  const int R = st.B;
+  int tok = forced ? forced[p] : bidx;
+  if (tok < 0 || tok >= st.V) tok = st.eos;   // out-of-range forced ID or an all-NaN row: end the sentence
+  const float lp = x[tok] - lse;
+  st.score[p] += lp;
+  if (tok == st.eos) {
+    st.done[b] = 1;
+    st.best_score[b] = st.score[p];
+    st.best_raw[b] = st.score[p];
+    st.best_nout[b] = t;
+    st.best_step[b] = t - 1;
+    st.best_row[b] = p;
+    return;
+  }
+  st.tok_hist[(size_t)t * R + p] = tok;
+  st.lp_hist[(size_t)t * R + p] = lp;
+  st.cur_tok[p] = tok;
+  if (t + 1 >= st.maxlen[b]) {
+    st.done[b] = 1;
+    st.best_score[b] = st.score[p];
+    st.best_raw[b] = st.score[p];
+    st.best_nout[b] = t + 1;
+    st.best_step[b] = t;
+    st.best_row[b] = p;
+  }
+}
+
+// ---- beam: per-row LSE and top-2K logits -----------------------------------------------
+template <int K2>
+__device__ __forceinline__ void list_insert(float (&v)[K2], int (&ix)[K2], float x, int i) {
+  if (!(x > v[K2 - 1])) return;       // equal values keep the earlier (lower) index
+  v[K2 - 1] = x;
+  ix[K2 - 1] = i;
+#pragma unroll
+  for (int j = K2 - 1; j > 0; --j) {
+    if (v[j] > v[j - 1]) {
+      const float tv = v[j]; v[j] = v[j - 1]; v[j - 1] = tv;
+      const int ti = ix[j]; ix[j] = ix[j - 1]; ix[j - 1] = ti;
+    }
+  }
+}
+
+template <int K2>
+__global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* __restrict__ logits, int V, int k2,
+                                                                  float* __restrict__ topv, int* __restrict__ topi,
+                                                                  float* __restrict__ lse_out) {
+  __shared__ float wv[SEL_THREADS / kWave][K2];
+  __shared__ int wi[SEL_THREADS / kWave][K2];
+  const int r = blockIdx.x;
+  const float* x = logits + (size_t)r * V;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+
+  float lse, best;
+  int bidx;
+  row_lse_argmax(x, V, lse, best, bidx);
+
+  float v[K2];
+  int ix[K2];
+#pragma unroll
+  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
+  for (int i = tid; i < V; i += SEL_THREADS) list_insert<K2>(v, ix, x[i], i);
+
+  // each wave merges its 64 lists: K2 rounds of a wave-wide (value desc, index asc) argmax;
+  // the winning lane drops its head
+  for (int round = 0; round < K2; ++round) {
+    float bv = v[0];
+    int bi = ix[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (lane == 0) { wv[wave][round] = bv; wi[wave][round] = bi; }
+    if (ix[0] == bi && v[0] == bv && bi != INT_MAX) {
+#pragma unroll
+      for (int j = 0; j < K2 - 1; ++j) { v[j] = v[j + 1]; ix[j] = ix[j + 1]; }
+      v[K2 - 1] = -INFINITY;
+      ix[K2 - 1] = INT_MAX;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int head[SEL_THREADS / kWave] = {0, 0, 0, 0};
+    for (int j = 0; j < k2; ++j) {
+      int w = 0;
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+      for (int q = 0; q < SEL_THREADS / kWave; ++q) {
+        if (head[q] >= K2 || wi[q][head[q]] == INT_MAX) continue;     // list exhausted
+        if (bi == INT_MAX || better(wv[q][head[q]], wi[q][head[q]], bv, bi)) {
+          bv = wv[q][head[q]]; bi = wi[q][head[q]]; w = q;
+        }
+      }
+      head[w]++;
+      topv[(size_t)r * k2 + j] = bv;
+      topi[(size_t)r * k2 + j] = bi;
+    }
+    lse_out[r] = lse;
+  }
+}
+
+// ---- beam: per-sentence update (one wave per live sentence) ----------------------------
+constexpr int MAXC = 8;       // candidates per lane: K * 2K <= 512 = 64 * 8
+
+__global__ __launch_bounds__(256) void beam_update_kernel(const float* __restrict__ topv,
+                                                          const int* __restrict__ topi,
+                                                          const float* __restrict__ lse, SearchState st, int t) {
+  __shared__ float sel_c[4][32], sel_lp[4][32];
+  __shared__ int sel_key[4][32];
+  __shared__ int nk_par[4][16], nk_cnt[4];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int bl = blockIdx.x * 4 + wave;
+  if (bl >= st.n_live) return;                      // whole wave leaves; no block barrier below
+  const int b = st.sent_list[bl];
+  if (st.done[b]) return;
+  const int K = st.beam, K2 = 2 * K, V = st.V, n = t + 1;
+  const int ncand = K * K2;
+
+  float cv[MAXC], clp[MAXC];
+  int ck[MAXC];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int q = lane + c * kWave;
+    cv[c] = -INFINITY;
+    clp[c] = 0.f;
+    ck[c] = INT_MAX;
+    if (q < ncand) {
+      const int k = q / K2, i = q - k * K2;
+      const int r = bl * K + k, p = b * K + k;
+      const float v = topv[(size_t)r * K2 + i];
+      const int w = topi[(size_t)r * K2 + i];
+      if (w == INT_MAX) continue;           // fewer than 2K words in the vocabulary
+      const float lp = v - lse[r];
+      cv[c] = st.score[p] + lp;
+      clp[c] = lp;
+      ck[c] = k * V + w;
+    }
+  }
+  // top-2K by (c desc, key asc): 2K rounds of a wave argmax; the winner is consumed
+  for (int j = 0; j < K2; ++j) {
+    float bv = -INFINITY, blp = 0.f;
+    int bk = INT_MAX;
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (ck[c] != INT_MAX && (better(cv[c], ck[c], bv, bk) || bk == INT_MAX)) { bv = cv[c]; bk = ck[c]; blp = clp[c]; }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int ok = __shfl_xor(bk, o, kWave);
+      const float olp = __shfl_xor(blp, o, kWave);
+      if (ok != INT_MAX && (bk == INT_MAX || better(ov, ok, bv, bk))) { bv = ov; bk = ok; blp = olp; }
+    }
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c)
+      if (ck[c] == bk) ck[c] = INT_MAX;     // keys are unique: exactly one lane consumes it
+    if (lane == 0) { sel_c[wave][j] = bv; sel_key[wave][j] = bk; sel_lp[wave][j] = blp; }
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+
+  const size_t R = (size_t)st.B * K;
+  if (lane == 0) {
+    const float lpn = powf((5.0f + (float)n) / 6.0f, st.alpha);
+    int nk = 0;
+    float nk_score[16];
+    int nk_tok[16];
+    float nk_lp[16];
+    for (int j = 0; j < K2; ++j) {
+      const int key = sel_key[wave][j];
+      if (key == INT_MAX) continue;
+      const float c = sel_c[wave][j];
+      const int k = key / V, w = key - k * V;
+      const int ppar = b * K + k;
+      if (w == st.eos) {
+        const float s = c / lpn;
+        if (st.best_nout[b] < 0 || s > st.best_score[b]) {
+          st.best_score[b] = s;
+          st.best_raw[b] = c;
+          st.best_step[b] = t - 1;
+          st.best_row[b] = ppar;
+          st.best_nout[b] = t;
+        }
+      } else if (nk < K) {
+        nk_score[nk] = c;
+        nk_tok[nk] = w;
+        nk_lp[nk] = sel_lp[wave][j];
+        nk_par[wave][nk] = ppar;
+        ++nk;
+      }
+    }
+    float mx = -INFINITY;
+    for (int k = 0; k < K; ++k) {
+      const int p = b * K + k;
+      if (k < nk) {
+        st.score[p] = nk_score[k];
+        st.cur_tok[p] = nk_tok[k];
+        st.tok_hist[(size_t)t * R + p] = nk_tok[k];
+        st.par_hist[(size_t)t * R + p] = nk_par[wave][k];
+        st.lp_hist[(size_t)t * R + p] = nk_lp[k];
+        mx = fmaxf(mx, nk_score[k]);
+      } else {
+        st.score[p] = -INFINITY;
+      }
+    }
+    int done = 0;
+    if (n >= st.maxlen[b]) {
+      for (int k = 0; k < nk; ++k) {
+        const float s = nk_score[k] / lpn;
+        if (st.best_nout[b] < 0 || s > st.best_score[b]) {
+          st.best_score[b] = s;
+          st.best_raw[b] = nk_score[k];
+          st.best_step[b] = t;
+          st.best_row[b] = b * K + k;
+          st.best_nout[b] = t + 1;
+        }
+      }
+      done = 1;
+    } else if (st.early_stop && st.best_nout[b] >= 0 && st.best_score[b] >= mx / lpn) {
+      done = 1;
+    } else if (nk == 0) {
+      done = 1;
+    }
+    st.done[b] = done;
+    nk_cnt[wave] = done ? 0 : nk;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  // ancestor table of the new beam: slot s < t lives where the parent's slot s lives;
+  // slot t is the parent's own row (written this step)
+  const int nk = nk_cnt[wave];
+  for (int k = 0; k < nk; ++k) {
+    const int p = b * K + k, par = nk_par[wave][k];
+    for (int s = lane; s <= t; s += kWave)
+      st.anc_next[(size_t)p * st.Tcap + s] = s < t ? st.anc_cur[(size_t)par * st.Tcap + s] : par;
+  }
+}
+
+// ---- compaction: order-preserving filter of the live list ---------------------------------
+__global__ __launch_bounds__(1024) void compact_kernel(const int* __restrict__ list, int n,
+                                                       const int* __restrict__ done, int* __restrict__ new_list,
+                                                       int* __restrict__ n_out) {
+  __shared__ int wsum[1024 / kWave];
+  __shared__ int base;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  if (tid == 0) base = 0;
+  __syncthreads();
+  for (int c0 = 0; c0 < n; c0 += 1024) {
+    const int i = c0 + tid;
+    const int b = i < n ? list[i] : 0;
+    const int keep = (i < n && !done[b]) ? 1 : 0;
+    // inclusive wave scan
+    int x = keep;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int y = __shfl_up(x, o, kWave);
+      if (lane >= o) x += y;
+    }
+    if (lane == kWave - 1) wsum[wave] = x;
+    __syncthreads();
+    int off = base;
+    for (int w = 0; w < wave; ++w) off += wsum[w];
+    if (keep) new_list[off + x - 1] = b;
+    __syncthreads();
+    if (tid == 0) {
+      int tot = 0;
+      for (int w = 0; w < 1024 / kWave; ++w) tot += wsum[w];
+      base += tot;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) *n_out = base;
+}
+
+__global__ void finalize_kernel(SearchState st, int* __restrict__ out_tok, float* __restrict__ out_lp,
+                                int* __restrict__ out_len, float* __restrict__ out_score) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= st.B) return;
+  const size_t R = (size_t)st.B * st.beam;
+  const int n = st.best_nout[b];
+  int s = st.best_step[b], p = st.best_row[b];
+  for (int i = n - 1; i >= 0; --i, --s) {
+    out_tok[(size_t)b * st.Tcap + i] = st.tok_hist[(size_t)s * R + p];
+    out_lp[(size_t)b * st.Tcap + i] = st.lp_hist[(size_t)s * R + p];
+    if (st.beam > 1) p = st.par_hist[(size_t)s * R + p];
+  }
+  out_len[b] = n < 0 ? 0 : n;
+  out_score[b] = st.best_score[b];
+}
+
+__global__ void init_kernel(SearchState st, int* __restrict__ list, int bos) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int R = st.B * st.beam;
+  if (i < R) {
+    st.score[i] = (i % st.beam == 0) ? 0.f : -INFINITY;
+    st.cur_tok[i] = bos;
+  }
+  if (i < st.B) {
+    st.done[i] = 0;
+    st.best_score[i] = -INFINITY;
+    st.best_raw[i] = -INFINITY;
+    st.best_step[i] = -1;
+    st.best_row[i] = -1;
+    st.best_nout[i] = -1;
+    list[i] = i;
+  }
+}
+
+__global__ void scatter_logits_kernel(const float* __restrict__ src, const int* __restrict__ sent_list, int beam,
+                                      int rows, int V, float* __restrict__ dst) {
+  const int r = blockIdx.y;
+  const int p = sent_list[r / beam] * beam + r % beam;
+  for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x)
+    dst[(size_t)p * V + v] = src[(size_t)r * V + v];
+}
+
+}  // namespace
+
+hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, int t, hipStream_t s) {
+  if (st.n_live <= 0) return hipSuccess;
+  hipLaunchKernelGGL(greedy_kernel, dim3(st.n_live), dim3(SEL_THREADS), 0, s, logits, forced, st, t);
+  return hipGetLastError();
+}
+
+hipError_t beam_select(const float* logits, int rows, int V, int k2, float* topv, int* topi, float* lse,
+                       hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+#define NT_SEL(K2) hipLaunchKernelGGL(beam_select_kernel<K2>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, V, k2, topv, topi, lse)
+  if (k2 <= 4) NT_SEL(4);
+  else if (k2 <= 8) NT_SEL(8);
+  else if (k2 <= 16) NT_SEL(16);
+  else if (k2 <= 32) NT_SEL(32);
+  else return hipErrorInvalidValue;
+#undef NT_SEL
+  return hipGetLastError();
+}
+
+hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, int t,
+                       hipStream_t s) {
+  if (st.n_live <= 0) return hipSuccess;
+  if (st.beam * 2 * st.beam > MAXC * kWave || st.beam > 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(beam_update_kernel, dim3((st.n_live + 3) / 4), dim3(256), 0, s, topv, topi, lse, st, t);
+  return hipGetLastError();
+}
+
+hipError_t compact(const int* list, int n, const int* done, int* new_list, int* n_out, hipStream_t s) {
+  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, list, n, done, new_list, n_out);
+  return hipGetLastError();
+}
+
+hipError_t finalize(const SearchState& st, int* out_tok, float* out_lp, int* out_len, float* out_score,
+                    hipStream_t s) {
+  hipLaunchKernelGGL(finalize_kernel, dim3((st.B + 127) / 128), dim3(128), 0, s, st, out_tok, out_lp, out_len,
+                     out_score);
+  return hipGetLastError();
+}
+
+hipError_t search_init(const SearchState& st, int* list, int bos, hipStream_t s) {
+  const int n = st.B * st.beam;
+  hipLaunchKernelGGL(init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, st, list, bos);
+  return hipGetLastError();
+}
+
+hipError_t scatter_logits(const float* logits, const int* sent_list, int beam, int rows, int V, float* dst,
+                          hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(scatter_logits_kernel, dim3((V + 255) / 256 < 64 ? (V + 255) / 256 : 64, rows), dim3(256), 0,
+                     s, logits, sent_list, beam, rows, V, dst);
+  return hipGetLastError();
+}
+
+}  // namespace nt

@@ -1,0 +1,83 @@
+"""Host-only checks of the C ABI: the library loads without a GPU, exports every entry
+point the header declares, and validates its arguments before touching a device."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def nt():
+    from paper_2109_08008_amd import nt as _nt
+    if not os.path.exists(_nt.LIB_PATH):
+        from paper_2109_08008_amd.build import build_library
+        build_library()
+    _nt.load_library()
+    return _nt
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "nt.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(nt_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_function_is_exported(nt):
+    declared = header_functions()
+    assert len(declared) >= 16
+    lib = nt.load_library()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(nt.EXPORTS) == declared
+
+
+def test_struct_layouts_match_header(nt):
+    import ctypes
+    assert ctypes.sizeof(nt.nt_model_cfg) == 13 * 4
+    assert ctypes.sizeof(nt.nt_search_cfg) == 8 * 4
+
+
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_weights_size_matches_canonical_blob(nt, name):
+    w = synth.WORKLOADS[name]
+    for dt in ("f32", "f16", "bf16"):
+        hf, db = nt.nt_weights_size(nt.model_cfg(w.model, dt))
+        assert hf == synth.blob_size(w.model)
+        elem = 4 if dt == "f32" else 2
+        mats = sum(e.size for e in synth.weight_layout(w.model) if e.name == "E" or ".W_" in e.name)
+        assert db >= mats * elem
+
+
+@pytest.mark.parametrize("shape,code", [
+    (synth.ModelShape(100, 4, 256, 1, 1, 50), 2),        # d % 64
+    (synth.ModelShape(128, 8, 256, 1, 1, 50), 2),        # head size 16
+    (synth.ModelShape(128, 4, 100, 1, 1, 50), 2),        # d_ffn % 64
+    (synth.ModelShape(128, 4, 256, 1, 0, 50), 1),        # no decoder layer
+    (synth.ModelShape(128, 4, 256, 1, 1, 3), 1),         # vocab without a word
+    (synth.ModelShape(128, 4, 256, 1, 1, 50, max_positions=2048), 2),
+])
+def test_invalid_configs_are_rejected(nt, shape, code):
+    with pytest.raises(nt.NTError) as e:
+        nt.nt_weights_size(nt.model_cfg(shape))
+    assert e.value.status == code
+    assert e.value.message
+    assert nt.load_library().nt_last_error().decode() == e.value.message
+
+
+def test_null_arguments_are_errors_not_crashes(nt):
+    import ctypes
+    lib = nt.load_library()
+    assert lib.nt_weights_size(None, None, None) == nt.NT_E_INVALID
+    assert lib.nt_translate(None, None, None, None, 0, None, 0, None, None, None, None, 0, None) == nt.NT_E_INVALID
+    assert lib.nt_decode_step(None, None, None, None, None) == nt.NT_E_INVALID
+    assert lib.nt_dec_state_info(None, *([None] * 6)) == nt.NT_E_INVALID
+    assert lib.nt_prof_get(99, None, None, None, None) == nt.NT_E_INVALID
+    n = ctypes.c_int64()
+    assert lib.nt_prof_get(0, ctypes.byref(n), None, None, None) == nt.NT_OK
+    lib.nt_free_state(None)
+    lib.nt_free_model(None)

@@ -1,0 +1,166 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Tolerances: fp32 logits <= 1e-3 max abs and identical token IDs (near-tie protocol);
+fp16 teacher-forced logits <= 5e-2 max abs and per-token log-probs of the returned
+hypothesis <= 1e-2; bf16 (8 mantissa bits against fp16's 11, so 8x the rounding
+error) logits <= 0.4.  The oracle always runs in fp64 on the weights as the GPU stores
+them (matrices rounded to the 16-bit type).
+"""
+import numpy as np
+import pytest
+
+import synth
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+LOGIT_TOL = {"f32": 1e-3, "f16": 5e-2, "bf16": 0.4}
+ENC_TOL = {"f32": 1e-4, "f16": 3e-2, "bf16": 0.25}
+
+SHAPES = {
+    "d64": synth.ModelShape(64, 2, 256, 2, 1, 101),
+    "d128": synth.ModelShape(128, 4, 512, 3, 2, 203),
+    "d256": synth.ModelShape(256, 4, 1024, 2, 1, 517),
+}
+
+
+def _sentences(n, lo, hi, V, seed):
+    ids, offs = synth.make_sentences(synth.DataSetup(n, "uniform", lo, hi, "uniform"), V, seed=seed)
+    return synth.sentence_list(ids, offs), ids, offs
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_encoder_output(name, dtype):
+    shape = SHAPES[name]
+    blob = synth.make_weights(shape, seed=11, lively=True)
+    srcs, _, _ = _sentences(12, 1, 23, shape.vocab, seed=3)
+    model = G.new_model(shape, blob, dtype)
+    st, keep = G.gpu_encode(model, srcs, synth.SearchSetup(beam=1, max_len_b=4))
+    from paper_2109_08008_amd import nt
+    try:
+        enc = nt.nt_dec_state_encoder_out(st, shape.d_model)
+    finally:
+        nt.nt_free_state(st)
+    om = G.oracle_model(shape, blob, dtype)
+    err = 0.0
+    for b, s in enumerate(srcs):
+        ref = om.encode(s)
+        err = max(err, float(np.abs(enc[b, :len(s)] - ref).max()))
+    print(f"{name} {dtype}: encoder max abs err {err:.3g}")
+    assert err <= ENC_TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_teacher_forced_logits(name, dtype):
+    shape = SHAPES[name]
+    blob = synth.make_weights(shape, seed=12, lively=True)
+    srcs, _, _ = _sentences(9, 1, 30, shape.vocab, seed=4)
+    rng = np.random.default_rng(5)
+    tgts = [list(rng.integers(3, shape.vocab, size=int(rng.integers(0, 12)))) for _ in srcs]
+    model = G.new_model(shape, blob, dtype)
+    got, scores, logp = G.gpu_teacher_forced(model, srcs, tgts, shape.vocab)
+    om = G.oracle_model(shape, blob, dtype)
+    err = 0.0
+    for b, (s, tg) in enumerate(zip(srcs, tgts)):
+        ref = om.teacher_forced_logits(s, tg)
+        err = max(err, float(np.abs(got[b] - ref).max()))
+        # the recorded per-token log-probs are the forced tokens' log_softmax values
+        ref_lp = ref - np.log(np.exp(ref - ref.max(1, keepdims=True)).sum(1, keepdims=True)) - ref.max(1, keepdims=True)
+        want = [ref_lp[t, tg[t]] for t in range(len(tg))]
+        assert np.abs(np.asarray(logp[b]) - want).max(initial=0) <= 10 * LOGIT_TOL[dtype]
+        full = sum(want) + ref_lp[len(tg), synth.EOS_ID]
+        assert abs(scores[b] - full) <= 10 * LOGIT_TOL[dtype] * (len(tg) + 1)
+    print(f"{name} {dtype}: teacher-forced logits max abs err {err:.3g}")
+    assert err <= LOGIT_TOL[dtype]
+
+
+def test_tiny_greedy_fp32_token_ids():
+    w = synth.WORKLOADS["tiny"]
+    blob = synth.make_weights(w.model, lively=True)
+    ids, offs = synth.make_sentences(w.data, w.model.vocab)
+    srcs = synth.sentence_list(ids, offs)
+    model = G.new_model(w.model, blob, "f32")
+    toks, scores, _ = model.translate(ids, offs, w.search)
+    om = G.oracle_model(w.model, blob, "f32")
+    import oracle
+    ties = 0
+    for s, tk, sc in zip(srcs, toks, scores):
+        ties += G.compare_greedy_ids(om, s, tk, 24)
+        ref = oracle.translate(om, s, w.search)
+        if list(ref.tokens) == list(tk):
+            assert abs(ref.score - sc) <= 1e-3
+    print("near-ties:", ties, "lengths:", [len(t) for t in toks])
+    assert ties <= 1
+
+
+@pytest.mark.parametrize("alpha,early", [(0.0, 1), (0.6, 1), (0.6, 0)])
+def test_beam_fp32_token_ids(alpha, early):
+    import oracle
+    shape = SHAPES["d128"]
+    blob = synth.make_weights(shape, seed=21, lively=True, eos_boost=4.0)
+    srcs, ids, offs = _sentences(10, 2, 20, shape.vocab, seed=6)
+    search = synth.SearchSetup(beam=4, len_penalty=alpha, max_len_a=1.0, max_len_b=6, early_stop=early)
+    model = G.new_model(shape, blob, "f32")
+    toks, scores, logp = model.translate(ids, offs, search)
+    om = G.oracle_model(shape, blob, "f32")
+    for s, tk, sc, lp in zip(srcs, toks, scores, logp):
+        ref = oracle.translate(om, s, search)
+        assert list(tk) == list(ref.tokens)
+        assert abs(sc - ref.score) <= 1e-3
+        np.testing.assert_allclose(lp, ref.tok_logp, atol=1e-3)
+    print("lengths:", [len(t) for t in toks])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("beam", [1, 4])
+def test_batching_and_pruning_do_not_change_results(dtype, beam):
+    shape = SHAPES["d128"]
+    blob = synth.make_weights(shape, seed=31, lively=True, eos_boost=4.0)
+    srcs, ids, offs = _sentences(24, 1, 30, shape.vocab, seed=7)
+    model = G.new_model(shape, blob, dtype)
+    base = synth.SearchSetup(beam=beam, len_penalty=0.6, max_len_a=1.5, max_len_b=5, token_budget=8192, prune=1)
+    ref_t, ref_s, ref_lp = model.translate(ids, offs, base)
+    assert any(len(t) < synth.max_target_len(base, len(s)) for t, s in zip(ref_t, srcs)), "nothing finished early"
+    for kw in [dict(prune=0), dict(token_budget=64), dict(token_budget=0, max_batch_sents=1),
+               dict(token_budget=16384, max_batch_sents=5)]:
+        t, s, lp = model.translate(ids, offs, synth.replace(base, **kw))
+        for a, b in zip(ref_t, t):
+            np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(ref_s, s)
+        for a, b in zip(ref_lp, lp):
+            np.testing.assert_array_equal(a, b)
+
+
+def test_fp16_translation_logprobs_within_tolerance():
+    shape = SHAPES["d256"]
+    blob = synth.make_weights(shape, seed=41, lively=True, eos_boost=4.0)
+    srcs, ids, offs = _sentences(10, 3, 25, shape.vocab, seed=8)
+    search = synth.SearchSetup(beam=4, len_penalty=0.6, max_len_a=1.5, max_len_b=5)
+    model = G.new_model(shape, blob, "f16")
+    toks, scores, logp = model.translate(ids, offs, search)
+    om = G.oracle_model(shape, blob, "f16")
+    worst = 0.0
+    for s, tk, lp in zip(srcs, toks, logp):
+        ref = om.teacher_forced_logits(s, list(tk))
+        lse = np.log(np.exp(ref - ref.max(1, keepdims=True)).sum(1)) + ref.max(1)
+        want = np.array([ref[t, tk[t]] - lse[t] for t in range(len(tk))])
+        if len(tk):
+            worst = max(worst, float(np.abs(lp - want).max()))
+    print("fp16 per-token log-prob max abs err", worst)
+    assert worst <= 1e-2
+
+
+def test_long_and_single_token_sentences():
+    """Attention over several 64-key chunks (S = 150) next to one-token sentences."""
+    shape = SHAPES["d128"]
+    blob = synth.make_weights(shape, seed=51, lively=True)
+    rng = np.random.default_rng(9)
+    srcs = [list(rng.integers(4, shape.vocab, size=n)) for n in (150, 1, 77, 1, 64, 65)]
+    tgts = [list(rng.integers(3, shape.vocab, size=4)) for _ in srcs]
+    model = G.new_model(shape, blob, "f32")
+    got, _, _ = G.gpu_teacher_forced(model, srcs, tgts, shape.vocab)
+    om = G.oracle_model(shape, blob, "f32")
+    for b, (s, tg) in enumerate(zip(srcs, tgts)):
+        np.testing.assert_allclose(got[b], om.teacher_forced_logits(s, tg), atol=1e-3)
