@@ -1,0 +1,201 @@
+#!/usr/bin/env python3
+"""Throughput benchmark: target tokens/s of whole-job batched translation on one MI355X.
+
+One step = one nt_translate call over the whole synthetic workload (sorting, dynamic
+batching, DLCL encoder, cached decoder steps, search, pruning, results back in host
+memory), with inputs and weights generated beforehand.  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload base-6-6]
+
+The line carries a roofline entry for the dominant kernel class, timed with HIP events
+on the launch stream inside the timed region, and the CPU oracle's throughput on a
+bounded sample of the same workload (the oracle as written, one process per core).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import synth  # noqa: E402
+
+PEAK = {  # MI355X published peaks (dense)
+    "hbm_GBps": 8000.0,
+    "mfma_TFLOPs": {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3},
+}
+GEMM_CLASSES = (0, 1, 2)
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="base-6-6", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work for the oracle sample")
+    ap.add_argument("--cpu-procs", type=int, default=0, help="oracle processes (0: min(16, cores))")
+    return ap.parse_args()
+
+
+def roofline_entry(cls: int, prof: dict, dtype: str) -> dict:
+    """Roofline of one kernel class from its event timings and algorithmic work."""
+    from paper_2109_08008_amd import nt
+    n = max(prof["launches"], 1)
+    sec = prof["ms"] / 1e3
+    intensity = prof["flops"] / max(prof["bytes"], 1.0)
+    ridge = PEAK["mfma_TFLOPs"][dtype] * 1e12 / (PEAK["hbm_GBps"] * 1e9)
+    if cls in GEMM_CLASSES and intensity >= ridge:
+        achieved = prof["flops"] / sec / 1e12
+        peak = PEAK["mfma_TFLOPs"][dtype]
+        bound, unit = "mfma", "TFLOP/s"
+    else:
+        achieved = prof["bytes"] / sec / 1e9
+        peak = PEAK["hbm_GBps"]
+        bound, unit = "hbm", "GB/s"
+    return {
+        "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+        "frac": round(achieved / peak, 4), "traffic": None,
+        "kernel": nt.KERNEL_CLASSES[cls], "launches": prof["launches"],
+        "avg_us": round(prof["ms"] * 1e3 / n, 2),
+        "alg_bytes_per_launch": round(prof["bytes"] / n), "alg_flops_per_launch": round(prof["flops"] / n),
+    }
+
+
+# ---- CPU oracle baseline ------------------------------------------------------------------
+_ORACLE = {}
+
+
+def _oracle_worker(idx):
+    from threadpoolctl import threadpool_limits
+    import oracle
+    with threadpool_limits(limits=1):
+        src = _ORACLE["srcs"][idx]
+        h = oracle.translate(_ORACLE["model"], src, _ORACLE["search"])
+        return len(h.tokens)
+
+
+def cpu_baseline(w: synth.Workload, blob, ids, offs, seconds: float, procs: int) -> dict:
+    """The fp32 oracle on a length-stratified sample, split over processes (one BLAS
+    thread each) the way the paper splits CPU decoding by lines."""
+    import multiprocessing as mp
+    import oracle
+    from threadpoolctl import threadpool_limits
+
+    P = procs or min(16, os.cpu_count() or 1)
+    srcs = synth.sentence_list(ids, offs)
+    model = oracle.OracleModel(w.model, blob, np.float32)
+    _ORACLE.update(model=model, srcs=srcs, search=w.search)
+    # calibrate on the median-length sentence, then size the sample to ~`seconds` of work
+    order = synth.stratified_subset(offs, len(srcs))
+    probe = int(order[len(order) // 2])
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        oracle.translate(model, srcs[probe], w.search)
+        t_one = time.perf_counter() - t0
+    n = int(max(P, min(len(srcs), P * max(1, math.floor(seconds / max(t_one, 1e-3))))))
+    sample = synth.stratified_subset(offs, n)
+    ctx = mp.get_context("fork")
+    with ctx.Pool(P) as pool:
+        t0 = time.perf_counter()
+        toks = pool.map(_oracle_worker, [int(i) for i in sample], chunksize=1)
+        dt = time.perf_counter() - t0
+    return {
+        "value": round(sum(toks) / dt, 2), "unit": "tokens/s", "cores": P, "kind": "oracle",
+        "sample": f"{n} of {len(srcs)} sentences, every ({len(srcs)}/{n})-th of the length-sorted order; "
+                  f"fp32 NumPy oracle, {P} processes x 1 BLAS thread; {sum(toks)} target tokens in {dt:.1f} s",
+    }
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported by this build "
+              "(sentences are independent: a multi-GPU run would shard batches across replicas)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2109_08008_amd import nt
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = synth.WORKLOADS[args.workload]
+    blob = synth.make_weights(w.model, seed=w.weights_seed)
+    ids, offs = synth.make_sentences(w.data, w.model.vocab, seed=w.data_seed)
+    model = nt.Model(w.model, blob, w.dtype)
+    sc = nt.search_cfg(w.search)
+    ws_bytes = nt.nt_translate_workspace_size(model.handle, sc, offs)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    cap = int(sum(synth.max_target_len(w.search, int(L)) for L in np.diff(offs)))
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        return nt.nt_translate(model.handle, sc, ids, offs, cap, ws.data_ptr(), ws_bytes, stream)
+
+    # warmup; the last warmup step times every kernel class to find the dominant one
+    breakdown = {}
+    for i in range(max(args.warmup, 1)):
+        if i == max(args.warmup, 1) - 1:
+            nt.nt_prof_reset()
+            nt.nt_prof_enable((1 << len(nt.KERNEL_CLASSES)) - 1)
+        step()
+    torch.cuda.synchronize()
+    for c, name in enumerate(nt.KERNEL_CLASSES):
+        breakdown[name] = nt.nt_prof_get(c)
+    nt.nt_prof_enable(0)
+    dominant = max(range(len(nt.KERNEL_CLASSES)), key=lambda c: breakdown[nt.KERNEL_CLASSES[c]]["ms"])
+
+    # timed region: events only on the dominant class
+    nt.nt_prof_reset()
+    nt.nt_prof_enable(1 << dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out, out_off, score, _ = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    nt.nt_prof_enable(0)
+    prof = nt.nt_prof_get(dominant)
+    n_tokens = int(out_off[-1])
+    elapsed = t1 - t0
+    value = n_tokens * args.steps / elapsed
+
+    line = {
+        "metric": "target tokens/sec translated (1 GPU)",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded token IDs and N(0,0.02) weights of the workload's shapes)",
+        "config": {
+            "workload": w.name, "description": w.description, "sentences": int(len(offs) - 1),
+            "source_tokens": int(offs[-1]), "target_tokens_per_step": n_tokens,
+            "beam": w.search.beam, "token_budget": w.search.token_budget,
+            "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
+        },
+        "roofline": roofline_entry(dominant, prof, w.dtype),
+        "breakdown_ms_per_step": {k: round(v["ms"], 3) for k, v in breakdown.items()},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, blob, ids, offs, args.cpu_seconds, args.cpu_procs)
+    else:
+        line["cpu_baseline"] = None
+    model.close()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -22,7 +22,7 @@ constexpr int QW = 8;        // queries per wave
 constexpr int KC = 64;       // keys per chunk
 constexpr int NW = 4;        // waves per workgroup
 
-template <typename T, int DH>
+template <typename T, int DH, int ROLE>
 __global__ __launch_bounds__(256) void mha_kernel(MhaArgs a) {
   constexpr int CPL = DH > 64 ? DH / 64 : 1;   // channels per lane in the P.V phase
   __shared__ float Ks[KC][DH + 1];
@@ -202,14 +202,14 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   }
 }
 
-template <typename T>
+template <typename T, int ROLE>
 hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
   const int qblocks = (a.q_per_group + NW * QW - 1) / (NW * QW);
   const dim3 grid(a.n_groups * qblocks, a.H);
   switch (a.dh) {
-    case 32: hipLaunchKernelGGL((mha_kernel<T, 32>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((mha_kernel<T, 64>), grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((mha_kernel<T, 128>), grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((mha_kernel<T, 32, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((mha_kernel<T, 64, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((mha_kernel<T, 128, ROLE>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -230,12 +230,12 @@ hipError_t self_t(const SelfAttnArgs& a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s) {
+hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s, int role) {
   if (a.n_groups <= 0 || a.q_per_group <= 0) return hipSuccess;
   switch (dt) {
-    case DT::F32: return mha_t<float>(a, s);
-    case DT::F16: return mha_t<f16>(a, s);
-    case DT::BF16: return mha_t<bf16>(a, s);
+    case DT::F32: return role ? mha_t<float, 1>(a, s) : mha_t<float, 0>(a, s);
+    case DT::F16: return role ? mha_t<f16, 1>(a, s) : mha_t<f16, 0>(a, s);
+    case DT::BF16: return role ? mha_t<bf16, 1>(a, s) : mha_t<bf16, 0>(a, s);
   }
   return hipErrorInvalidValue;
 }

@@ -141,7 +141,7 @@ __device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N,
   }
 }
 
-template <typename T>
+template <typename T, int ROLE>
 __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int lda, const T* __restrict__ Bt,
                                                     int M, int N, int K, GemmEpi epi, int tiles_m, int tiles_n) {
   __shared__ __attribute__((aligned(16))) unsigned char lds[2][(BM + BN) * ROWB];
@@ -270,23 +270,33 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   }
 }
 
-template <typename T>
+template <typename T, int ROLE>
 hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi, hipStream_t s) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-  hipLaunchKernelGGL(gemm_kernel<T>, dim3(tm * tn), dim3(NTHR), 0, s, static_cast<const T*>(A), lda,
+  hipLaunchKernelGGL((gemm_kernel<T, ROLE>), dim3(tm * tn), dim3(NTHR), 0, s, static_cast<const T*>(A), lda,
                      static_cast<const T*>(Bt), M, N, K, epi, tm, tn);
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_role(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
+                       hipStream_t s, int role) {
+  switch (role) {
+    case 1: return launch<T, 1>(A, lda, Bt, M, N, K, epi, s);
+    case 2: return launch<T, 2>(A, lda, Bt, M, N, K, epi, s);
+    default: return launch<T, 0>(A, lda, Bt, M, N, K, epi, s);
+  }
 }
 
 }  // namespace
 
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
-                hipStream_t s) {
+                hipStream_t s, int role) {
   switch (dt) {
-    case DT::F32: return launch<float>(A, lda, Bt, M, N, K, epi, s);
-    case DT::F16: return launch<f16>(A, lda, Bt, M, N, K, epi, s);
-    case DT::BF16: return launch<bf16>(A, lda, Bt, M, N, K, epi, s);
+    case DT::F32: return launch_role<float>(A, lda, Bt, M, N, K, epi, s, role);
+    case DT::F16: return launch_role<f16>(A, lda, Bt, M, N, K, epi, s, role);
+    case DT::BF16: return launch_role<bf16>(A, lda, Bt, M, N, K, epi, s, role);
   }
   return hipErrorInvalidValue;
 }

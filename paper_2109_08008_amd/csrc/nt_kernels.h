@@ -42,8 +42,10 @@ struct GemmEpi {
   int B = 0, S = 0;
 };
 
+// role: 0 encoder, 1 decoder step, 2 output projection.  Only the kernel's symbol name
+// depends on it, so profiles separate the three uses.
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
-                hipStream_t s);
+                hipStream_t s, int role = 0);
 
 // ---------------------------------------------------------------------------------
 // Normalisation / embedding kernels (one wave per row of d = 64*EPL elements).
@@ -101,7 +103,8 @@ struct MhaArgs {
   int n_groups, H, dh;
   float scale;
 };
-hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s);
+// role: 0 encoder self-attention, 1 encoder-decoder attention (symbol name only).
+hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s, int role = 0);
 
 // Decoder self-attention of each live row over its cached slots 0..t.
 struct SelfAttnArgs {

@@ -529,7 +529,8 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
   auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
     const double ob = e.out_f32 ? 4.0 : eb;
     const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
-    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, R, N, Kd, e, s); });
+    const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
+    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, R, N, Kd, e, s, role); });
   };
 
   NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
@@ -613,7 +614,7 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
     ma.dh = m.dh;
     ma.scale = 1.0f / std::sqrt((float)m.dh);
     NT_HIP(timed(NT_K_ATTN_CROSS, s, ((double)st->n_live * 2 * st->S * d + 2.0 * R * d) * eb,
-                 4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s); }));
+                 4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s, 1); }));
 
     e = nt::GemmEpi{};
     e.mode = nt::EPI_RESID;
