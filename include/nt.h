@@ -190,6 +190,18 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
                        int64_t* h_out_off, float* h_score, float* h_tok_logp, void* d_ws,
                        size_t ws_bytes, void* stream);
 
+/* ---- kernel-level entry point (diagnostics and tests) ----------------------------------
+ * One dense projection as the translation path runs it (the "MM" of the paper's GPU
+ * profile, Sec. 4.4): out[M,N] = A[M,K] . Bt[N,K]^T (+ bias[N]) (+ resid[M,N]), then
+ * ReLU if relu != 0.  A, Bt, resid and out are device arrays in `dtype` (out is fp32
+ * if out_f32); rows of A are lda elements apart, rows of out/resid ldc elements apart;
+ * Bt is [N][K] contiguous.  K % 64 == 0; rows of A start 16-byte aligned.  tile: 0 = chosen by
+ * shape, 1 = 64x32, 2 = 128x128, 3 = 128x64 output tiles (the choice never changes a
+ * result).  Asynchronous. */
+nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N, int32_t K,
+                     const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
+                     int32_t relu, int32_t tile, void* stream);
+
 /* Thread-local message of the last failing call on this thread ("" if none). */
 const char* nt_last_error(void);
 
@@ -212,6 +224,9 @@ typedef enum {
 } nt_kernel_class;
 
 nt_status nt_prof_enable(uint32_t class_mask);   /* bit i enables class i; 0 disables */
+/* Like nt_prof_enable, but only every `stride`-th launch of an enabled class is timed
+ * (stride >= 1), which keeps the host cost of event recording out of a timed run. */
+nt_status nt_prof_config(uint32_t class_mask, int32_t stride);
 nt_status nt_prof_reset(void);
 /* Totals since the last reset for one class; synchronises on the recorded events. */
 nt_status nt_prof_get(int32_t kernel_class, int64_t* launches, double* total_ms, double* alg_bytes,

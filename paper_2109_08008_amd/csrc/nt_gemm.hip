@@ -2,11 +2,13 @@
 // (the "MM" that dominates the paper's GPU profile, Sec. 4.4) as one MFMA GEMM for
 // gfx950:  C[M,N] = A[M,K] . Bt[N,K]^T with fp32 accumulation and a fused epilogue.
 //
-// Tiling: 128x128 output tile per 256-thread workgroup, four waves in a 2x2 grid, each
-// owning 64x64 = 4x4 MFMA blocks of 16x16.  K advances 128 bytes per step (64 halves or
-// 32 floats), double-buffered through LDS (2 x 32 KB) with an XOR swizzle of the
-// 16-byte chunks so that both the cooperative stores and the fragment reads are free of
-// bank conflicts.  fp16/bf16 use v_mfma_f32_16x16x32_{f16,bf16}; fp32 uses four
+// Tiling: BMxBN output tile (128x128, 128x64 or 64x32) per 256-thread workgroup, four
+// waves in a 2x2 grid of 16x16 MFMA blocks.  K advances 128 bytes per step (64 halves or 32
+// floats) through a ring of STAGES LDS slots filled by direct global->LDS loads
+// (global_load_lds_dwordx4), so STAGES-1 k-tiles are in flight while one is multiplied;
+// one barrier per k-step.  The loop body is kept compact (no unrolling over k): every
+// workgroup of a small decode-step GEMM starts on a cold instruction cache.  The 16-byte chunks of each tile row are XOR-swizzled so that
+// the fragment reads are free of bank conflicts.  fp16/bf16 use v_mfma_f32_16x16x32_{f16,bf16}; fp32 uses four
 // v_mfma_f32_16x16x4_f32 per 16-byte fragment (true fp32 products, no reduced-precision
 // inputs).  Because the two operands of an MFMA only need to agree on which k each
 // lane supplies, lane l feeds A[row l%16][k-chunk l/16] and Bt[col l%16][same chunk].
@@ -31,24 +33,25 @@ constexpr int NTHR = 256;
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bhalf8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 template <typename T> struct Mfma;
 template <> struct Mfma<f16> {
-  static __device__ __forceinline__ floatx4 step(const uint4& a, const uint4& b, floatx4 c) {
+  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c,
                                                   0, 0, 0);
   }
 };
 template <> struct Mfma<bf16> {
-  static __device__ __forceinline__ floatx4 step(const uint4& a, const uint4& b, floatx4 c) {
+  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bhalf8, a), __builtin_bit_cast(bhalf8, b),
                                                    c, 0, 0, 0);
   }
 };
 template <> struct Mfma<float> {
-  static __device__ __forceinline__ floatx4 step(const uint4& a, const uint4& b, floatx4 c) {
-    const float4 av = __builtin_bit_cast(float4, a);
-    const float4 bv = __builtin_bit_cast(float4, b);
+  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
+    const floatx4 av = __builtin_bit_cast(floatx4, a);
+    const floatx4 bv = __builtin_bit_cast(floatx4, b);
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, c, 0, 0, 0);
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, c, 0, 0, 0);
     c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, c, 0, 0, 0);
@@ -141,10 +144,73 @@ __device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N,
   }
 }
 
-template <typename T, int ROLE>
+// s_waitcnt immediate that waits until at most `vm` vector-memory operations of this wave
+// are outstanding (expcnt / lgkmcnt left unconstrained).
+__host__ __device__ constexpr int vmcnt_imm(int vm) { return (vm & 0xF) | ((vm >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+#define NT_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Fragment reads are issued as inline ds_read_b128 so that the compiler does not place a
+// wait for every in-flight direct global->LDS load in front of them (it cannot tell them
+// apart from the loads still filling other slots).  Completion is then made explicit:
+// lds_wait() waits for the reads and names the fragments as operands, so no use of a
+// fragment can be scheduled before it.
+__device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
+  u32x4 v;
+  const unsigned a = (unsigned)(uintptr_t)NT_LDS(p);
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+template <int FM, int FN> struct LdsWait;
+template <> struct LdsWait<1, 1> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[1], u32x4 (&b)[1]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(b[0]));
+  }
+};
+template <> struct LdsWait<1, 2> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[1], u32x4 (&b)[2]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(b[0]), "+v"(b[1]));
+  }
+};
+template <> struct LdsWait<2, 1> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[1]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]));
+  }
+};
+template <> struct LdsWait<2, 4> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+  }
+};
+template <> struct LdsWait<4, 2> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[4], u32x4 (&b)[2]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]));
+  }
+};
+template <> struct LdsWait<2, 2> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[2]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]));
+  }
+};
+template <> struct LdsWait<4, 4> {
+  static __device__ __forceinline__ void run(u32x4 (&a)[4], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+  }
+};
+
+template <typename T, int BM_, int BN_, int STAGES, int ROLE>
 __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int lda, const T* __restrict__ Bt,
                                                     int M, int N, int K, GemmEpi epi, int tiles_m, int tiles_n) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds[2][(BM + BN) * ROWB];
+  constexpr int STAGE_BYTES = (BM_ + BN_) * ROWB;
+  constexpr int GROUPS = (BM_ + BN_) / 8;          // 8 tile rows = one 1 KB wave load
+  constexpr int LPW = GROUPS / 4;                   // loads per wave per stage
+  constexpr int WM = BM_ / 2, WN = BN_ / 2;         // 2x2 waves
+  constexpr int FM = WM / 16, FN = WN / 16;         // 16x16 blocks per wave
+  static_assert(GROUPS % 4 == 0, "tile rows must split evenly over 4 waves");
+  static_assert(STAGES >= 2 && STAGES <= 8, "1..7 k-tiles in flight");
+  static_assert((STAGES - 2) * LPW <= 63, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES * STAGE_BYTES];
 
   // --- tile assignment: XCD-contiguous, then grouped by 8 tile-rows ---
   const int ntiles = tiles_m * tiles_n;
@@ -159,144 +225,145 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   const int gsize = min(tiles_m - first_m, GROUP);
   const int tm = first_m + (pid % per_group) % gsize;
   const int tn = (pid % per_group) / gsize;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * BM_, n0 = tn * BN_;
 
-  const int tid = threadIdx.x;
-  const char* Ab = reinterpret_cast<const char*>(A);
-  const char* Bb = reinterpret_cast<const char*>(Bt);
-
-  // --- global -> register staging: 4 chunks of A and 4 of Bt per thread per step ---
-  // Rows past the edge re-read the last valid row; their results are never stored.
-  const int row0 = tid / CH, ch0 = tid % CH;      // chunk i covers tile row row0 + 32*i
-  constexpr int RSTEP = NTHR / CH;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const size_t lda_b = (size_t)lda * sizeof(T), ldb_b = (size_t)K * sizeof(T);
-  const char* const pa0 = Ab + (size_t)min(m0 + row0 + 0 * RSTEP, M - 1) * lda_b + ch0 * 16;
-  const char* const pa1 = Ab + (size_t)min(m0 + row0 + 1 * RSTEP, M - 1) * lda_b + ch0 * 16;
-  const char* const pa2 = Ab + (size_t)min(m0 + row0 + 2 * RSTEP, M - 1) * lda_b + ch0 * 16;
-  const char* const pa3 = Ab + (size_t)min(m0 + row0 + 3 * RSTEP, M - 1) * lda_b + ch0 * 16;
-  const char* const pb0 = Bb + (size_t)min(n0 + row0 + 0 * RSTEP, N - 1) * ldb_b + ch0 * 16;
-  const char* const pb1 = Bb + (size_t)min(n0 + row0 + 1 * RSTEP, N - 1) * ldb_b + ch0 * 16;
-  const char* const pb2 = Bb + (size_t)min(n0 + row0 + 2 * RSTEP, N - 1) * ldb_b + ch0 * 16;
-  const char* const pb3 = Bb + (size_t)min(n0 + row0 + 3 * RSTEP, N - 1) * ldb_b + ch0 * 16;
-  const int lo0 = swz(row0 + 0 * RSTEP, ch0), lo1 = swz(row0 + 1 * RSTEP, ch0);
-  const int lo2 = swz(row0 + 2 * RSTEP, ch0), lo3 = swz(row0 + 3 * RSTEP, ch0);
-  uint4 ra0, ra1, ra2, ra3, rb0, rb1, rb2, rb3;
-#define NT_GLOAD(kt)                                                 \
-  {                                                                  \
-    const size_t kb_ = (size_t)(kt) * ROWB;                          \
-    ra0 = *reinterpret_cast<const uint4*>(pa0 + kb_);                \
-    ra1 = *reinterpret_cast<const uint4*>(pa1 + kb_);                \
-    ra2 = *reinterpret_cast<const uint4*>(pa2 + kb_);                \
-    ra3 = *reinterpret_cast<const uint4*>(pa3 + kb_);                \
-    rb0 = *reinterpret_cast<const uint4*>(pb0 + kb_);                \
-    rb1 = *reinterpret_cast<const uint4*>(pb1 + kb_);                \
-    rb2 = *reinterpret_cast<const uint4*>(pb2 + kb_);                \
-    rb3 = *reinterpret_cast<const uint4*>(pb3 + kb_);                \
-  }
-#define NT_LSTORE(buf)                                               \
-  {                                                                  \
-    unsigned char* la_ = lds[buf];                                   \
-    unsigned char* lb_ = lds[buf] + BM * ROWB;                       \
-    *reinterpret_cast<uint4*>(la_ + lo0) = ra0;                      \
-    *reinterpret_cast<uint4*>(la_ + lo1) = ra1;                      \
-    *reinterpret_cast<uint4*>(la_ + lo2) = ra2;                      \
-    *reinterpret_cast<uint4*>(la_ + lo3) = ra3;                      \
-    *reinterpret_cast<uint4*>(lb_ + lo0) = rb0;                      \
-    *reinterpret_cast<uint4*>(lb_ + lo1) = rb1;                      \
-    *reinterpret_cast<uint4*>(lb_ + lo2) = rb2;                      \
-    *reinterpret_cast<uint4*>(lb_ + lo3) = rb3;                      \
+
+  // Direct global -> LDS loads: one instruction moves 8 tile rows (64 lanes x 16 B, lane l
+  // to LDS byte 16*l of the group).  Lane l fills LDS chunk (l & 7) of row l/8, which
+  // holds global chunk (l & 7) ^ (row & 7) under the swizzle; rows past the edge re-read
+  // the last valid row (their results are never stored).
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  const char* Ab = reinterpret_cast<const char*>(A) + lchunk * 16;
+  const char* Bb = reinterpret_cast<const char*>(Bt) + lchunk * 16;
+#define NT_ISSUE(kt, SL)                                                                          \
+  {                                                                                               \
+    unsigned char* sb_ = lds + (SL) * STAGE_BYTES;                                                \
+    const size_t kb_ = (size_t)(kt) * ROWB;                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < LPW; ++i_) {                                          \
+      const int g_ = wave * LPW + i_;                                                             \
+      const int row_ = g_ * 8 + lrow;                                                             \
+      const char* src_ = row_ < BM_ ? Ab + (size_t)min(m0 + row_, M - 1) * lda_b + kb_            \
+                                    : Bb + (size_t)min(n0 + row_ - BM_, N - 1) * ldb_b + kb_;     \
+      __builtin_amdgcn_global_load_lds(src_, NT_LDS(sb_ + g_ * 1024), 16, 0, 0);                 \
+    }                                                                                             \
   }
 
-  const int wave = tid / kWave, lane = tid % kWave;
-  const int wm = wave >> 1, wn = wave & 1;
   const int fr = lane & 15, fc = lane >> 4;   // fragment row / 16-byte chunk within a k-slice
-  floatx4 acc[4][4];
+  floatx4 acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  const int wm = wave >> 1, wn = wave & 1;
   const int nk = (int)((size_t)K * sizeof(T) / ROWB);
-  NT_GLOAD(0);
-  NT_LSTORE(0);
-  __syncthreads();
+  for (int st = 0; st < STAGES - 1 && st < nk; ++st) NT_ISSUE(st, st)
+  int slot = 0;   // slot of k-step kt
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) NT_GLOAD(kt + 1);
-    const unsigned char* As = lds[buf];
-    const unsigned char* Bs = lds[buf] + BM * ROWB;
+    if (kt + STAGES - 2 <= nk - 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm((STAGES - 2) * LPW));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    __builtin_amdgcn_s_barrier();   // tile kt is in LDS for every wave; slot kt-1 is free
+    if (kt + STAGES - 1 < nk) NT_ISSUE(kt + STAGES - 1, slot == 0 ? STAGES - 1 : slot - 1)
+    const unsigned char* As = lds + slot * STAGE_BYTES;
+    const unsigned char* Bs = As + BM_ * ROWB;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      uint4 af[4], bf[4];
+      u32x4 af[FM], bf[FN];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        af[i] = *reinterpret_cast<const uint4*>(As + swz(wm * 64 + i * 16 + fr, kk * 4 + fc));
-        bf[i] = *reinterpret_cast<const uint4*>(Bs + swz(wn * 64 + i * 16 + fr, kk * 4 + fc));
-      }
+      for (int i = 0; i < FM; ++i) af[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, kk * 4 + fc));
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < FN; ++j) bf[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, kk * 4 + fc));
+      LdsWait<FM, FN>::run(af, bf);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = Mfma<T>::step(af[i], bf[j], acc[i][j]);
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af[i], bf[j], acc[i][j]);
     }
-    if (kt + 1 < nk) NT_LSTORE(buf ^ 1);
-    __syncthreads();
+    slot = slot == STAGES - 1 ? 0 : slot + 1;
   }
+#undef NT_ISSUE
+  __syncthreads();
 
-#undef NT_GLOAD
-#undef NT_LSTORE
-
-  // --- epilogue through LDS, 64 rows at a time: fragments -> [64][132] fp32 tile (the
-  // 132-float row stride keeps the fragment writes conflict-free) -> 4 consecutive
+  // --- epilogue through the first LDS slot in passes of ER rows: fragments -> [ER][BN+4] fp32
+  // tile (the BN+4 stride keeps the fragment writes conflict-free) -> 4 consecutive
   // columns per thread for coalesced stores ---
-  constexpr int CS = 132;
-  float* cs = reinterpret_cast<float*>(&lds[0][0]);
+  constexpr int CS = BN_ + 4;
+  constexpr int ER = (BM_ * CS * 4 <= STAGE_BYTES) ? BM_ : (WM * CS * 4 <= STAGE_BYTES) ? WM : WM / 2;
+  constexpr int PASSES = BM_ / ER;
+  static_assert(ER * CS * 4 <= STAGE_BYTES && ER % 16 == 0, "epilogue tile fits one slot");
+  float* cs = reinterpret_cast<float*>(lds);
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    if (half) __syncthreads();
-    if (wm == half) {
+  for (int pass = 0; pass < PASSES; ++pass) {
+    if (pass) __syncthreads();
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < FM; ++i) {
+      const int rb = wm * WM + i * 16;            // first tile row of this block
+      if (rb >= pass * ER && rb < pass * ER + ER) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) cs[(i * 16 + fc * 4 + r) * CS + wn * 64 + j * 16 + fr] = acc[i][j][r];
+          for (int r = 0; r < 4; ++r)
+            cs[(rb - pass * ER + fc * 4 + r) * CS + wn * WN + j * 16 + fr] = acc[i][j][r];
+      }
     }
     __syncthreads();
-    for (int g = tid; g < 64 * 32; g += NTHR) {
-      const int row = g >> 5, c4 = g & 31;
-      const int m = m0 + half * 64 + row, n = n0 + c4 * 4;
+    for (int g = tid; g < ER * (BN_ / 4); g += NTHR) {
+      const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+      const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
       if (m < M && n < N) epilogue4<T>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]));
     }
   }
 }
 
-template <typename T, int ROLE>
-hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi, hipStream_t s) {
-  if (M <= 0 || N <= 0) return hipSuccess;
-  const int tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-  hipLaunchKernelGGL((gemm_kernel<T, ROLE>), dim3(tm * tn), dim3(NTHR), 0, s, static_cast<const T*>(A), lda,
-                     static_cast<const T*>(Bt), M, N, K, epi, tm, tn);
+template <typename T, int BM_, int BN_, int STAGES, int ROLE>
+hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
+                       hipStream_t s) {
+  const int tm = (M + BM_ - 1) / BM_, tn = (N + BN_ - 1) / BN_;
+  hipLaunchKernelGGL((gemm_kernel<T, BM_, BN_, STAGES, ROLE>), dim3(tm * tn), dim3(NTHR), 0, s,
+                     static_cast<const T*>(A), lda, static_cast<const T*>(Bt), M, N, K, epi, tm, tn);
   return hipGetLastError();
+}
+
+// Tile choice by problem size (measured on MI355X): LDS footprint matters more than
+// pipeline depth, so big tiles use two stages (two workgroups per CU).
+//   128x128, 2 stages (64 KB)  when that gives >= 512 tiles (vocabulary, encoder);
+//   128x64,  2 stages (48 KB)  when that gives >= 256 tiles;
+//   64x32,   3 stages (36 KB)  otherwise (skinny decode-step shapes, ~5 us).
+// All reduce each output over K in the same order, so the choice never changes a result.
+template <typename T, int ROLE>
+hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi, hipStream_t s,
+                  int tile) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const long long t128 = (long long)((M + 127) / 128) * ((N + 127) / 128);
+  const long long t12864 = (long long)((M + 127) / 128) * ((N + 63) / 64);
+  if (tile == 0) tile = t128 >= 512 ? 2 : t12864 >= 256 ? 3 : 1;
+  switch (tile) {
+    case 2: return launch_tile<T, 128, 128, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
+    case 3: return launch_tile<T, 128, 64, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
+    default: return launch_tile<T, 64, 32, 3, ROLE>(A, lda, Bt, M, N, K, epi, s);
+  }
 }
 
 template <typename T>
 hipError_t launch_role(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
-                       hipStream_t s, int role) {
+                       hipStream_t s, int role, int tile) {
   switch (role) {
-    case 1: return launch<T, 1>(A, lda, Bt, M, N, K, epi, s);
-    case 2: return launch<T, 2>(A, lda, Bt, M, N, K, epi, s);
-    default: return launch<T, 0>(A, lda, Bt, M, N, K, epi, s);
+    case 1: return launch<T, 1>(A, lda, Bt, M, N, K, epi, s, tile);
+    case 2: return launch<T, 2>(A, lda, Bt, M, N, K, epi, s, tile);
+    default: return launch<T, 0>(A, lda, Bt, M, N, K, epi, s, tile);
   }
 }
 
 }  // namespace
 
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
-                hipStream_t s, int role) {
+                hipStream_t s, int role, int tile) {
   switch (dt) {
-    case DT::F32: return launch_role<float>(A, lda, Bt, M, N, K, epi, s, role);
-    case DT::F16: return launch_role<f16>(A, lda, Bt, M, N, K, epi, s, role);
-    case DT::BF16: return launch_role<bf16>(A, lda, Bt, M, N, K, epi, s, role);
+    case DT::F32: return launch_role<float>(A, lda, Bt, M, N, K, epi, s, role, tile);
+    case DT::F16: return launch_role<f16>(A, lda, Bt, M, N, K, epi, s, role, tile);
+    case DT::BF16: return launch_role<bf16>(A, lda, Bt, M, N, K, epi, s, role, tile);
   }
   return hipErrorInvalidValue;
 }

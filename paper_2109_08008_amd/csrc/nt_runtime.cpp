@@ -66,6 +66,8 @@ struct ProfRec {
 };
 std::mutex g_prof_mu;
 uint32_t g_prof_mask = 0;
+int g_prof_stride = 1;
+int64_t g_prof_seen[NT_K_COUNT] = {};
 std::vector<ProfRec> g_prof;
 std::vector<hipEvent_t> g_prof_pool;
 
@@ -84,6 +86,7 @@ template <typename F>
 hipError_t timed(int cls, hipStream_t s, double bytes, double flops, F&& launch) {
   if (!(g_prof_mask & (1u << cls))) return launch();
   std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (g_prof_seen[cls]++ % g_prof_stride != 0) return launch();
   hipEvent_t a = prof_event(), b = prof_event();
   if (!a || !b) return hipErrorOutOfMemory;
   hipError_t e = hipEventRecord(a, s);
@@ -1143,11 +1146,41 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
   return NT_OK;
 }
 
-nt_status nt_prof_enable(uint32_t class_mask) {
-  std::lock_guard<std::mutex> lk(g_prof_mu);
-  g_prof_mask = class_mask & ((1u << NT_K_COUNT) - 1);
+nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N, int32_t K,
+                     const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
+                     int32_t relu, int32_t tile, void* stream) {
+  g_err.clear();
+  if (!d_A || !d_Bt || !d_out) return fail(NT_E_INVALID, "null argument to nt_op_gemm");
+  if (dtype < NT_F32 || dtype > NT_BF16) return fail(NT_E_INVALID, "unknown dtype %d", dtype);
+  if (M < 0 || N <= 0 || K <= 0 || K % 64 != 0) return fail(NT_E_UNSUPPORTED, "need N > 0, K > 0, K %% 64 == 0");
+  const int eb = dtype == NT_F32 ? 4 : 2;
+  if (lda < K || (lda * eb) % 16 != 0 || ldc < N)
+    return fail(NT_E_INVALID, "lda must be >= K with 16-byte rows, ldc >= N");
+  if (tile < 0 || tile > 3) return fail(NT_E_INVALID, "tile must be 0..3");
+  if (relu && (d_resid || out_f32)) return fail(NT_E_UNSUPPORTED, "relu combines with neither resid nor fp32 out");
+  if (d_resid && out_f32) return fail(NT_E_UNSUPPORTED, "resid needs a model-dtype output");
+  nt::GemmEpi e{};
+  e.mode = relu ? nt::EPI_RELU : d_resid ? nt::EPI_RESID : nt::EPI_STORE;
+  e.bias = d_bias;
+  e.resid = d_resid;
+  e.out = d_out;
+  e.ldc = ldc;
+  e.out_f32 = out_f32 ? 1 : 0;
+  NT_HIP(nt::gemm(static_cast<DT>(dtype), d_A, lda, d_Bt, M, N, K, e, static_cast<hipStream_t>(stream), 0, tile));
   return NT_OK;
 }
+
+nt_status nt_prof_config(uint32_t class_mask, int32_t stride) {
+  g_err.clear();
+  if (stride < 1) return fail(NT_E_INVALID, "stride must be >= 1");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_mask = class_mask & ((1u << NT_K_COUNT) - 1);
+  g_prof_stride = stride;
+  for (auto& c : g_prof_seen) c = 0;
+  return NT_OK;
+}
+
+nt_status nt_prof_enable(uint32_t class_mask) { return nt_prof_config(class_mask, 1); }
 
 nt_status nt_prof_reset(void) {
   std::lock_guard<std::mutex> lk(g_prof_mu);

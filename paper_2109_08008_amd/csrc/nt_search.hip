@@ -29,7 +29,7 @@ __device__ __forceinline__ MaxSum ms_merge(MaxSum a, MaxSum b) {
   if (b.m == -INFINITY) return a;
   if (a.m == -INFINITY) return b;
   const float m = fmaxf(a.m, b.m);
-  return {m, a.s * expf(a.m - m) + b.s * expf(b.m - m)};
+  return {m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
 }
 // (value desc, index asc)
 __device__ __forceinline__ bool better(float v1, int i1, float v2, int i2) {
@@ -52,10 +52,10 @@ __device__ void row_lse_argmax(const float* __restrict__ x, int V, float& lse, f
       const float4 v = x4[i];
       const float mx = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
       if (mx > acc.m) {
-        acc.s = acc.m == -INFINITY ? 0.f : acc.s * expf(acc.m - mx);
+        acc.s = acc.m == -INFINITY ? 0.f : acc.s * __expf(acc.m - mx);
         acc.m = mx;
       }
-      acc.s += expf(v.x - acc.m) + expf(v.y - acc.m) + expf(v.z - acc.m) + expf(v.w - acc.m);
+      acc.s += __expf(v.x - acc.m) + __expf(v.y - acc.m) + __expf(v.z - acc.m) + __expf(v.w - acc.m);
       if (v.x > bv) { bv = v.x; bi = 4 * i; }
       if (v.y > bv) { bv = v.y; bi = 4 * i + 1; }
       if (v.z > bv) { bv = v.z; bi = 4 * i + 2; }
@@ -65,10 +65,10 @@ __device__ void row_lse_argmax(const float* __restrict__ x, int V, float& lse, f
     for (int i = tid; i < V; i += SEL_THREADS) {
       const float v = x[i];
       if (v > acc.m) {
-        acc.s = acc.m == -INFINITY ? 0.f : acc.s * expf(acc.m - v);
+        acc.s = acc.m == -INFINITY ? 0.f : acc.s * __expf(acc.m - v);
         acc.m = v;
       }
-      acc.s += expf(v - acc.m);
+      acc.s += __expf(v - acc.m);
       if (v > bv) { bv = v; bi = i; }
     }
   }
@@ -155,19 +155,50 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
                                                                   float* __restrict__ lse_out) {
   __shared__ float wv[SEL_THREADS / kWave][K2];
   __shared__ int wi[SEL_THREADS / kWave][K2];
+  __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
   const int r = blockIdx.x;
   const float* x = logits + (size_t)r * V;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
 
-  float lse, best;
-  int bidx;
-  row_lse_argmax(x, V, lse, best, bidx);
-
+  // one pass over the row: online max/sum for the LSE and a sorted list of this
+  // thread's K2 largest logits (elements visited in increasing index)
+  MaxSum acc{-INFINITY, 0.f};
   float v[K2];
   int ix[K2];
 #pragma unroll
   for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
-  for (int i = tid; i < V; i += SEL_THREADS) list_insert<K2>(v, ix, x[i], i);
+  const bool vec = (V % 4) == 0 && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
+  if (vec) {
+    const float4* x4 = reinterpret_cast<const float4*>(x);
+    for (int i = tid; i < V / 4; i += SEL_THREADS) {
+      const float4 q = x4[i];
+      const float mx = fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w));
+      if (mx > acc.m) {
+        acc.s = acc.m == -INFINITY ? 0.f : acc.s * __expf(acc.m - mx);
+        acc.m = mx;
+      }
+      acc.s += __expf(q.x - acc.m) + __expf(q.y - acc.m) + __expf(q.z - acc.m) + __expf(q.w - acc.m);
+      if (mx > v[K2 - 1]) {
+        list_insert<K2>(v, ix, q.x, 4 * i);
+        list_insert<K2>(v, ix, q.y, 4 * i + 1);
+        list_insert<K2>(v, ix, q.z, 4 * i + 2);
+        list_insert<K2>(v, ix, q.w, 4 * i + 3);
+      }
+    }
+  } else {
+    for (int i = tid; i < V; i += SEL_THREADS) {
+      const float q = x[i];
+      if (q > acc.m) {
+        acc.s = acc.m == -INFINITY ? 0.f : acc.s * __expf(acc.m - q);
+        acc.m = q;
+      }
+      acc.s += __expf(q - acc.m);
+      list_insert<K2>(v, ix, q, i);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; }
 
   // each wave merges its 64 lists: K2 rounds of a wave-wide (value desc, index asc) argmax;
   // the winning lane drops its head
@@ -205,7 +236,10 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
       topv[(size_t)r * k2 + j] = bv;
       topi[(size_t)r * k2 + j] = bi;
     }
-    lse_out[r] = lse;
+    MaxSum tot{sm[0], ss[0]};
+#pragma unroll
+    for (int w = 1; w < SEL_THREADS / kWave; ++w) tot = ms_merge(tot, MaxSum{sm[w], ss[w]});
+    lse_out[r] = tot.m + logf(tot.s);
   }
 }
 

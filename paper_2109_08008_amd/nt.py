@@ -29,6 +29,7 @@ EXPORTS = [
     "nt_weights_size", "nt_load_weights", "nt_free_model", "nt_workspace_size", "nt_translate_workspace_size",
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
+    "nt_op_gemm", "nt_prof_config",
 ]
 
 
@@ -83,8 +84,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    P, c_size_t, P]),
         "nt_last_error": (c_char_p, []),
         "nt_prof_enable": (c_int32, [c_uint32]),
+        "nt_prof_config": (c_int32, [c_uint32, c_int32]),
         "nt_prof_reset": (c_int32, []),
         "nt_prof_get": (c_int32, [c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
+        "nt_op_gemm": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, P, P, c_int32, c_int32, c_int32,
+                                 c_int32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -219,8 +223,19 @@ def nt_translate(m, search: nt_search_cfg, h_src: np.ndarray, h_src_off: np.ndar
     return out[:out_off[-1]], out_off, score, logp[:out_off[-1]]
 
 
+def nt_op_gemm(dtype: str, d_A: int, lda: int, d_Bt: int, M: int, N: int, K: int, d_bias, d_resid, d_out: int,
+               ldc: int, out_f32: bool = False, relu: bool = False, tile: int = 0, stream=None):
+    _check(load_library().nt_op_gemm(DTYPES[dtype], c_void_p(d_A), lda, c_void_p(d_Bt), M, N, K,
+                                     c_void_p(d_bias) if d_bias else None, c_void_p(d_resid) if d_resid else None,
+                                     c_void_p(d_out), ldc, int(out_f32), int(relu), tile, _stream(stream)))
+
+
 def nt_prof_enable(mask: int):
     _check(load_library().nt_prof_enable(mask))
+
+
+def nt_prof_config(mask: int, stride: int):
+    _check(load_library().nt_prof_config(mask, stride))
 
 
 def nt_prof_reset():
