@@ -102,7 +102,7 @@ def cpu_baseline(w: synth.Workload, blob, ids, offs, seconds: float, procs: int)
         t0 = time.perf_counter()
         oracle.translate(model, srcs[probe], w.search)
         t_one = time.perf_counter() - t0
-    n = int(max(P, min(len(srcs), P * max(1, math.floor(seconds / max(t_one, 1e-3))))))
+    n = int(min(len(srcs), max(P, P * max(1, math.floor(seconds / max(t_one, 1e-3))))))
     sample = synth.stratified_subset(offs, n)
     ctx = mp.get_context("fork")
     with ctx.Pool(P) as pool:
