@@ -20,7 +20,11 @@ enum EpiMode : int {
   EPI_RESID = 2,      // out = resid + acc + bias  (resid may alias out)
   EPI_SELF_QKV = 3,   // decoder: cols [0,d) -> q out; [d,3d) -> K/V cache slot t of phys row
   EPI_CROSS_KV = 4,   // encoder: cols of [Ld][K|V][d] -> cross cache [Ld][2][B][H][S][dh]
+  EPI_TOPK = 5,       // output projection: per row and 128-column tile, the (max, sum exp,
+                      // k2 largest (value, index)) partials instead of the logits
 };
+constexpr int TOPK_MAX = 8;   // k2 of the fused selection (greedy 1, beam up to 4 -> 8)
+__host__ __device__ inline int topk_record(int k2) { return 2 + 2 * k2; }   // floats per partial record
 
 struct GemmEpi {
   int mode = EPI_STORE;
@@ -40,6 +44,10 @@ struct GemmEpi {
   // EPI_CROSS_KV
   void* cross = nullptr;           // [Ld][2][B][H][S][dh]
   int B = 0, S = 0;
+  // EPI_TOPK (the launch uses 128x128 tiles, so n_tiles = ceil(N / 128))
+  float* part = nullptr;           // [M][n_tiles][topk_record(k2)]
+  int k2 = 1;
+  int n_tiles = 0;
 };
 
 // role: 0 encoder, 1 decoder step, 2 output projection.  Only the kernel's symbol name
@@ -153,6 +161,13 @@ hipError_t beam_select(const float* logits, int rows, int V, int k2, float* topv
                        hipStream_t s);
 hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, int t,
                        hipStream_t s);
+
+// Fused selection after an EPI_TOPK projection: merge the per-tile partials of each live
+// row.  Greedy: argmax + LSE, then the greedy update.  Beam: top-k2 + LSE into
+// topv/topi/lse for beam_update.
+hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, int t, hipStream_t s);
+hipError_t beam_merge(const float* part, int n_tiles, int rows, int k2, float* topv, int* topi, float* lse,
+                      hipStream_t s);
 
 // Compaction: new_list = [b in list if !done[b]] in order; count -> *n_out (device).
 hipError_t compact(const int* list, int n, const int* done, int* new_list, int* n_out, hipStream_t s);

@@ -333,7 +333,8 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.dq = take(R * d * eb);
   p.datt = take(R * d * eb);
   p.df = take(R * m.F * eb);
-  p.logits = take(R * m.V * 4);
+  // fp32 logits, or (fused selection) the per-tile partial records, whichever is larger
+  p.logits = take(std::max(R * m.V * 4, R * (size_t)((m.V + 127) / 128) * nt::topk_record(nt::TOPK_MAX) * 4));
   p.topv = take(R * 2 * K * 4);
   p.topi = take(R * 2 * K * 4);
   p.lse = take(R * 4);
@@ -530,10 +531,11 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
   const int* list = st->list(st->list_cur);
 
   auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
-    const double ob = e.out_f32 ? 4.0 : eb;
+    const double ob = e.mode == nt::EPI_TOPK ? 0.0 : e.out_f32 ? 4.0 : eb;
     const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
     const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
-    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, R, N, Kd, e, s, role); });
+    const int tile = e.mode == nt::EPI_TOPK ? 2 : 0;   // the partial records assume 128-column tiles
+    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, R, N, Kd, e, s, role, tile); });
   };
 
   NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
@@ -650,7 +652,35 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
                  [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), R, d, eps, s); }));
   }
 
-  // tied output projection: logits = LN_dec(z) E^T  (fp32 logits)
+  nt::SearchState ss = st->search();
+  // Tied output projection.  Normally the projection's epilogue reduces each row to
+  // per-tile (max, sum exp, k2 best) partials and the logits never reach HBM; teacher
+  // forcing and the logits copy-out use the plain path that writes fp32 logits.
+  // (measured: the fused epilogue pays for itself for greedy's argmax; a top-8 per tile
+  // row costs more than writing and re-reading the logits, so beam keeps the plain path)
+  const int k2 = K == 1 ? 1 : 2 * K;
+  if (!d_logits && !d_forced && K == 1) {
+    const int n_tiles = (m.V + 127) / 128;
+    nt::GemmEpi e{};
+    e.mode = nt::EPI_TOPK;
+    e.part = st->at<float>(p.logits);
+    e.k2 = k2;
+    e.n_tiles = n_tiles;
+    NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+    const float* part = st->at<float>(p.logits);
+    const double pbytes = (double)R * n_tiles * nt::topk_record(k2) * 4;
+    if (K == 1) {
+      NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, t, s); }));
+    } else {
+      NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] {
+        return nt::beam_merge(part, n_tiles, R, k2, st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), s);
+      }));
+      NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
+        return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, t, s);
+      }));
+      st->anc_cur ^= 1;
+    }
+  } else {
   nt::GemmEpi e{};
   e.mode = nt::EPI_STORE;
   e.out = at(p.logits);
@@ -659,7 +689,6 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
   NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
   if (d_logits) NT_HIP(nt::scatter_logits(st->at<float>(p.logits), list, K, R, m.V, d_logits, s));
 
-  nt::SearchState ss = st->search();
   if (K == 1) {
     NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V,
                  [&] { return nt::greedy_step(st->at<float>(p.logits), d_forced, ss, t, s); }));
@@ -672,6 +701,7 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
       return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, t, s);
     }));
     st->anc_cur ^= 1;
+  }
   }
   int* cnt = st->at<int>(p.count);
   NT_HIP(timed(NT_K_SEARCH, s, (double)st->n_live * 8, 0.0, [&] {

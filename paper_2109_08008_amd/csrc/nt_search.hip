@@ -97,20 +97,12 @@ __device__ void row_lse_argmax(const float* __restrict__ x, int V, float& lse, f
   bidx = fi;
 }
 
-__global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __restrict__ logits,
-                                                             const int* __restrict__ forced, SearchState st, int t) {
-  const int r = blockIdx.x;
-  const int b = st.sent_list[r];
-  const int p = b;                      // beam 1: physical row = sentence
-  const float* x = logits + (size_t)r * st.V;
-  float lse, best;
-  int bidx;
-  row_lse_argmax(x, st.V, lse, best, bidx);
-  if (threadIdx.x != 0 || st.done[b]) return;
+// Greedy update of sentence b (beam 1: physical row = sentence) with the emitted token
+// and its log-prob: EOS finishes the sentence (its log-prob counts in the score), as does
+// reaching the length limit.
+__device__ void greedy_update(const SearchState& st, int b, int tok, float lp, int t) {
+  const int p = b;
   const int R = st.B;
-  int tok = forced ? forced[p] : bidx;
-  if (tok < 0 || tok >= st.V) tok = st.eos;   // out-of-range forced ID or an all-NaN row: end the sentence
-  const float lp = x[tok] - lse;
   st.score[p] += lp;
   if (tok == st.eos) {
     st.done[b] = 1;
@@ -132,6 +124,63 @@ __global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __rest
     st.best_step[b] = t;
     st.best_row[b] = p;
   }
+}
+
+__global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __restrict__ logits,
+                                                             const int* __restrict__ forced, SearchState st, int t) {
+  const int r = blockIdx.x;
+  const int b = st.sent_list[r];
+  const float* x = logits + (size_t)r * st.V;
+  float lse, best;
+  int bidx;
+  row_lse_argmax(x, st.V, lse, best, bidx);
+  if (threadIdx.x != 0 || st.done[b]) return;
+  int tok = forced ? forced[b] : bidx;
+  if (tok < 0 || tok >= st.V) tok = st.eos;   // out-of-range forced ID or an all-NaN row: end the sentence
+  greedy_update(st, b, tok, x[tok] - lse, t);
+}
+
+// Greedy selection from the projection's per-tile partials [rows][n_tiles][4]
+// (max, sum exp, best value, best index): merged in tile order, then the update.
+__global__ __launch_bounds__(SEL_THREADS) void greedy_fused_kernel(const float* __restrict__ part, int n_tiles,
+                                                                   SearchState st, int t) {
+  __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave], sb[SEL_THREADS / kWave];
+  __shared__ int si[SEL_THREADS / kWave];
+  const int r = blockIdx.x;
+  const int b = st.sent_list[r];
+  const float* rec = part + (size_t)r * n_tiles * 4;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  MaxSum acc{-INFINITY, 0.f};
+  float bv = -INFINITY;
+  int bi = INT_MAX;
+  for (int i = tid; i < n_tiles; i += SEL_THREADS) {
+    const float4 q = reinterpret_cast<const float4*>(rec)[i];
+    acc = ms_merge(acc, MaxSum{q.x, q.y});
+    const int qi = __float_as_int(q.w);
+    if (qi != INT_MAX && better(q.z, qi, bv, bi)) { bv = q.z; bi = qi; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+    const float ov = __shfl_xor(bv, o, kWave);
+    const int oi = __shfl_xor(bi, o, kWave);
+    if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+  }
+  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; sb[wave] = bv; si[wave] = bi; }
+  __syncthreads();
+  if (tid != 0 || st.done[b]) return;
+  MaxSum tot{sm[0], ss[0]};
+  float fb = sb[0];
+  int fi = si[0];
+  for (int w = 1; w < SEL_THREADS / kWave; ++w) {
+    tot = ms_merge(tot, MaxSum{sm[w], ss[w]});
+    if (better(sb[w], si[w], fb, fi)) { fb = sb[w]; fi = si[w]; }
+  }
+  const float lse = tot.m + logf(tot.s);
+  int tok = fi;
+  float lp = fb - lse;
+  if (tok < 0 || tok >= st.V) { tok = st.eos; lp = 0.f; }   // an all-NaN row: end the sentence
+  greedy_update(st, b, tok, lp, t);
 }
 
 // ---- beam: per-row LSE and top-2K logits -----------------------------------------------
@@ -228,6 +277,78 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
       int bi = INT_MAX;
       for (int q = 0; q < SEL_THREADS / kWave; ++q) {
         if (head[q] >= K2 || wi[q][head[q]] == INT_MAX) continue;     // list exhausted
+        if (bi == INT_MAX || better(wv[q][head[q]], wi[q][head[q]], bv, bi)) {
+          bv = wv[q][head[q]]; bi = wi[q][head[q]]; w = q;
+        }
+      }
+      head[w]++;
+      topv[(size_t)r * k2 + j] = bv;
+      topi[(size_t)r * k2 + j] = bi;
+    }
+    MaxSum tot{sm[0], ss[0]};
+#pragma unroll
+    for (int w = 1; w < SEL_THREADS / kWave; ++w) tot = ms_merge(tot, MaxSum{sm[w], ss[w]});
+    lse_out[r] = tot.m + logf(tot.s);
+  }
+}
+
+// Beam selection from the projection's per-tile partials [rows][n_tiles][2 + 2*k2]: each
+// tile's k2 best (value desc, index asc) and its (max, sum exp).  Same merge as
+// beam_select_kernel, over tile lists instead of logits.
+template <int K2>
+__global__ __launch_bounds__(SEL_THREADS) void beam_merge_kernel(const float* __restrict__ part, int n_tiles, int k2,
+                                                                 float* __restrict__ topv, int* __restrict__ topi,
+                                                                 float* __restrict__ lse_out) {
+  __shared__ float wv[SEL_THREADS / kWave][K2];
+  __shared__ int wi[SEL_THREADS / kWave][K2];
+  __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
+  const int r = blockIdx.x;
+  const int rs = 2 + 2 * k2;
+  const float* rec = part + (size_t)r * n_tiles * rs;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  MaxSum acc{-INFINITY, 0.f};
+  float v[K2];
+  int ix[K2];
+#pragma unroll
+  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
+  for (int i = tid; i < n_tiles; i += SEL_THREADS) {
+    const float* q = rec + (size_t)i * rs;
+    acc = ms_merge(acc, MaxSum{q[0], q[1]});
+    for (int j = 0; j < k2; ++j) {
+      const int qi = __float_as_int(q[3 + 2 * j]);
+      if (qi == INT_MAX) break;
+      list_insert<K2>(v, ix, q[2 + 2 * j], qi);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; }
+  for (int round = 0; round < K2; ++round) {
+    float bv = v[0];
+    int bi = ix[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (lane == 0) { wv[wave][round] = bv; wi[wave][round] = bi; }
+    if (ix[0] == bi && v[0] == bv && bi != INT_MAX) {
+#pragma unroll
+      for (int j = 0; j < K2 - 1; ++j) { v[j] = v[j + 1]; ix[j] = ix[j + 1]; }
+      v[K2 - 1] = -INFINITY;
+      ix[K2 - 1] = INT_MAX;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int head[SEL_THREADS / kWave] = {0, 0, 0, 0};
+    for (int j = 0; j < k2; ++j) {
+      int w = 0;
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+      for (int q = 0; q < SEL_THREADS / kWave; ++q) {
+        if (head[q] >= K2 || wi[q][head[q]] == INT_MAX) continue;
         if (bi == INT_MAX || better(wv[q][head[q]], wi[q][head[q]], bv, bi)) {
           bv = wv[q][head[q]]; bi = wi[q][head[q]]; w = q;
         }
@@ -462,6 +583,21 @@ __global__ void scatter_logits_kernel(const float* __restrict__ src, const int* 
 hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, int t, hipStream_t s) {
   if (st.n_live <= 0) return hipSuccess;
   hipLaunchKernelGGL(greedy_kernel, dim3(st.n_live), dim3(SEL_THREADS), 0, s, logits, forced, st, t);
+  return hipGetLastError();
+}
+
+hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, int t, hipStream_t s) {
+  if (st.n_live <= 0) return hipSuccess;
+  hipLaunchKernelGGL(greedy_fused_kernel, dim3(st.n_live), dim3(SEL_THREADS), 0, s, part, n_tiles, st, t);
+  return hipGetLastError();
+}
+
+hipError_t beam_merge(const float* part, int n_tiles, int rows, int k2, float* topv, int* topi, float* lse,
+                      hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (k2 > TOPK_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(beam_merge_kernel<TOPK_MAX>, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, k2, topv, topi,
+                     lse);
   return hipGetLastError();
 }
 
