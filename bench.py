@@ -42,6 +42,7 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="base-6-6", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graphs", action="store_true", help="replay each batch's decoder step as a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work for the oracle sample")
     ap.add_argument("--cpu-procs", type=int, default=0, help="oracle processes (0: min(16, cores))")
     return ap.parse_args()
@@ -129,6 +130,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     blob = synth.make_weights(w.model, seed=w.weights_seed)
     ids, offs = synth.make_sentences(w.data, w.model.vocab, seed=w.data_seed)
+    nt.nt_set_graphs(args.graphs)
     model = nt.Model(w.model, blob, w.dtype)
     sc = nt.search_cfg(w.search)
     ws_bytes = nt.nt_translate_workspace_size(model.handle, sc, offs)
@@ -185,6 +187,7 @@ def main():
             "source_tokens": int(offs[-1]), "target_tokens_per_step": n_tokens,
             "beam": w.search.beam, "token_budget": w.search.token_budget,
             "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
+            "decode_step_graphs": bool(args.graphs),
         },
         "roofline": roofline_entry(dominant, prof, w.dtype),
         "breakdown_ms_per_step": {k: round(v["ms"], 3) for k, v in breakdown.items()},

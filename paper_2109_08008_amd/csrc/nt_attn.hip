@@ -1,135 +1,187 @@
 // Attention kernels for gfx950.
 //
-// mha_kernel: groups of queries that share one set of keys -- encoder self-attention
-// (a group is a sentence and its tokens are the queries) and the decoder's
-// encoder-decoder attention (a group is a live sentence and its beam rows are the
-// queries; the sentence's cross keys/values, computed once per batch, are read once per
-// workgroup and shared by every hypothesis, Sec. 4.1 "Caching").  Keys stream through
-// LDS in chunks of 64; each wave carries 8 queries with an online (running max / sum)
-// fp32 softmax, so any key length works with a fixed LDS footprint.  Keys past the
-// group's length are masked (padding is inert).
-//
-// cross_attn_kernel: the decoder's encoder-decoder attention with one wave per (live
-// sentence, head); the sentence's beam rows are the wave's queries.
+// attn_mfma_kernel: groups of queries that share one set of keys, on the matrix cores --
+// encoder self-attention (a group is a sentence and its tokens are the queries) and the
+// decoder's encoder-decoder attention (a group is a live sentence and its beam rows are
+// the queries; the sentence's cross keys/values, computed once per batch, are read once
+// for all of its hypotheses, Sec. 4.1 "Caching").  Keys past the group's length are
+// masked (padding is inert).
 //
 // self_attn_kernel: one wave per (live row, head) attends over the row's cached
 // self-attention slots 0..t; with beam search a slot may live in the row of an
-// ancestor hypothesis (anc table), so beams never copy caches when they reorder.
+// ancestor hypothesis (anc table), so beams never copy caches when they reorder.  With
+// a single query per row this is a streaming kernel, not a contraction, so it stays on
+// the vector units.
 #include "nt_common.h"
 #include "nt_kernels.h"
 
 namespace nt {
 namespace {
 
-constexpr int QW = 8;        // queries per wave
-constexpr int KC = 64;       // keys per chunk
-constexpr int NW = 4;        // waves per workgroup
+constexpr int KC = 64;       // keys per chunk of the one-wave-per-row self-attention
 
+// Grouped attention on the matrix cores: one wave per (group, head, block of 16 queries).
+// Scores are formed transposed, S^T = K.Q^T, so lane l holds the scores of query l%16
+// for keys 4*(l/16)+r of each 16-key block; those are exactly the key slots the lane
+// supplies as the A operand of the P.V product (an MFMA only needs its two operands to
+// agree on which k each lane element carries), so P never leaves registers.  Values are
+// staged through a per-wave LDS tile and read key-major for the B operand.  Softmax is
+// exact within chunks of 128 keys (scores kept in registers) with an online rescale
+// between chunks; exponentials and sums are fp32, P enters P.V in the model dtype.  Keys
+// past the group's length get -inf scores (their value rows are clamped to a valid one).
 template <typename T, int DH, int ROLE>
-__global__ __launch_bounds__(256) void mha_kernel(MhaArgs a) {
-  constexpr int CPL = DH > 64 ? DH / 64 : 1;   // channels per lane in the P.V phase
-  __shared__ float Ks[KC][DH + 1];
-  __shared__ float Vs[KC][DH];
-  __shared__ float Qs[NW * QW][DH];
-  __shared__ float Ps[NW][KC][QW];
+__global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
+  constexpr int EB = sizeof(T);
+  constexpr int FE = 16 / EB;            // elements per 16-byte fragment
+  constexpr int KSTEP = 4 * FE;          // reduction length of one MFMA step (32 or 16)
+  constexpr int QK = DH / KSTEP;         // steps over the head dimension
+  constexpr int SB = KSTEP / 16;         // 16-key score blocks per P.V step
+  constexpr int CB = DH / 16;            // 16-channel output blocks
+  constexpr int NSB = 8;                 // score blocks per softmax chunk (128 keys)
+  constexpr int ROWP = DH * EB / 16;     // 16-byte pieces per key row
+  constexpr int VSTR = DH * EB / 4 + (EB == 2 ? 2 : 4);   // LDS row stride (dwords), spreads banks
+  static_assert(DH % KSTEP == 0 && NSB % SB == 0, "head dim must fill whole MFMA steps");
+  __shared__ __attribute__((aligned(16))) unsigned Vs[4][KSTEP][VSTR];
 
-  const int qblocks = (a.q_per_group + NW * QW - 1) / (NW * QW);
-  const int g = blockIdx.x / qblocks, qb = blockIdx.x % qblocks;
-  const int h = blockIdx.y;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int grp = lane >> 4, ln = lane & 15;
+  const int qblocks = (a.q_per_group + 15) / 16;
+  const int n_groups = a.ctl ? min(a.n_groups, a.ctl[CTL_NLIVE]) : a.n_groups;
+  const int task = blockIdx.x * 4 + wave;
+  if (task >= n_groups * a.H * qblocks) return;   // whole wave; wave-local sync only below
+  const int qb = task % qblocks, gh = task / qblocks;
+  const int h = gh % a.H, g = gh / a.H;
   const int b = a.group_map ? a.group_map[g] : g;
   const int len = a.lens[b];
   const int nq = a.self_queries ? min(len, a.q_per_group) : a.q_per_group;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-
-  const T* Q = static_cast<const T*>(a.q);
-  const T* Kp = static_cast<const T*>(a.k) + (size_t)b * a.kb + (size_t)h * a.kh;
-  const T* Vp = static_cast<const T*>(a.v) + (size_t)b * a.kb + (size_t)h * a.kh;
-
-  // queries of this workgroup -> LDS, pre-scaled by 1/sqrt(dh)
-  for (int idx = tid; idx < NW * QW * DH; idx += 256) {
-    const int qi = idx / DH, e = idx % DH;
-    const int i = qb * NW * QW + qi;
-    float v = 0.f;
-    if (i < nq) v = to_f32(Q[(size_t)(g * a.q_per_group + i) * a.q_ld + h * DH + e]) * a.scale;
-    Qs[qi][e] = v;
-  }
-
-  float m[QW], l[QW], o[QW][CPL];
-#pragma unroll
-  for (int j = 0; j < QW; ++j) {
-    m[j] = -INFINITY;
-    l[j] = 0.f;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) o[j][c] = 0.f;
-  }
-
-  for (int c0 = 0; c0 < len; c0 += KC) {
-    __syncthreads();
-    for (int idx = tid; idx < KC * DH; idx += 256) {
-      const int r = idx / DH, e = idx % DH;
-      const int s = c0 + r;
-      float kv = 0.f, vv = 0.f;
-      if (s < len) {
-        kv = to_f32(Kp[(size_t)s * a.ks + e]);
-        vv = to_f32(Vp[(size_t)s * a.ks + e]);
-      }
-      Ks[r][e] = kv;
-      Vs[r][e] = vv;
-    }
-    __syncthreads();
-
-    // scores: lane = key
-    const bool valid = c0 + lane < len;
-    float sc[QW];
-#pragma unroll
-    for (int j = 0; j < QW; ++j) sc[j] = 0.f;
-#pragma unroll 8
-    for (int e = 0; e < DH; ++e) {
-      const float kv = Ks[lane][e];
-#pragma unroll
-      for (int j = 0; j < QW; ++j) sc[j] += Qs[wave * QW + j][e] * kv;
-    }
-#pragma unroll
-    for (int j = 0; j < QW; ++j) {
-      const float s = valid ? sc[j] : -INFINITY;
-      const float mn = fmaxf(m[j], wave_max(s));
-      const float p = valid ? expf(s - mn) : 0.f;
-      const float alpha = expf(m[j] - mn);
-      l[j] = l[j] * alpha + wave_sum(p);
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) o[j][c] *= alpha;
-      m[j] = mn;
-      Ps[wave][lane][j] = p;
-    }
-    __syncthreads();
-
-    // P.V: lane = channel
-    const int kmax = min(KC, len - c0);
-    for (int k = 0; k < kmax; ++k) {
-      const float4 p0 = *reinterpret_cast<const float4*>(&Ps[wave][k][0]);
-      const float4 p1 = *reinterpret_cast<const float4*>(&Ps[wave][k][4]);
-      const float pk[QW] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        const int e = lane * CPL + c;
-        const float v = e < DH ? Vs[k][e] : 0.f;
-#pragma unroll
-        for (int j = 0; j < QW; ++j) o[j][c] += pk[j] * v;
-      }
-    }
-  }
-
+  const int q0 = qb * 16;
   T* out = static_cast<T*>(a.out);
+  auto out_at = [&](int i, int ch) -> T* { return out + (size_t)(g * a.q_per_group + i) * a.out_ld + h * DH + ch; };
+
+  if (q0 >= nq) {                                  // a block of padding queries: zero rows
 #pragma unroll
-  for (int j = 0; j < QW; ++j) {
-    const int i = qb * NW * QW + wave * QW + j;
-    if (i >= a.q_per_group) continue;
-    const size_t row = (size_t)(g * a.q_per_group + i) * a.out_ld + h * DH;
+    for (int r = 0; r < 4; ++r) {
+      const int i = q0 + 4 * grp + r;
+      if (i < a.q_per_group)
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      const int e = lane * CPL + c;
-      if (e < DH) out[row + e] = from_f32<T>(i < nq ? o[j][c] / l[j] : 0.f);
+        for (int c = 0; c < CB; ++c) *out_at(i, c * 16 + ln) = from_f32<T>(0.f);
     }
+    return;
+  }
+
+  const size_t ks_b = (size_t)a.ks * EB;
+  const char* Kb = reinterpret_cast<const char*>(static_cast<const T*>(a.k) + (size_t)b * a.kb + (size_t)h * a.kh);
+  const char* Vb = reinterpret_cast<const char*>(static_cast<const T*>(a.v) + (size_t)b * a.kb + (size_t)h * a.kh);
+  const char* qrow = reinterpret_cast<const char*>(static_cast<const T*>(a.q) +
+                                                   (size_t)(g * a.q_per_group + min(q0 + ln, nq - 1)) * a.q_ld +
+                                                   h * DH);
+  u32x4 qf[QK];
+#pragma unroll
+  for (int st = 0; st < QK; ++st) qf[st] = *reinterpret_cast<const u32x4*>(qrow + st * 64 + grp * 16);
+
+  float m = -INFINITY, lsum = 0.f;   // running max / sum of query q0+ln (same in all 4 groups)
+  floatx4 o[CB];                     // O[q0 + 4*grp + r][c*16 + ln]
+#pragma unroll
+  for (int c = 0; c < CB; ++c) o[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const unsigned short* vh = reinterpret_cast<const unsigned short*>(&Vs[wave][0][0]);
+
+  for (int c0 = 0; c0 < len; c0 += NSB * 16) {
+    const int nb = min(NSB, (len - c0 + 15) / 16);
+    floatx4 sc[NSB];
+    float cmax = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NSB; ++kb) {
+      sc[kb] = floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      if (kb < nb) {
+        const char* krow = Kb + (size_t)min(c0 + kb * 16 + ln, len - 1) * ks_b;
+        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < QK; ++st)
+          acc = Mfma<T>::step(*reinterpret_cast<const u32x4*>(krow + st * 64 + grp * 16), qf[st], acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = c0 + kb * 16 + 4 * grp + r;
+          sc[kb][r] = key < len ? acc[r] * a.scale : -INFINITY;
+          cmax = fmaxf(cmax, sc[kb][r]);
+        }
+      }
+    }
+    cmax = fmaxf(cmax, __shfl_xor(cmax, 16, kWave));
+    cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));
+    const float mn = fmaxf(m, cmax);
+    const float alpha = __expf(m - mn);              // 0 on the first chunk
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < NSB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        sc[kb][r] = __expf(sc[kb][r] - mn);
+        psum += sc[kb][r];
+      }
+    psum += __shfl_xor(psum, 16, kWave);
+    psum += __shfl_xor(psum, 32, kWave);
+    lsum = lsum * alpha + psum;
+    m = mn;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float ar = __shfl(alpha, 4 * grp + r, kWave);   // alpha of query q0 + 4*grp + r
+#pragma unroll
+      for (int c = 0; c < CB; ++c) o[c][r] *= ar;
+    }
+
+    for (int kb = 0; kb < nb; kb += SB) {
+      // value rows c0 + kb*16 .. + KSTEP -> LDS (8-byte writes; rows past len clamped)
+#pragma unroll
+      for (int pc = lane; pc < KSTEP * ROWP; pc += kWave) {
+        const int row = pc / ROWP, col = pc % ROWP;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(Vb + (size_t)min(c0 + kb * 16 + row, len - 1) * ks_b + col * 16);
+        unsigned* dst = &Vs[wave][row][col * 4];
+        *reinterpret_cast<uint2*>(dst) = make_uint2(v.x, v.y);
+        *reinterpret_cast<uint2*>(dst + 2) = make_uint2(v.z, v.w);
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      // A operand: P of query ln at keys 16*(kb+j) + 4*grp + r, in the model dtype
+      u32x4 pf;
+      if constexpr (EB == 2) {
+        T pe[8];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) pe[4 * j + r] = from_f32<T>(sc[kb + j][r]);
+        pf = __builtin_bit_cast(u32x4, pe);
+      } else {
+        pf = __builtin_bit_cast(u32x4, sc[kb]);
+      }
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        // B operand: V[key 16*j + 4*grp + r][channel c*16 + ln], same key order as pf
+        u32x4 vf;
+        if constexpr (EB == 2) {
+          unsigned short e[8];
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) e[4 * j + r] = vh[(16 * j + 4 * grp + r) * (VSTR * 2) + c * 16 + ln];
+          vf = __builtin_bit_cast(u32x4, e);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) vf[r] = Vs[wave][4 * grp + r][c * 16 + ln];
+        }
+        o[c] = Mfma<T>::step(pf, vf, o[c]);
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    }
+  }
+
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = q0 + 4 * grp + r;
+    const float inv = 1.0f / __shfl(lsum, 4 * grp + r, kWave);
+    if (i >= a.q_per_group) continue;
+#pragma unroll
+    for (int c = 0; c < CB; ++c) *out_at(i, c * 16 + ln) = from_f32<T>(i < nq ? o[c][r] * inv : 0.f);
   }
 }
 
@@ -210,54 +262,12 @@ __device__ __forceinline__ void wave_attend(const float (&Qs)[KQ][DH], float (&P
   }
 }
 
-// Encoder-decoder attention of the decoder step: one wave per (live sentence, head).
-// The KQ beam rows of a sentence share its cross keys/values, so the wave reads each
-// key and value of the sentence once for all of them.
 // Waves per workgroup for the one-wave-per-task attention kernels: as many as fit in
 // 64 KB of LDS (so two workgroups share a CU), at most 4.
 template <typename T, int DH, int KQ>
 constexpr int attn_waves() {
   constexpr int per_wave = KQ * DH * 4 + KQ * KC * 4 + KC * (DH + 8) * (int)sizeof(T);
   return per_wave * 4 <= 65536 ? 4 : per_wave * 2 <= 65536 ? 2 : 1;
-}
-
-template <typename T, int DH, int KQ>
-__global__ __launch_bounds__(256) void cross_attn_kernel(MhaArgs a) {
-  constexpr int CPL = DH > 64 ? DH / 64 : 1;
-  constexpr int NWV = attn_waves<T, DH, KQ>();
-  __shared__ float Qs[NWV][KQ][DH];
-  __shared__ float Ps[NWV][KQ][KC];
-  __shared__ __attribute__((aligned(16))) T Vs[NWV][KC][DH + 8];
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int pair = blockIdx.x * NWV + wave;
-  if (pair >= a.n_groups * a.H) return;          // whole wave exits; no block barrier below
-  const int g = pair / a.H, h = pair % a.H;
-  const int b = a.group_map ? a.group_map[g] : g;
-  const int len = a.lens[b];
-  const int nq = a.q_per_group;                  // <= KQ
-  const T* Q = static_cast<const T*>(a.q);
-  for (int idx = lane; idx < KQ * DH; idx += kWave) {
-    const int i = idx / DH, e = idx % DH;
-    Qs[wave][i][e] = i < nq ? to_f32(Q[(size_t)(g * nq + i) * a.q_ld + h * DH + e]) * a.scale : 0.f;
-  }
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  const T* Kp = static_cast<const T*>(a.k) + (size_t)b * a.kb + (size_t)h * a.kh;
-  const T* Vp = static_cast<const T*>(a.v) + (size_t)b * a.kb + (size_t)h * a.kh;
-  const long long ks = a.ks;
-  float o[KQ][CPL], l[KQ];
-  wave_attend<T, DH, KQ>(Qs[wave], Ps[wave], Vs[wave], len, Kp, Vp, [&](int s) { return (size_t)s * ks; }, o, l);
-  T* out = static_cast<T*>(a.out);
-#pragma unroll
-  for (int i = 0; i < KQ; ++i) {
-    if (i >= nq) continue;
-    const float inv = 1.0f / l[i];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      const int e = lane * CPL + c;
-      if (e < DH) out[(size_t)(g * nq + i) * a.out_ld + h * DH + e] = from_f32<T>(o[i][c] * inv);
-    }
-  }
 }
 
 // Decoder self-attention: one wave per (live row, head) over the row's cached slots
@@ -272,7 +282,8 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   __shared__ __attribute__((aligned(16))) T Vs[NWV][KC][DH + 8];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int pair = blockIdx.x * NWV + wave;
-  if (pair >= a.rows * a.H) return;            // whole wave exits; no block barrier below
+  const int rows = min(a.rows, a.ctl[CTL_NLIVE] * a.beam);
+  if (pair >= rows * a.H) return;              // whole wave exits; no block barrier below
   const int row = pair / a.H, h = pair % a.H;
   const int p = a.sent_list[row / a.beam] * a.beam + row % a.beam;
   const T* q = static_cast<const T*>(a.q) + (size_t)row * a.H * DH + h * DH;
@@ -281,8 +292,8 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   const size_t head = (size_t)h * a.Tcap * DH;
   const size_t row_stride = (size_t)a.H * a.Tcap * DH;
-  const int* anc = a.anc ? a.anc + (size_t)p * a.Tcap : nullptr;
-  const int t = a.t;
+  const int* anc = a.anc ? a.anc + (size_t)a.ctl[CTL_ANC] * a.anc_stride + (size_t)p * a.Tcap : nullptr;
+  const int t = a.ctl[CTL_T];
   auto row_of = [&](int s) {
     const int ph = (anc && s < t) ? anc[s] : p;
     return (size_t)ph * row_stride + (size_t)s * DH;
@@ -299,41 +310,14 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   }
 }
 
-template <typename T, int DH, int KQ>
-void cross_launch(const MhaArgs& a, hipStream_t s) {
-  constexpr int NWV = attn_waves<T, DH, KQ>();
-  const dim3 grid((a.n_groups * a.H + NWV - 1) / NWV);
-  hipLaunchKernelGGL((cross_attn_kernel<T, DH, KQ>), grid, dim3(NWV * kWave), 0, s, a);
-}
-
-template <typename T, int DH>
-hipError_t cross_t(const MhaArgs& a, hipStream_t s) {
-  const int q = a.q_per_group;
-  if (q <= 1) cross_launch<T, DH, 1>(a, s);
-  else if (q <= 2) cross_launch<T, DH, 2>(a, s);
-  else if (q <= 4) cross_launch<T, DH, 4>(a, s);
-  else if (q <= 8) cross_launch<T, DH, 8>(a, s);
-  else if (q <= 16) cross_launch<T, DH, 16>(a, s);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
 template <typename T, int ROLE>
 hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
-  if (ROLE == 1 && !a.self_queries) {
-    switch (a.dh) {
-      case 32: return cross_t<T, 32>(a, s);
-      case 64: return cross_t<T, 64>(a, s);
-      case 128: return cross_t<T, 128>(a, s);
-      default: return hipErrorInvalidValue;
-    }
-  }
-  const int qblocks = (a.q_per_group + NW * QW - 1) / (NW * QW);
-  const dim3 grid(a.n_groups * qblocks, a.H);
+  const long long tasks = (long long)a.n_groups * a.H * ((a.q_per_group + 15) / 16);
+  const dim3 grid((unsigned)((tasks + 3) / 4));
   switch (a.dh) {
-    case 32: hipLaunchKernelGGL((mha_kernel<T, 32, ROLE>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((mha_kernel<T, 64, ROLE>), grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((mha_kernel<T, 128, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((attn_mfma_kernel<T, 32, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((attn_mfma_kernel<T, 64, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((attn_mfma_kernel<T, 128, ROLE>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -14,6 +14,41 @@ constexpr int kWave = 64;
 template <typename T> __device__ __forceinline__ float to_f32(T v) { return static_cast<float>(v); }
 template <typename T> __device__ __forceinline__ T from_f32(float v) { return static_cast<T>(v); }
 
+// One MFMA step over a 16-byte fragment per lane: 16x16 fp32 accumulator C += A.B^T
+// with lane l supplying row (l % 16) of A and of B^T at k-chunk (l / 16); only the two
+// operands' agreement on which k a lane element carries matters.  fp16/bf16 use
+// v_mfma_f32_16x16x32_{f16,bf16} (k = 32); fp32 uses four v_mfma_f32_16x16x4_f32 (true
+// fp32 products, k = 16).  Lane l receives C[4*(l/16) + r][l % 16] in element r.
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bhalf8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Mfma;
+template <> struct Mfma<f16> {
+  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c,
+                                                  0, 0, 0);
+  }
+};
+template <> struct Mfma<bf16> {
+  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bhalf8, a), __builtin_bit_cast(bhalf8, b),
+                                                   c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<float> {
+  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
+    const floatx4 av = __builtin_bit_cast(floatx4, a);
+    const floatx4 bv = __builtin_bit_cast(floatx4, b);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, c, 0, 0, 0);
+    return c;
+  }
+};
+
 // Elements of T in one 16-byte vector.
 template <typename T> struct Vec { static constexpr int N = 16 / sizeof(T); };
 

@@ -32,36 +32,6 @@ constexpr int ROWB = 128;           // bytes of K per tile row per step
 constexpr int CH = ROWB / 16;       // 16-byte chunks per tile row
 constexpr int NTHR = 256;
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bhalf8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-
-template <typename T> struct Mfma;
-template <> struct Mfma<f16> {
-  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c,
-                                                  0, 0, 0);
-  }
-};
-template <> struct Mfma<bf16> {
-  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bhalf8, a), __builtin_bit_cast(bhalf8, b),
-                                                   c, 0, 0, 0);
-  }
-};
-template <> struct Mfma<float> {
-  static __device__ __forceinline__ floatx4 step(u32x4 a, u32x4 b, floatx4 c) {
-    const floatx4 av = __builtin_bit_cast(floatx4, a);
-    const floatx4 bv = __builtin_bit_cast(floatx4, b);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, c, 0, 0, 0);
-    return c;
-  }
-};
-
 // Byte offset of 16-byte chunk `ch` of tile row `row` in a swizzled LDS tile.
 __device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ (row & 7)) << 4); }
 
@@ -69,7 +39,7 @@ __device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^
 // d, dh and ldc are multiples of 4 in every mode that scatters, so the 4 columns never
 // straddle a head or a K/V boundary and land on 4 consecutive destination elements.
 template <typename T>
-__device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N, float4 v4) {
+__device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N, float4 v4, int t_slot) {
   float v[4] = {v4.x, v4.y, v4.z, v4.w};
   const int cnt = min(4, N - n);
   if (e.bias) {
@@ -116,7 +86,7 @@ __device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N,
         c -= kv * e.d;
         const int h = c / e.dh, x = c - h * e.dh;
         const int p = e.sent_list[m / e.beam] * e.beam + m % e.beam;
-        o = static_cast<T*>(kv ? e.vcache : e.kcache) + ((size_t)(p * e.H + h) * e.Tcap + e.t) * e.dh + x;
+        o = static_cast<T*>(kv ? e.vcache : e.kcache) + ((size_t)(p * e.H + h) * e.Tcap + t_slot) * e.dh + x;
       }
       break;
     }
@@ -315,6 +285,10 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   const int tm = first_m + (pid % per_group) % gsize;
   const int tn = (pid % per_group) / gsize;
   const int m0 = tm * BM_, n0 = tn * BN_;
+  // live rows of a decode step (the grid covers the whole batch)
+  if (epi.ctl) M = min(M, epi.ctl[CTL_NLIVE] * epi.ctl_rows);
+  if (m0 >= M) return;
+  const int t_slot = epi.ctl ? epi.ctl[CTL_T] : epi.t;
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const size_t lda_b = (size_t)lda * sizeof(T), ldb_b = (size_t)K * sizeof(T);
@@ -407,7 +381,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     for (int g = tid; g < ER * (BN_ / 4); g += NTHR) {
       const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
       const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
-      if (m < M && n < N) epilogue4<T>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]));
+      if (m < M && n < N) epilogue4<T>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), t_slot);
     }
   }
 }

@@ -9,6 +9,21 @@
 namespace nt {
 
 enum class DT : int { F32 = 0, F16 = 1, BF16 = 2 };
+
+// Decode-step control block in device memory.  Every decoder-step kernel reads the step
+// index and the live counts from it (grids are sized for the whole batch and surplus
+// workgroups return at once), and the step-end kernel advances it, so the kernel
+// sequence of one step can be captured once and replayed for every step.
+enum CtlField : int {
+  CTL_T = 0,        // current step t
+  CTL_NLIVE = 1,    // entries of the live-sentence list the step works on
+  CTL_NALIVE = 2,   // sentences not finished yet
+  CTL_ANC = 3,      // which half of the ancestor table is current (beam)
+  CTL_WORDS = 4
+};
+// The step-end kernel also copies the new block into slot (t % CTL_MIRROR_SLOTS) of a
+// pinned host mirror, so the host can read step t's outcome while later steps run.
+constexpr int CTL_MIRROR_SLOTS = 4;
 inline size_t dt_bytes(DT t) { return t == DT::F32 ? 4 : 2; }
 
 // ---------------------------------------------------------------------------------
@@ -27,6 +42,8 @@ constexpr int TOPK_MAX = 8;   // k2 of the fused selection (greedy 1, beam up to
 __host__ __device__ inline int topk_record(int k2) { return 2 + 2 * k2; }   // floats per partial record
 
 struct GemmEpi {
+  const int* ctl = nullptr;        // if set, M = ctl[CTL_NLIVE] * ctl_rows (<= the launch M),
+  int ctl_rows = 1;                //   and EPI_SELF_QKV writes slot ctl[CTL_T]
   int mode = EPI_STORE;
   const float* bias = nullptr;   // [N] fp32 or null
   const void* resid = nullptr;   // [M][ldc], same type as out
@@ -81,12 +98,15 @@ struct DlclArgs {
 };
 hipError_t dlcl_combine(DT dt, const DlclArgs& a, hipStream_t s);
 
-// y = LN(x) row-wise; gamma|beta at ln[0..d), ln[d..2d).
-hipError_t layernorm(DT dt, const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s);
+// y = LN(x) row-wise; gamma|beta at ln[0..d), ln[d..2d).  With ctl, the live row count is
+// ctl[CTL_NLIVE] * ctl_rows (rows is then the launch maximum).
+hipError_t layernorm(DT dt, const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s,
+                     const int* ctl = nullptr, int ctl_rows = 1);
 
-// Decoder step input: z[r] = emb_scale*E[tok[phys(r)]] + pe[t]; u[r] = LN(z[r]).
+// Decoder step input: z[r] = emb_scale*E[tok[phys(r)]] + pe[t]; u[r] = LN(z[r]); rows and t
+// from ctl (rows = ctl[CTL_NLIVE] * beam, t = ctl[CTL_T]), `rows` being the launch maximum.
 hipError_t dec_embed_ln(DT dt, const int* cur_tok, const int* sent_list, int beam, const void* E,
-                        const float* pe, int t, float emb_scale, const float* ln, void* z, void* u,
+                        const float* pe, const int* ctl, float emb_scale, const float* ln, void* z, void* u,
                         int rows, int d, float eps, hipStream_t s);
 
 // Weight packing: dst[n][k] = (T) src[k][n] (src fp32 [K][N] row-major).
@@ -109,8 +129,9 @@ struct MhaArgs {
   const int* lens;               // [b] valid keys (and valid queries for self-attention)
   int q_per_group;               // queries of group g are rows g*q_per_group + i
   int self_queries;              // 1: query i valid only if i < lens[b] (padded rows -> 0)
-  int n_groups, H, dh;
+  int n_groups, H, dh;           // n_groups: launch maximum when ctl is set
   float scale;
+  const int* ctl = nullptr;      // if set, the live group count is ctl[CTL_NLIVE]
 };
 // role: 0 encoder self-attention, 1 encoder-decoder attention (symbol name only).
 hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s, int role = 0);
@@ -120,10 +141,12 @@ struct SelfAttnArgs {
   const void* q;              // [rows][d]
   const void* kcache; const void* vcache;  // [R][H][Tcap][dh]
   const int* sent_list; int beam;
-  const int* anc;             // [R][Tcap] physical row holding slot s (null: own row)
+  const int* anc;             // [2][R][Tcap] physical row holding slot s (null: own row);
+  size_t anc_stride;          //   half ctl[CTL_ANC] is current
   void* out;                  // [rows][d]
-  int rows, H, dh, t, Tcap;
+  int rows, H, dh, Tcap;      // rows: launch maximum; live rows = ctl[CTL_NLIVE] * beam
   float scale;
+  const int* ctl;             // step t = ctl[CTL_T]
 };
 hipError_t self_attn(DT dt, const SelfAttnArgs& a, hipStream_t s);
 
@@ -134,14 +157,14 @@ struct SearchState {
   float alpha;
   int early_stop;
   const int* sent_list;   // live sentences (logical order)
-  int n_live;             // entries in sent_list
+  const int* ctl;         // t = ctl[CTL_T], live list entries = ctl[CTL_NLIVE]
   float* score;           // [R] raw hypothesis scores
   int* cur_tok;           // [R] next input token
   int* tok_hist;          // [Tcap][R]
   int* par_hist;          // [Tcap][R]
   float* lp_hist;         // [Tcap][R]
-  const int* anc_cur;     // [R][Tcap]
-  int* anc_next;
+  int* anc;               // [2][R][Tcap]; half ctl[CTL_ANC] is current, the other is written
+  size_t anc_stride;
   int* done;              // [B]
   const int* maxlen;      // [B]
   float* best_score;      // [B] normalised
@@ -153,34 +176,41 @@ struct SearchState {
 
 // Greedy: per live row, argmax (lowest ID on ties) and log-sum-exp over V logits, then
 // the update (token, log-prob, EOS / length stop).  forced: [R] (by phys row) or null.
-hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, int t, hipStream_t s);
+// Grids cover the whole batch (st.B * st.beam rows); rows past the live count return.
+hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, hipStream_t s);
 
 // Beam: per live row, log-sum-exp and the 2K largest logits; then per live sentence the
 // candidate ranking, the walk, the stop rule and the ancestor-table update.
-hipError_t beam_select(const float* logits, int rows, int V, int k2, float* topv, int* topi, float* lse,
-                       hipStream_t s);
-hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, int t,
-                       hipStream_t s);
+hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, int V, int k2, float* topv, int* topi,
+                       float* lse, hipStream_t s);
+hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, hipStream_t s);
 
 // Fused selection after an EPI_TOPK projection: merge the per-tile partials of each live
 // row.  Greedy: argmax + LSE, then the greedy update.  Beam: top-k2 + LSE into
 // topv/topi/lse for beam_update.
-hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, int t, hipStream_t s);
-hipError_t beam_merge(const float* part, int n_tiles, int rows, int k2, float* topv, int* topi, float* lse,
-                      hipStream_t s);
+hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, hipStream_t s);
+hipError_t beam_merge(const float* part, int n_tiles, const int* ctl, int beam, int rows, int k2, float* topv,
+                      int* topi, float* lse, hipStream_t s);
 
-// Compaction: new_list = [b in list if !done[b]] in order; count -> *n_out (device).
-hipError_t compact(const int* list, int n, const int* done, int* new_list, int* n_out, hipStream_t s);
+// End of a decode step (one workgroup): counts the unfinished sentences of the live list,
+// drops the finished ones in place when pruning, advances t, flips the ancestor half
+// (beam) and writes the new block into ctl and, if host_ctl is set (a device-visible
+// pointer to pinned host memory of CTL_MIRROR_SLOTS * CTL_WORDS ints), into its mirror
+// slot.  Once nothing is alive, or t reaches Tcap, the live count is 0: later steps,
+// this kernel included, do nothing.
+hipError_t step_end(int* list, const int* done, int* ctl, int* host_ctl, int prune, int beam, int Tcap,
+                    hipStream_t s);
 
 // Backtrack every sentence's best hypothesis into out_tok/out_lp [B][Tcap], out_len/out_score [B].
 hipError_t finalize(const SearchState& st, int* out_tok, float* out_lp, int* out_len, float* out_score,
                     hipStream_t s);
 
-// Initialise per-batch search state (scores 0 / -inf, BOS, best = -inf, done = 0, identity list).
-hipError_t search_init(const SearchState& st, int* list, int bos, hipStream_t s);
+// Initialise per-batch search state (scores 0 / -inf, BOS, best = -inf, done = 0, identity
+// list) and the control block (t = 0, all B sentences live and alive).
+hipError_t search_init(const SearchState& st, int* list, int* ctl, int bos, hipStream_t s);
 
-// Scatter rows of the compact logits [rows][V] to dst[phys(r)][V].
-hipError_t scatter_logits(const float* logits, const int* sent_list, int beam, int rows, int V, float* dst,
-                          hipStream_t s);
+// Scatter the live rows of the compact logits [rows][V] to dst[phys(r)][V].
+hipError_t scatter_logits(const float* logits, const int* sent_list, const int* ctl, int beam, int rows, int V,
+                          float* dst, hipStream_t s);
 
 }  // namespace nt

@@ -86,8 +86,10 @@ __global__ __launch_bounds__(256) void dlcl_kernel(DlclArgs a) {
 
 template <typename T, int EPL>
 __global__ __launch_bounds__(256) void ln_kernel(const T* __restrict__ x, const float* __restrict__ ln,
-                                                 T* __restrict__ y, int rows, int d, float eps) {
+                                                 T* __restrict__ y, int rows, int d, float eps, const int* ctl,
+                                                 int ctl_rows) {
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
+  if (ctl) rows = min(rows, ctl[CTL_NLIVE] * ctl_rows);
   if (row >= rows) return;
   const int c0 = (threadIdx.x % kWave) * EPL;
   float v[EPL], o[EPL];
@@ -101,11 +103,12 @@ template <typename T, int EPL>
 __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ cur_tok,
                                                         const int* __restrict__ sent_list, int beam,
                                                         const T* __restrict__ E, const float* __restrict__ pe,
-                                                        int t, float scale, const float* __restrict__ ln,
-                                                        T* __restrict__ z, T* __restrict__ u, int rows, int d,
-                                                        float eps) {
+                                                        const int* __restrict__ ctl, float scale,
+                                                        const float* __restrict__ ln, T* __restrict__ z,
+                                                        T* __restrict__ u, int rows, int d, float eps) {
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
-  if (row >= rows) return;
+  if (row >= min(rows, ctl[CTL_NLIVE] * beam)) return;
+  const int t = ctl[CTL_T];
   const int c0 = (threadIdx.x % kWave) * EPL;
   const int p = sent_list[row / beam] * beam + row % beam;
   float v[EPL], o[EPL];
@@ -164,22 +167,24 @@ hipError_t dlcl_t(const DlclArgs& a, hipStream_t s) {
 }
 
 template <typename T>
-hipError_t ln_t(const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s) {
+hipError_t ln_t(const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s, const int* ctl,
+                int ctl_rows) {
   const dim3 grid((rows + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
-#define NT_CALL(E) \
-  hipLaunchKernelGGL((ln_kernel<T, E>), grid, dim3(256), 0, s, static_cast<const T*>(x), ln, static_cast<T*>(y), rows, d, eps)
+#define NT_CALL(E)                                                                                            \
+  hipLaunchKernelGGL((ln_kernel<T, E>), grid, dim3(256), 0, s, static_cast<const T*>(x), ln, static_cast<T*>(y), \
+                     rows, d, eps, ctl, ctl_rows)
   NT_EPL_SWITCH(d, NT_CALL)
 #undef NT_CALL
   return hipGetLastError();
 }
 
 template <typename T>
-hipError_t emb_t(const int* cur_tok, const int* sent_list, int beam, const void* E, const float* pe, int t,
+hipError_t emb_t(const int* cur_tok, const int* sent_list, int beam, const void* E, const float* pe, const int* ctl,
                  float scale, const float* ln, void* z, void* u, int rows, int d, float eps, hipStream_t s) {
   const dim3 grid((rows + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
-#define NT_CALL(EP)                                                                                          \
-  hipLaunchKernelGGL((dec_embed_kernel<T, EP>), grid, dim3(256), 0, s, cur_tok, sent_list, beam,             \
-                     static_cast<const T*>(E), pe, t, scale, ln, static_cast<T*>(z), static_cast<T*>(u), rows, \
+#define NT_CALL(EP)                                                                                            \
+  hipLaunchKernelGGL((dec_embed_kernel<T, EP>), grid, dim3(256), 0, s, cur_tok, sent_list, beam,               \
+                     static_cast<const T*>(E), pe, ctl, scale, ln, static_cast<T*>(z), static_cast<T*>(u), rows, \
                      d, eps)
   NT_EPL_SWITCH(d, NT_CALL)
 #undef NT_CALL
@@ -201,16 +206,17 @@ hipError_t dlcl_combine(DT dt, const DlclArgs& a, hipStream_t s) {
   NT_DT_SWITCH(dt, dlcl_t, a, s)
 }
 
-hipError_t layernorm(DT dt, const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s) {
+hipError_t layernorm(DT dt, const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s,
+                     const int* ctl, int ctl_rows) {
   if (rows <= 0) return hipSuccess;
-  NT_DT_SWITCH(dt, ln_t, x, ln, y, rows, d, eps, s)
+  NT_DT_SWITCH(dt, ln_t, x, ln, y, rows, d, eps, s, ctl, ctl_rows)
 }
 
 hipError_t dec_embed_ln(DT dt, const int* cur_tok, const int* sent_list, int beam, const void* E, const float* pe,
-                        int t, float emb_scale, const float* ln, void* z, void* u, int rows, int d, float eps,
-                        hipStream_t s) {
+                        const int* ctl, float emb_scale, const float* ln, void* z, void* u, int rows, int d,
+                        float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  NT_DT_SWITCH(dt, emb_t, cur_tok, sent_list, beam, E, pe, t, emb_scale, ln, z, u, rows, d, eps, s)
+  NT_DT_SWITCH(dt, emb_t, cur_tok, sent_list, beam, E, pe, ctl, emb_scale, ln, z, u, rows, d, eps, s)
 }
 
 namespace {

@@ -17,6 +17,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 #include <numeric>
 #include <string>
@@ -82,11 +83,30 @@ hipEvent_t prof_event() {
   return e;
 }
 
+// How launches of enabled classes are timed on this thread: every stride-th launch of a
+// class (direct launches), never (while a step is being captured into a graph), or every
+// launch (a sampled step of a graph-replayed decode, issued directly).
+enum ProfMode { PROF_STRIDE = 0, PROF_NONE = 1, PROF_ALL = 2 };
+thread_local int g_prof_mode = PROF_STRIDE;
+int64_t g_prof_steps = 0;   // decode steps seen while profiling (graph mode samples every stride-th)
+std::atomic<bool> g_use_graphs{false};  // nt_translate replays a captured decode step
+
+struct ProfModeScope {
+  int saved;
+  explicit ProfModeScope(int m) : saved(g_prof_mode) { g_prof_mode = m; }
+  ~ProfModeScope() { g_prof_mode = saved; }
+};
+
+bool prof_step_sampled() {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  return g_prof_mask != 0 && g_prof_steps++ % g_prof_stride == 0;
+}
+
 template <typename F>
 hipError_t timed(int cls, hipStream_t s, double bytes, double flops, F&& launch) {
-  if (!(g_prof_mask & (1u << cls))) return launch();
+  if (g_prof_mode == PROF_NONE || !(g_prof_mask & (1u << cls))) return launch();
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  if (g_prof_seen[cls]++ % g_prof_stride != 0) return launch();
+  if (g_prof_mode == PROF_STRIDE && g_prof_seen[cls]++ % g_prof_stride != 0) return launch();
   hipEvent_t a = prof_event(), b = prof_event();
   if (!a || !b) return hipErrorOutOfMemory;
   hipError_t e = hipEventRecord(a, s);
@@ -274,7 +294,7 @@ struct WsPlan {
   // persistent through the batch
   size_t src, len, maxlen, enc_out, cross;
   size_t kself, vself, score, cur_tok, tok_hist, par_hist, lp_hist, anc, done, best_score, best_raw, best_step,
-      best_row, best_nout, list, count, out_tok, out_lp, out_len, out_score;
+      best_row, best_nout, list, ctl, out_tok, out_lp, out_len, out_score;
   // encoder temporaries (union with the decoder buffers below)
   size_t hist, x, u, qkv, att, a, f, y;
   // decoder buffers
@@ -309,8 +329,8 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.best_step = take(B * 4);
   p.best_row = take(B * 4);
   p.best_nout = take(B * 4);
-  p.list = take(2 * (size_t)B * 4);
-  p.count = take(16);
+  p.list = take((size_t)B * 4);
+  p.ctl = take(nt::CTL_WORDS * 4);
   p.out_tok = take((size_t)B * Tcap * 4);
   p.out_lp = take((size_t)B * Tcap * 4);
   p.out_len = take(B * 4);
@@ -365,18 +385,19 @@ struct nt_dec_state {
   nt_model* m;
   nt_search_cfg sc;
   int B, S, K, Tcap;
+  // host copy of the device control block, as of the last step the host has read
   int t = 0;
-  int n_live = 0;     // entries of the current live list
+  int n_live = 0;     // entries of the live list
   int n_alive = 0;    // sentences not finished
-  int list_cur = 0;   // which half of the list buffer is current
-  int anc_cur = 0;
   bool finished = false;
   WsPlan plan;
   char* ws;
-  int* h_count = nullptr;   // pinned 4-byte mailbox
+  int* h_ctl = nullptr;   // pinned mirror [CTL_MIRROR_SLOTS][CTL_WORDS], written by the step-end kernel
+  int* d_hctl = nullptr;  // its device-side address
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
-  int* list(int which) const { return at<int>(plan.list) + (size_t)which * B; }
-  int* anc(int which) const { return at<int>(plan.anc) + (size_t)which * B * K * Tcap; }
+  int* list() const { return at<int>(plan.list); }
+  int* ctl() const { return at<int>(plan.ctl); }
+  size_t anc_stride() const { return (size_t)B * K * Tcap; }
   nt::SearchState search() const {
     nt::SearchState s;
     s.B = B;
@@ -386,15 +407,15 @@ struct nt_dec_state {
     s.Tcap = Tcap;
     s.alpha = sc.len_penalty;
     s.early_stop = sc.early_stop;
-    s.sent_list = list(list_cur);
-    s.n_live = n_live;
+    s.sent_list = list();
+    s.ctl = ctl();
     s.score = at<float>(plan.score);
     s.cur_tok = at<int>(plan.cur_tok);
     s.tok_hist = at<int>(plan.tok_hist);
     s.par_hist = at<int>(plan.par_hist);
     s.lp_hist = at<float>(plan.lp_hist);
-    s.anc_cur = K > 1 ? anc(anc_cur) : nullptr;
-    s.anc_next = K > 1 ? anc(anc_cur ^ 1) : nullptr;
+    s.anc = K > 1 ? at<int>(plan.anc) : nullptr;
+    s.anc_stride = anc_stride();
     s.done = at<int>(plan.done);
     s.maxlen = at<int>(plan.maxlen);
     s.best_score = at<float>(plan.best_score);
@@ -520,27 +541,35 @@ nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
 }
 
 // ---- one decoder step ------------------------------------------------------------------
-nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, hipStream_t s) {
+// Enqueues every kernel of one step.  Grids are sized for the whole batch (Rp = B*K rows,
+// B sentences); each kernel reads the live counts and t from the device control block, so
+// the same sequence serves every step and can be captured once and replayed.  R and t
+// below are the host's copy of the block and only feed the work figures of the timing.
+nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, hipStream_t s) {
   const nt_model& m = *st->m;
   const WsPlan& p = st->plan;
   const int K = st->K, d = m.d, R = st->n_live * K, t = st->t;
-  const size_t Rp = (size_t)st->B * K;
+  const int Rp = st->B * K;
   const double eb = (double)m.eb;
   const float eps = m.cfg.ln_eps;
   auto at = [&](size_t o) { return st->ws + o; };
-  const int* list = st->list(st->list_cur);
+  int* list = st->list();
+  int* ctl = st->ctl();
 
   auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
     const double ob = e.mode == nt::EPI_TOPK ? 0.0 : e.out_f32 ? 4.0 : eb;
     const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
     const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
     const int tile = e.mode == nt::EPI_TOPK ? 2 : 0;   // the partial records assume 128-column tiles
-    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, R, N, Kd, e, s, role, tile); });
+    nt::GemmEpi ec = e;
+    ec.ctl = ctl;
+    ec.ctl_rows = K;
+    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, Rp, N, Kd, ec, s, role, tile); });
   };
 
   NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
-    return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, t, std::sqrt((float)d), m.dec[0].ln1,
-                            at(p.z), at(p.du), R, d, eps, s);
+    return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, ctl, std::sqrt((float)d), m.dec[0].ln1,
+                            at(p.z), at(p.du), Rp, d, eps, s);
   }));
 
   for (int j = 0; j < m.Ld; ++j) {
@@ -557,7 +586,6 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
     e.beam = K;
     e.kcache = kc;
     e.vcache = vc;
-    e.t = t;
     e.Tcap = st->Tcap;
     e.d = d;
     e.H = m.H;
@@ -570,14 +598,15 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
     sa.vcache = vc;
     sa.sent_list = list;
     sa.beam = K;
-    sa.anc = K > 1 ? st->anc(st->anc_cur) : nullptr;
+    sa.anc = K > 1 ? st->at<int>(p.anc) : nullptr;
+    sa.anc_stride = st->anc_stride();
     sa.out = at(p.datt);
-    sa.rows = R;
+    sa.rows = Rp;
     sa.H = m.H;
     sa.dh = m.dh;
-    sa.t = t;
     sa.Tcap = st->Tcap;
     sa.scale = 1.0f / std::sqrt((float)m.dh);
+    sa.ctl = ctl;
     NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * (2.0 + 2.0 * (t + 1)), 4.0 * R * (t + 1) * (double)d,
                  [&] { return nt::self_attn(m.dt, sa, s); }));
 
@@ -590,7 +619,7 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
     NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Wo, d, d, e));
 
     NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), R, d, eps, s); }));
+                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), Rp, d, eps, s, ctl, K); }));
 
     e = nt::GemmEpi{};
     e.mode = nt::EPI_STORE;
@@ -614,10 +643,11 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
     ma.lens = st->at<int>(p.len);
     ma.q_per_group = K;
     ma.self_queries = 0;
-    ma.n_groups = st->n_live;
+    ma.n_groups = st->B;
     ma.H = m.H;
     ma.dh = m.dh;
     ma.scale = 1.0f / std::sqrt((float)m.dh);
+    ma.ctl = ctl;
     NT_HIP(timed(NT_K_ATTN_CROSS, s, ((double)st->n_live * 2 * st->S * d + 2.0 * R * d) * eb,
                  4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s, 1); }));
 
@@ -630,7 +660,7 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
     NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Woc, d, d, e));
 
     NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), R, d, eps, s); }));
+                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), Rp, d, eps, s, ctl, K); }));
 
     e = nt::GemmEpi{};
     e.mode = nt::EPI_RELU;
@@ -649,75 +679,137 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
 
     const float* next_ln = j + 1 < m.Ld ? m.dec[j + 1].ln1 : m.dec_out_ln;
     NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                 [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), R, d, eps, s); }));
+                 [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), Rp, d, eps, s, ctl, K); }));
   }
 
   nt::SearchState ss = st->search();
   // Tied output projection.  Normally the projection's epilogue reduces each row to
-  // per-tile (max, sum exp, k2 best) partials and the logits never reach HBM; teacher
+  // per-tile (max, sum exp, best) partials and the logits never reach HBM; teacher
   // forcing and the logits copy-out use the plain path that writes fp32 logits.
   // (measured: the fused epilogue pays for itself for greedy's argmax; a top-8 per tile
   // row costs more than writing and re-reading the logits, so beam keeps the plain path)
-  const int k2 = K == 1 ? 1 : 2 * K;
   if (!d_logits && !d_forced && K == 1) {
     const int n_tiles = (m.V + 127) / 128;
     nt::GemmEpi e{};
     e.mode = nt::EPI_TOPK;
     e.part = st->at<float>(p.logits);
-    e.k2 = k2;
+    e.k2 = 1;
     e.n_tiles = n_tiles;
     NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
     const float* part = st->at<float>(p.logits);
-    const double pbytes = (double)R * n_tiles * nt::topk_record(k2) * 4;
+    const double pbytes = (double)R * n_tiles * nt::topk_record(1) * 4;
+    NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, s); }));
+  } else {
+    nt::GemmEpi e{};
+    e.mode = nt::EPI_STORE;
+    e.out = at(p.logits);
+    e.ldc = m.V;
+    e.out_f32 = 1;
+    NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+    if (d_logits) NT_HIP(nt::scatter_logits(st->at<float>(p.logits), list, ctl, K, Rp, m.V, d_logits, s));
     if (K == 1) {
-      NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, t, s); }));
+      NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V,
+                   [&] { return nt::greedy_step(st->at<float>(p.logits), d_forced, ss, s); }));
     } else {
-      NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] {
-        return nt::beam_merge(part, n_tiles, R, k2, st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), s);
+      NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V, [&] {
+        return nt::beam_select(st->at<float>(p.logits), ctl, K, Rp, m.V, 2 * K, st->at<float>(p.topv),
+                               st->at<int>(p.topi), st->at<float>(p.lse), s);
       }));
       NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
-        return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, t, s);
+        return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, s);
       }));
-      st->anc_cur ^= 1;
     }
-  } else {
-  nt::GemmEpi e{};
-  e.mode = nt::EPI_STORE;
-  e.out = at(p.logits);
-  e.ldc = m.V;
-  e.out_f32 = 1;
-  NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
-  if (d_logits) NT_HIP(nt::scatter_logits(st->at<float>(p.logits), list, K, R, m.V, d_logits, s));
-
-  if (K == 1) {
-    NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V,
-                 [&] { return nt::greedy_step(st->at<float>(p.logits), d_forced, ss, t, s); }));
-  } else {
-    NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V, [&] {
-      return nt::beam_select(st->at<float>(p.logits), R, m.V, 2 * K, st->at<float>(p.topv), st->at<int>(p.topi),
-                             st->at<float>(p.lse), s);
-    }));
-    NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
-      return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, t, s);
-    }));
-    st->anc_cur ^= 1;
   }
-  }
-  int* cnt = st->at<int>(p.count);
   NT_HIP(timed(NT_K_SEARCH, s, (double)st->n_live * 8, 0.0, [&] {
-    return nt::compact(list, st->n_live, st->at<int>(p.done), st->list(st->list_cur ^ 1), cnt, s);
+    return nt::step_end(list, st->at<int>(p.done), ctl, st->d_hctl, st->sc.prune, K, st->Tcap, s);
   }));
-  NT_HIP(hipMemcpyAsync(st->h_count, cnt, sizeof(int), hipMemcpyDeviceToHost, s));
-  NT_HIP(hipStreamSynchronize(s));
-  st->t = t + 1;
-  st->n_alive = *st->h_count;
-  if (st->sc.prune) {
-    st->list_cur ^= 1;
-    st->n_live = st->n_alive;
-  }
+  return NT_OK;
+}
+
+// Takes in the outcome of step `step` from its mirror slot (the step must have completed).
+nt_status absorb_step(nt_dec_state* st, int step) {
+  const volatile int* c = st->h_ctl + (step % nt::CTL_MIRROR_SLOTS) * nt::CTL_WORDS;
+  if (c[nt::CTL_T] != step + 1)
+    return fail(NT_E_STATE, "internal: step %d left t=%d in the control block", step, c[nt::CTL_T]);
+  st->t = c[nt::CTL_T];
+  st->n_live = c[nt::CTL_NLIVE];
+  st->n_alive = c[nt::CTL_NALIVE];
   if (st->n_alive == 0) st->finished = true;
-  if (!st->finished && st->t >= st->Tcap)
+  if (!st->finished && (st->t >= st->Tcap || st->n_live == 0))
     return fail(NT_E_STATE, "internal: %d sentences alive after %d steps", st->n_alive, st->t);
+  return NT_OK;
+}
+
+// One step issued directly and waited for.
+nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, hipStream_t s) {
+  const int step = st->t;
+  NT_TRY(enqueue_step(st, d_forced, d_logits, s));
+  NT_HIP(hipStreamSynchronize(s));
+  return absorb_step(st, step);
+}
+
+// Every remaining step of a batch from one captured step: the graph is replayed with up
+// to two steps in flight, the host reading step i's outcome from the mirror while step
+// i+1 runs (a step issued after the last one finished everything does nothing).  A step
+// sampled for timing is issued directly, with its kernel events, once nothing is in flight.
+struct GraphCtx {
+  hipStream_t cs = nullptr;     // capture stream (default priority, non-blocking)
+  hipEvent_t done[2] = {nullptr, nullptr};
+  ~GraphCtx() {
+    for (auto e : done)
+      if (e) (void)hipEventDestroy(e);
+    if (cs) (void)hipStreamDestroy(cs);
+  }
+  nt_status init() {
+    NT_HIP(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
+    for (auto& e : done) NT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming | hipEventReleaseToSystem));
+    return NT_OK;
+  }
+};
+
+nt_status decode_graph(nt_dec_state* st, GraphCtx& g, hipStream_t s) {
+  hipGraph_t graph = nullptr;
+  nt_status r;
+  {
+    ProfModeScope nop(PROF_NONE);
+    NT_HIP(hipStreamBeginCapture(g.cs, hipStreamCaptureModeThreadLocal));
+    r = enqueue_step(st, nullptr, nullptr, g.cs);
+    const hipError_t e = hipStreamEndCapture(g.cs, &graph);
+    if (r == NT_OK && e != hipSuccess) r = fail(NT_E_DEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
+  }
+  if (r != NT_OK) {
+    if (graph) (void)hipGraphDestroy(graph);
+    return r;
+  }
+  struct Exec {
+    hipGraphExec_t x = nullptr;
+    ~Exec() { if (x) (void)hipGraphExecDestroy(x); }
+  } exec;
+  const hipError_t ie = hipGraphInstantiate(&exec.x, graph, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph);
+  NT_HIP(ie);
+
+  int issued = st->t, read = st->t;
+  bool sampled = prof_step_sampled();
+  while (!st->finished) {
+    if (issued - read < 2 && (!sampled || issued == read)) {
+      if (sampled) {
+        ProfModeScope all(PROF_ALL);
+        NT_TRY(enqueue_step(st, nullptr, nullptr, s));
+      } else {
+        NT_HIP(hipGraphLaunch(exec.x, s));
+      }
+      NT_HIP(hipEventRecord(g.done[issued % 2], s));
+      ++issued;
+      sampled = prof_step_sampled();
+      continue;
+    }
+    NT_HIP(hipEventSynchronize(g.done[read % 2]));
+    NT_TRY(absorb_step(st, read));
+    ++read;
+  }
+  // a step still in flight found nothing live; let it finish before its graph goes
+  if (issued > read) NT_HIP(hipEventSynchronize(g.done[(issued - 1) % 2]));
   return NT_OK;
 }
 
@@ -760,12 +852,15 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
   st->ws = static_cast<char*>(d_ws);
   st->n_live = B;
   st->n_alive = B;
-  if (hipHostMalloc((void**)&st->h_count, sizeof(int), hipHostMallocDefault) != hipSuccess) {
+  if (hipHostMalloc((void**)&st->h_ctl, sizeof(int) * nt::CTL_MIRROR_SLOTS * nt::CTL_WORDS,
+                    hipHostMallocCoherent | hipHostMallocMapped) != hipSuccess ||
+      hipHostGetDevicePointer((void**)&st->d_hctl, st->h_ctl, 0) != hipSuccess) {
+    if (st->h_ctl) (void)hipHostFree(st->h_ctl);
     delete st;
-    return fail(NT_E_DEVICE, "hipHostMalloc failed");
+    return fail(NT_E_DEVICE, "pinned control-block mirror: hipHostMalloc / hipHostGetDevicePointer failed");
   }
   auto bail = [&](nt_status code) {
-    (void)hipHostFree(st->h_count);
+    (void)hipHostFree(st->h_ctl);
     delete st;
     return code;
   };
@@ -788,7 +883,7 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
       (r = chk(hipMemsetAsync(st->at<int>(plan.anc), 0, sizeof(int) * 2 * (size_t)B * st->K * Tcap, s), "clear anc")) != NT_OK)
     return r;
   if ((r = run_encoder(st, s)) != NT_OK) return bail(r);
-  if ((r = chk(nt::search_init(st->search(), st->list(0), m->cfg.bos_id, s), "search init")) != NT_OK) return r;
+  if ((r = chk(nt::search_init(st->search(), st->list(), st->ctl(), m->cfg.bos_id, s), "search init")) != NT_OK) return r;
   // the host copy of maxlen must not be freed before the copy has run
   if ((r = chk(hipStreamSynchronize(s), "sync")) != NT_OK) return r;
   *out = st;
@@ -813,7 +908,7 @@ nt_status read_impl(nt_dec_state* st, int32_t* h_tokens, int32_t* h_lens, float*
 
 void free_state(nt_dec_state* st) {
   if (!st) return;
-  if (st->h_count) (void)hipHostFree(st->h_count);
+  if (st->h_ctl) (void)hipHostFree(st->h_ctl);
   delete st;
 }
 
@@ -1126,6 +1221,9 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
   int* p_otok = reinterpret_cast<int*>(p_oscore + maxB);
   float* p_olp = reinterpret_cast<float*>(p_otok + maxBT);
 
+  GraphCtx graphs;
+  if (g_use_graphs) NT_TRY(graphs.init());
+
   std::vector<std::vector<int>> res_tok(n_sent);
   std::vector<std::vector<float>> res_lp(n_sent);
   std::vector<float> res_score(n_sent);
@@ -1148,7 +1246,10 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
     NT_TRY(encode_impl(m, reinterpret_cast<int*>(ws + plan.src), reinterpret_cast<int*>(ws + plan.len), p_len, B, S,
                        search, d_ws, ws_bytes, s, &st));
     nt_status r = NT_OK;
-    while (!st->finished && r == NT_OK) r = run_step(st, nullptr, nullptr, s);
+    if (g_use_graphs)
+      r = decode_graph(st, graphs, s);
+    else
+      while (!st->finished && r == NT_OK) r = run_step(st, nullptr, nullptr, s);
     if (r == NT_OK) r = read_impl(st, p_otok, p_olen, p_oscore, p_olp, s);
     const int Tcap = st->Tcap;
     free_state(st);
@@ -1207,6 +1308,13 @@ nt_status nt_prof_config(uint32_t class_mask, int32_t stride) {
   g_prof_mask = class_mask & ((1u << NT_K_COUNT) - 1);
   g_prof_stride = stride;
   for (auto& c : g_prof_seen) c = 0;
+  g_prof_steps = 0;
+  return NT_OK;
+}
+
+nt_status nt_set_graphs(int32_t enable) {
+  g_err.clear();
+  g_use_graphs = enable != 0;
   return NT_OK;
 }
 

@@ -127,8 +127,10 @@ __device__ void greedy_update(const SearchState& st, int b, int tok, float lp, i
 }
 
 __global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __restrict__ logits,
-                                                             const int* __restrict__ forced, SearchState st, int t) {
+                                                             const int* __restrict__ forced, SearchState st) {
   const int r = blockIdx.x;
+  if (r >= st.ctl[CTL_NLIVE]) return;           // block-uniform; beam 1: rows = live sentences
+  const int t = st.ctl[CTL_T];
   const int b = st.sent_list[r];
   const float* x = logits + (size_t)r * st.V;
   float lse, best;
@@ -143,10 +145,12 @@ __global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __rest
 // Greedy selection from the projection's per-tile partials [rows][n_tiles][4]
 // (max, sum exp, best value, best index): merged in tile order, then the update.
 __global__ __launch_bounds__(SEL_THREADS) void greedy_fused_kernel(const float* __restrict__ part, int n_tiles,
-                                                                   SearchState st, int t) {
+                                                                   SearchState st) {
   __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave], sb[SEL_THREADS / kWave];
   __shared__ int si[SEL_THREADS / kWave];
   const int r = blockIdx.x;
+  if (r >= st.ctl[CTL_NLIVE]) return;
+  const int t = st.ctl[CTL_T];
   const int b = st.sent_list[r];
   const float* rec = part + (size_t)r * n_tiles * 4;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -199,13 +203,15 @@ __device__ __forceinline__ void list_insert(float (&v)[K2], int (&ix)[K2], float
 }
 
 template <int K2>
-__global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* __restrict__ logits, int V, int k2,
+__global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* __restrict__ logits,
+                                                                  const int* __restrict__ ctl, int beam, int V, int k2,
                                                                   float* __restrict__ topv, int* __restrict__ topi,
                                                                   float* __restrict__ lse_out) {
   __shared__ float wv[SEL_THREADS / kWave][K2];
   __shared__ int wi[SEL_THREADS / kWave][K2];
   __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
   const int r = blockIdx.x;
+  if (r >= ctl[CTL_NLIVE] * beam) return;
   const float* x = logits + (size_t)r * V;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
 
@@ -296,13 +302,15 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
 // tile's k2 best (value desc, index asc) and its (max, sum exp).  Same merge as
 // beam_select_kernel, over tile lists instead of logits.
 template <int K2>
-__global__ __launch_bounds__(SEL_THREADS) void beam_merge_kernel(const float* __restrict__ part, int n_tiles, int k2,
+__global__ __launch_bounds__(SEL_THREADS) void beam_merge_kernel(const float* __restrict__ part, int n_tiles,
+                                                                 const int* __restrict__ ctl, int beam, int k2,
                                                                  float* __restrict__ topv, int* __restrict__ topi,
                                                                  float* __restrict__ lse_out) {
   __shared__ float wv[SEL_THREADS / kWave][K2];
   __shared__ int wi[SEL_THREADS / kWave][K2];
   __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
   const int r = blockIdx.x;
+  if (r >= ctl[CTL_NLIVE] * beam) return;
   const int rs = 2 + 2 * k2;
   const float* rec = part + (size_t)r * n_tiles * rs;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
@@ -369,13 +377,16 @@ constexpr int MAXC = 8;       // candidates per lane: K * 2K <= 512 = 64 * 8
 
 __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restrict__ topv,
                                                           const int* __restrict__ topi,
-                                                          const float* __restrict__ lse, SearchState st, int t) {
+                                                          const float* __restrict__ lse, SearchState st) {
   __shared__ float sel_c[4][32], sel_lp[4][32];
   __shared__ int sel_key[4][32];
   __shared__ int nk_par[4][16], nk_cnt[4];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int bl = blockIdx.x * 4 + wave;
-  if (bl >= st.n_live) return;                      // whole wave leaves; no block barrier below
+  if (bl >= st.ctl[CTL_NLIVE]) return;              // whole wave leaves; no block barrier below
+  const int t = st.ctl[CTL_T];
+  const int* anc_cur = st.anc + (size_t)st.ctl[CTL_ANC] * st.anc_stride;
+  int* anc_next = st.anc + (size_t)(st.ctl[CTL_ANC] ^ 1) * st.anc_stride;
   const int b = st.sent_list[bl];
   if (st.done[b]) return;
   const int K = st.beam, K2 = 2 * K, V = st.V, n = t + 1;
@@ -496,25 +507,28 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
   for (int k = 0; k < nk; ++k) {
     const int p = b * K + k, par = nk_par[wave][k];
     for (int s = lane; s <= t; s += kWave)
-      st.anc_next[(size_t)p * st.Tcap + s] = s < t ? st.anc_cur[(size_t)par * st.Tcap + s] : par;
+      anc_next[(size_t)p * st.Tcap + s] = s < t ? anc_cur[(size_t)par * st.Tcap + s] : par;
   }
 }
 
-// ---- compaction: order-preserving filter of the live list ---------------------------------
-__global__ __launch_bounds__(1024) void compact_kernel(const int* __restrict__ list, int n,
-                                                       const int* __restrict__ done, int* __restrict__ new_list,
-                                                       int* __restrict__ n_out) {
+// ---- end of step: order-preserving in-place filter of the live list ----------------------
+// Every entry of a 1024-chunk is read before the chunk's first barrier and written after
+// it, at a position no larger than its own, so the filter can run in place.
+__global__ __launch_bounds__(1024) void step_end_kernel(int* __restrict__ list, const int* __restrict__ done,
+                                                        int* __restrict__ ctl, int* __restrict__ host_ctl,
+                                                        int prune, int beam, int Tcap) {
   __shared__ int wsum[1024 / kWave];
   __shared__ int base;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int n = ctl[CTL_NLIVE], t = ctl[CTL_T];
+  if (n == 0) return;                                // nothing was live: the step did nothing
   if (tid == 0) base = 0;
   __syncthreads();
   for (int c0 = 0; c0 < n; c0 += 1024) {
     const int i = c0 + tid;
     const int b = i < n ? list[i] : 0;
     const int keep = (i < n && !done[b]) ? 1 : 0;
-    // inclusive wave scan
-    int x = keep;
+    int x = keep;                                    // inclusive wave scan
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
       const int y = __shfl_up(x, o, kWave);
@@ -524,7 +538,7 @@ __global__ __launch_bounds__(1024) void compact_kernel(const int* __restrict__ l
     __syncthreads();
     int off = base;
     for (int w = 0; w < wave; ++w) off += wsum[w];
-    if (keep) new_list[off + x - 1] = b;
+    if (prune && keep) list[off + x - 1] = b;
     __syncthreads();
     if (tid == 0) {
       int tot = 0;
@@ -533,7 +547,23 @@ __global__ __launch_bounds__(1024) void compact_kernel(const int* __restrict__ l
     }
     __syncthreads();
   }
-  if (tid == 0) *n_out = base;
+  if (tid == 0) {
+    const int alive = base;
+    int c[CTL_WORDS];
+    c[CTL_T] = t + 1;
+    // every sentence stops by its length limit (<= Tcap); the second test only guarantees
+    // that no step can ever write a cache slot >= Tcap
+    c[CTL_NLIVE] = (alive == 0 || t + 1 >= Tcap) ? 0 : (prune ? alive : n);
+    c[CTL_NALIVE] = alive;
+    c[CTL_ANC] = beam > 1 ? ctl[CTL_ANC] ^ 1 : 0;
+#pragma unroll
+    for (int j = 0; j < CTL_WORDS; ++j) ctl[j] = c[j];
+    if (host_ctl) {
+      // the mirror slot of step t, in pinned host memory, for the host to read once the step is done
+#pragma unroll
+      for (int j = 0; j < CTL_WORDS; ++j) host_ctl[(t % CTL_MIRROR_SLOTS) * CTL_WORDS + j] = c[j];
+    }
+  }
 }
 
 __global__ void finalize_kernel(SearchState st, int* __restrict__ out_tok, float* __restrict__ out_lp,
@@ -552,9 +582,15 @@ __global__ void finalize_kernel(SearchState st, int* __restrict__ out_tok, float
   out_score[b] = st.best_score[b];
 }
 
-__global__ void init_kernel(SearchState st, int* __restrict__ list, int bos) {
+__global__ void init_kernel(SearchState st, int* __restrict__ list, int* __restrict__ ctl, int bos) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   const int R = st.B * st.beam;
+  if (i == 0) {
+    ctl[CTL_T] = 0;
+    ctl[CTL_NLIVE] = st.B;
+    ctl[CTL_NALIVE] = st.B;
+    ctl[CTL_ANC] = 0;
+  }
   if (i < R) {
     st.score[i] = (i % st.beam == 0) ? 0.f : -INFINITY;
     st.cur_tok[i] = bos;
@@ -570,9 +606,10 @@ __global__ void init_kernel(SearchState st, int* __restrict__ list, int bos) {
   }
 }
 
-__global__ void scatter_logits_kernel(const float* __restrict__ src, const int* __restrict__ sent_list, int beam,
-                                      int rows, int V, float* __restrict__ dst) {
+__global__ void scatter_logits_kernel(const float* __restrict__ src, const int* __restrict__ sent_list,
+                                      const int* __restrict__ ctl, int beam, int V, float* __restrict__ dst) {
   const int r = blockIdx.y;
+  if (r >= ctl[CTL_NLIVE] * beam) return;
   const int p = sent_list[r / beam] * beam + r % beam;
   for (int v = blockIdx.x * blockDim.x + threadIdx.x; v < V; v += gridDim.x * blockDim.x)
     dst[(size_t)p * V + v] = src[(size_t)r * V + v];
@@ -580,31 +617,35 @@ __global__ void scatter_logits_kernel(const float* __restrict__ src, const int* 
 
 }  // namespace
 
-hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, int t, hipStream_t s) {
-  if (st.n_live <= 0) return hipSuccess;
-  hipLaunchKernelGGL(greedy_kernel, dim3(st.n_live), dim3(SEL_THREADS), 0, s, logits, forced, st, t);
+hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, hipStream_t s) {
+  const int rows = st.B * st.beam;
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(greedy_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, logits, forced, st);
   return hipGetLastError();
 }
 
-hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, int t, hipStream_t s) {
-  if (st.n_live <= 0) return hipSuccess;
-  hipLaunchKernelGGL(greedy_fused_kernel, dim3(st.n_live), dim3(SEL_THREADS), 0, s, part, n_tiles, st, t);
+hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, hipStream_t s) {
+  const int rows = st.B * st.beam;
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(greedy_fused_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, st);
   return hipGetLastError();
 }
 
-hipError_t beam_merge(const float* part, int n_tiles, int rows, int k2, float* topv, int* topi, float* lse,
-                      hipStream_t s) {
+hipError_t beam_merge(const float* part, int n_tiles, const int* ctl, int beam, int rows, int k2, float* topv,
+                      int* topi, float* lse, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (k2 > TOPK_MAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(beam_merge_kernel<TOPK_MAX>, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, k2, topv, topi,
-                     lse);
+  hipLaunchKernelGGL(beam_merge_kernel<TOPK_MAX>, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, ctl, beam, k2,
+                     topv, topi, lse);
   return hipGetLastError();
 }
 
-hipError_t beam_select(const float* logits, int rows, int V, int k2, float* topv, int* topi, float* lse,
-                       hipStream_t s) {
+hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, int V, int k2, float* topv, int* topi,
+                       float* lse, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-#define NT_SEL(K2) hipLaunchKernelGGL(beam_select_kernel<K2>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, V, k2, topv, topi, lse)
+#define NT_SEL(K2)                                                                                          \
+  hipLaunchKernelGGL(beam_select_kernel<K2>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, ctl, beam, V, k2, topv, \
+                     topi, lse)
   if (k2 <= 4) NT_SEL(4);
   else if (k2 <= 8) NT_SEL(8);
   else if (k2 <= 16) NT_SEL(16);
@@ -614,16 +655,16 @@ hipError_t beam_select(const float* logits, int rows, int V, int k2, float* topv
   return hipGetLastError();
 }
 
-hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, int t,
-                       hipStream_t s) {
-  if (st.n_live <= 0) return hipSuccess;
+hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, hipStream_t s) {
+  if (st.B <= 0) return hipSuccess;
   if (st.beam * 2 * st.beam > MAXC * kWave || st.beam > 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(beam_update_kernel, dim3((st.n_live + 3) / 4), dim3(256), 0, s, topv, topi, lse, st, t);
+  hipLaunchKernelGGL(beam_update_kernel, dim3((st.B + 3) / 4), dim3(256), 0, s, topv, topi, lse, st);
   return hipGetLastError();
 }
 
-hipError_t compact(const int* list, int n, const int* done, int* new_list, int* n_out, hipStream_t s) {
-  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, list, n, done, new_list, n_out);
+hipError_t step_end(int* list, const int* done, int* ctl, int* host_ctl, int prune, int beam, int Tcap,
+                    hipStream_t s) {
+  hipLaunchKernelGGL(step_end_kernel, dim3(1), dim3(1024), 0, s, list, done, ctl, host_ctl, prune, beam, Tcap);
   return hipGetLastError();
 }
 
@@ -634,17 +675,17 @@ hipError_t finalize(const SearchState& st, int* out_tok, float* out_lp, int* out
   return hipGetLastError();
 }
 
-hipError_t search_init(const SearchState& st, int* list, int bos, hipStream_t s) {
+hipError_t search_init(const SearchState& st, int* list, int* ctl, int bos, hipStream_t s) {
   const int n = st.B * st.beam;
-  hipLaunchKernelGGL(init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, st, list, bos);
+  hipLaunchKernelGGL(init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, st, list, ctl, bos);
   return hipGetLastError();
 }
 
-hipError_t scatter_logits(const float* logits, const int* sent_list, int beam, int rows, int V, float* dst,
-                          hipStream_t s) {
+hipError_t scatter_logits(const float* logits, const int* sent_list, const int* ctl, int beam, int rows, int V,
+                          float* dst, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(scatter_logits_kernel, dim3((V + 255) / 256 < 64 ? (V + 255) / 256 : 64, rows), dim3(256), 0,
-                     s, logits, sent_list, beam, rows, V, dst);
+                     s, logits, sent_list, ctl, beam, V, dst);
   return hipGetLastError();
 }
 

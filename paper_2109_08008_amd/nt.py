@@ -29,7 +29,7 @@ EXPORTS = [
     "nt_weights_size", "nt_load_weights", "nt_free_model", "nt_workspace_size", "nt_translate_workspace_size",
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
-    "nt_op_gemm", "nt_prof_config",
+    "nt_op_gemm", "nt_prof_config", "nt_set_graphs",
 ]
 
 
@@ -85,6 +85,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_last_error": (c_char_p, []),
         "nt_prof_enable": (c_int32, [c_uint32]),
         "nt_prof_config": (c_int32, [c_uint32, c_int32]),
+        "nt_set_graphs": (c_int32, [c_int32]),
         "nt_prof_reset": (c_int32, []),
         "nt_prof_get": (c_int32, [c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
         "nt_op_gemm": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, P, P, c_int32, c_int32, c_int32,
@@ -236,6 +237,10 @@ def nt_prof_enable(mask: int):
 
 def nt_prof_config(mask: int, stride: int):
     _check(load_library().nt_prof_config(mask, stride))
+
+
+def nt_set_graphs(enable: bool):
+    _check(load_library().nt_set_graphs(int(bool(enable))))
 
 
 def nt_prof_reset():

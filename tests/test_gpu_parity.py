@@ -133,6 +133,40 @@ def test_batching_and_pruning_do_not_change_results(dtype, beam):
             np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("beam,prune", [(1, 1), (1, 0), (4, 1), (4, 0)])
+def test_graph_replay_matches_direct_launches(beam, prune):
+    """Launched kernel by kernel (the default), replayed as one captured decoder step per
+    batch, or replayed with every third step issued directly for event timing: the
+    results are bitwise the same."""
+    from paper_2109_08008_amd import nt
+    shape = SHAPES["d128"]
+    blob = synth.make_weights(shape, seed=33, lively=True, eos_boost=4.0)
+    srcs, ids, offs = _sentences(40, 1, 30, shape.vocab, seed=17)
+    model = G.new_model(shape, blob, "f16")
+    search = synth.SearchSetup(beam=beam, len_penalty=0.6, max_len_a=1.5, max_len_b=5, token_budget=256, prune=prune)
+    ref_t, ref_s, ref_lp = model.translate(ids, offs, search)
+    assert any(len(t) < synth.max_target_len(search, len(s)) for t, s in zip(ref_t, srcs)), "nothing finished early"
+    runs = []
+    try:
+        nt.nt_set_graphs(True)
+        runs.append(model.translate(ids, offs, search))
+        nt.nt_prof_reset()
+        nt.nt_prof_config((1 << len(nt.KERNEL_CLASSES)) - 1, 3)
+        runs.append(model.translate(ids, offs, search))
+        timed = nt.nt_prof_get(nt.KERNEL_CLASSES.index("gemm_vocab"))
+    finally:
+        nt.nt_set_graphs(False)
+        nt.nt_prof_enable(0)
+        nt.nt_prof_reset()
+    assert timed["launches"] > 0
+    for t, s, lp in runs:
+        for a, b in zip(ref_t, t):
+            np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(ref_s, s)
+        for a, b in zip(ref_lp, lp):
+            np.testing.assert_array_equal(a, b)
+
+
 def test_fp16_translation_logprobs_within_tolerance():
     shape = SHAPES["d256"]
     blob = synth.make_weights(shape, seed=41, lively=True, eos_boost=4.0)
