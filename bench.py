@@ -7,8 +7,12 @@ memory), with inputs and weights generated beforehand.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload base-6-6]
 
-The line carries a roofline entry for the dominant kernel class, timed with HIP events
-on the launch stream inside the timed region, and the CPU oracle's throughput on a
+Batches are decoded three at a time on their own streams (the library default), each
+decoder step replayed from a captured HIP graph.  The line carries a roofline entry for
+the dominant kernel class, timed with HIP events on the launch stream inside the timed
+region: about 12 units (decoder steps or batch encodes) are sampled, and each sample
+runs alone on the GPU so that its kernel durations are the kernel's own, as a
+kernel-trace profiler reports them.  It also carries the CPU oracle's throughput on a
 bounded sample of the same workload (the oracle as written, one process per core).
 """
 from __future__ import annotations
@@ -33,6 +37,7 @@ PEAK = {  # MI355X published peaks (dense)
     "mfma_TFLOPs": {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3},
 }
 GEMM_CLASSES = (0, 1, 2)
+ENCODE_ONLY_CLASSES = (0, 3, 5)   # launched only by batch encodes (GEMM_ENC, DLCL, ATTN_ENC)
 
 
 def parse_args():
@@ -42,7 +47,9 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="base-6-6", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--graphs", action="store_true", help="replay each batch's decoder step as a HIP graph")
+    ap.add_argument("--no-graphs", action="store_true", help="launch decoder steps kernel by kernel")
+    ap.add_argument("--streams", type=int, default=0, help="batches decoded concurrently (0: library default)")
+    ap.add_argument("--samples", type=int, default=12, help="timing samples (isolated units) in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work for the oracle sample")
     ap.add_argument("--cpu-procs", type=int, default=0, help="oracle processes (0: min(16, cores))")
     return ap.parse_args()
@@ -130,7 +137,9 @@ def main():
     w = synth.WORKLOADS[args.workload]
     blob = synth.make_weights(w.model, seed=w.weights_seed)
     ids, offs = synth.make_sentences(w.data, w.model.vocab, seed=w.data_seed)
-    nt.nt_set_graphs(args.graphs)
+    nt.nt_set_graphs(not args.no_graphs)
+    if args.streams:
+        nt.nt_set_streams(args.streams)
     model = nt.Model(w.model, blob, w.dtype)
     sc = nt.search_cfg(w.search)
     ws_bytes = nt.nt_translate_workspace_size(model.handle, sc, offs)
@@ -141,7 +150,8 @@ def main():
     def step():
         return nt.nt_translate(model.handle, sc, ids, offs, cap, ws.data_ptr(), ws_bytes, stream)
 
-    # warmup; the last warmup step times every kernel class to find the dominant one
+    # warmup; the last warmup step times every unit (decoder step or batch encode), each
+    # run alone, to find the dominant kernel class and count the units of one step
     breakdown = {}
     for i in range(max(args.warmup, 1)):
         if i == max(args.warmup, 1) - 1:
@@ -149,14 +159,18 @@ def main():
             nt.nt_prof_enable((1 << len(nt.KERNEL_CLASSES)) - 1)
         step()
     torch.cuda.synchronize()
+    enc_units, step_units = nt.nt_prof_units()
     for c, name in enumerate(nt.KERNEL_CLASSES):
         breakdown[name] = nt.nt_prof_get(c)
     nt.nt_prof_enable(0)
     dominant = max(range(len(nt.KERNEL_CLASSES)), key=lambda c: breakdown[nt.KERNEL_CLASSES[c]]["ms"])
 
-    # timed region: events on every 8th launch of the dominant class only
+    # timed region: events on the dominant class in about `samples` units, each run alone
+    # (the other batches' streams drained first) so that they time the kernel by itself
+    units = enc_units if dominant in ENCODE_ONLY_CLASSES else step_units
+    stride = max(1, (units * args.steps) // max(args.samples, 1))
     nt.nt_prof_reset()
-    nt.nt_prof_config(1 << dominant, 8)
+    nt.nt_prof_config(1 << dominant, stride)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -187,10 +201,10 @@ def main():
             "source_tokens": int(offs[-1]), "target_tokens_per_step": n_tokens,
             "beam": w.search.beam, "token_budget": w.search.token_budget,
             "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
-            "decode_step_graphs": bool(args.graphs),
+            "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 3,
         },
-        "roofline": roofline_entry(dominant, prof, w.dtype),
-        "breakdown_ms_per_step": {k: round(v["ms"], 3) for k, v in breakdown.items()},
+        "roofline": dict(roofline_entry(dominant, prof, w.dtype), sampled_units_stride=stride),
+        "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, blob, ids, offs, args.cpu_seconds, args.cpu_procs)

@@ -123,8 +123,10 @@ void nt_free_model(nt_model* m);
 nt_status nt_workspace_size(const nt_model* m, const nt_search_cfg* search, int32_t max_sents,
                             int32_t max_src, size_t* bytes);
 
-/* Bytes of workspace nt_translate needs for this exact input: the maximum over the
- * batches that dynamic batching forms from it. */
+/* Bytes of workspace nt_translate needs for this exact input at the current stream
+ * setting (nt_set_streams): one slice per concurrently decoded batch, each the maximum
+ * over the batches that dynamic batching forms from it.  A smaller workspace (at least
+ * one slice) makes nt_translate decode fewer batches at once. */
 nt_status nt_translate_workspace_size(const nt_model* m, const nt_search_cfg* search,
                                       const int64_t* h_src_off, int32_t n_sent, size_t* bytes);
 
@@ -184,11 +186,14 @@ void nt_free_state(nt_dec_state* st);
  * h_out receives the concatenated output tokens (capacity out_cap; the sum of every
  * sentence's max target length always suffices), h_out_off [n_sent+1] the offsets,
  * h_score [n_sent] (or NULL) the scores, h_tok_logp [out_cap] (or NULL) each output
- * token's log-prob.  Returns when the outputs are in host memory.
+ * token's log-prob.  Returns when the outputs are in host memory.  Batches run on library
+ * streams that wait for the work already queued on `stream`, several at a time
+ * (nt_set_streams), each in its own workspace slice, so that the small kernels of one
+ * batch's decoder step overlap those of another; results do not depend on it.
  * Every per-step quantity lives in a device-side control block, so the decoder step is
- * one fixed kernel sequence: by default it is launched kernel by kernel; after
- * nt_set_graphs(1) each batch's step is captured once into a HIP graph and replayed.
- * Both ways run the same kernels and give bitwise identical results. */
+ * one fixed kernel sequence: each batch's step is captured once into a HIP graph and
+ * replayed (or, after nt_set_graphs(0), launched kernel by kernel).  Both ways run the
+ * same kernels and give bitwise identical results. */
 nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* h_src,
                        const int64_t* h_src_off, int32_t n_sent, int32_t* h_out, int64_t out_cap,
                        int64_t* h_out_off, float* h_score, float* h_tok_logp, void* d_ws,
@@ -206,10 +211,14 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
                      const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
                      int32_t relu, int32_t tile, void* stream);
 
-/* Process-wide switch for nt_translate's graph replay of the decoder step (default off:
- * on MI355X the replay measured about 1% slower than direct launches, whose host side
- * already runs ahead of the GPU). */
+/* Process-wide switch for nt_translate's graph replay of the decoder step (default on;
+ * with 0, every step is launched kernel by kernel). */
 nt_status nt_set_graphs(int32_t enable);
+
+/* Process-wide number of batches nt_translate decodes concurrently, 1..8 (default 3: with
+ * HIP's four hardware queues per process, a fourth batch stream shares a queue with the
+ * caller's and measured slower). */
+nt_status nt_set_streams(int32_t n);
 
 /* Thread-local message of the last failing call on this thread ("" if none). */
 const char* nt_last_error(void);
@@ -234,11 +243,16 @@ typedef enum {
 
 nt_status nt_prof_enable(uint32_t class_mask);   /* bit i enables class i; 0 disables */
 /* Like nt_prof_enable, but only every `stride`-th launch of an enabled class is timed
- * (stride >= 1), which keeps the host cost of event recording out of a timed run.  In
- * nt_translate's graph replay, every stride-th decoder step is issued kernel by kernel
- * with events on all launches of the enabled classes, and the other steps replay the
- * graph untimed. */
+ * (stride >= 1), which keeps the host cost of event recording out of a timed run.
+ * nt_translate instead samples whole units -- every stride-th decoder step or batch
+ * encode -- and runs each sample alone on the GPU (the other batches' streams drained
+ * first) with events on every launch of the enabled classes, so the times are those of
+ * the kernels by themselves, as a kernel-trace profiler reports them. */
 nt_status nt_prof_config(uint32_t class_mask, int32_t stride);
+/* Units nt_translate has counted since the last nt_prof_config, per kind: batch
+ * encodes and decoder steps (each counted while a class that kind launches is enabled;
+ * stride applies per kind).  Either pointer may be NULL. */
+nt_status nt_prof_units(int64_t* encodes, int64_t* steps);
 nt_status nt_prof_reset(void);
 /* Totals since the last reset for one class; synchronises on the recorded events. */
 nt_status nt_prof_get(int32_t kernel_class, int64_t* launches, double* total_ms, double* alg_bytes,

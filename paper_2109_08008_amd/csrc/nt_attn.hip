@@ -315,9 +315,9 @@ hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
   const long long tasks = (long long)a.n_groups * a.H * ((a.q_per_group + 15) / 16);
   const dim3 grid((unsigned)((tasks + 3) / 4));
   switch (a.dh) {
-    case 32: hipLaunchKernelGGL((attn_mfma_kernel<T, 32, ROLE>), grid, dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((attn_mfma_kernel<T, 64, ROLE>), grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((attn_mfma_kernel<T, 128, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 32: NT_LAUNCH((attn_mfma_kernel<T, 32, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 64: NT_LAUNCH((attn_mfma_kernel<T, 64, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 128: NT_LAUNCH((attn_mfma_kernel<T, 128, ROLE>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -327,7 +327,7 @@ template <typename T, int DH>
 void self_launch(const SelfAttnArgs& a, hipStream_t s) {
   constexpr int NWV = attn_waves<T, DH, 1>();
   const dim3 grid((a.rows * a.H + NWV - 1) / NWV);
-  hipLaunchKernelGGL((self_attn_kernel<T, DH>), grid, dim3(NWV * kWave), 0, s, a);
+  NT_LAUNCH((self_attn_kernel<T, DH>), grid, dim3(NWV * kWave), 0, s, a);
 }
 
 template <typename T>

@@ -6,6 +6,7 @@
 
 namespace nt {
 
+
 typedef _Float16 f16;
 typedef __bf16 bf16;
 

@@ -390,7 +390,7 @@ template <typename T, int BM_, int BN_, int STAGES, int ROLE>
 hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                        hipStream_t s) {
   const int tm = (M + BM_ - 1) / BM_, tn = (N + BN_ - 1) / BN_;
-  hipLaunchKernelGGL((gemm_kernel<T, BM_, BN_, STAGES, ROLE>), dim3(tm * tn), dim3(NTHR), 0, s,
+  NT_LAUNCH((gemm_kernel<T, BM_, BN_, STAGES, ROLE>), dim3(tm * tn), dim3(NTHR), 0, s,
                      static_cast<const T*>(A), lda, static_cast<const T*>(Bt), M, N, K, epi, tm, tn);
   return hipGetLastError();
 }

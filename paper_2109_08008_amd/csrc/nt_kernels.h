@@ -2,11 +2,32 @@
 // returns hipGetLastError() of the launch.  Shapes are validated by the runtime
 // (nt_runtime.cpp) before any launch; launchers assume them.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace nt {
+
+// Event pair into which the next kernel launch on this thread writes its own start and
+// stop times (set by the runtime's kernel timing, cleared by the launch that takes it).
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
+
+// Every kernel launch of the library: hipExtLaunchKernelGGL with the pending event pair
+// (the events then carry the dispatch's own timestamps), else hipLaunchKernelGGL.
+#define NT_LAUNCH(kernel, grid, block, shmem, stream, ...)                                        \
+  do {                                                                                            \
+    if (::nt::g_launch_events.start) {                                                            \
+      const ::nt::LaunchEvents ev_ = ::nt::g_launch_events;                                       \
+      ::nt::g_launch_events = ::nt::LaunchEvents{};                                               \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev_.start, ev_.stop, 0, __VA_ARGS__); \
+    } else {                                                                                      \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                        \
+    }                                                                                             \
+  } while (0)
 
 enum class DT : int { F32 = 0, F16 = 1, BF16 = 2 };
 

@@ -160,7 +160,7 @@ __global__ void convert_kernel(const float* __restrict__ src, T* __restrict__ ds
 template <typename T>
 hipError_t dlcl_t(const DlclArgs& a, hipStream_t s) {
   const dim3 grid((a.rows + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
-#define NT_CALL(E) hipLaunchKernelGGL((dlcl_kernel<T, E>), grid, dim3(256), 0, s, a)
+#define NT_CALL(E) NT_LAUNCH((dlcl_kernel<T, E>), grid, dim3(256), 0, s, a)
   NT_EPL_SWITCH(a.d, NT_CALL)
 #undef NT_CALL
   return hipGetLastError();
@@ -171,7 +171,7 @@ hipError_t ln_t(const void* x, const float* ln, void* y, int rows, int d, float 
                 int ctl_rows) {
   const dim3 grid((rows + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
 #define NT_CALL(E)                                                                                            \
-  hipLaunchKernelGGL((ln_kernel<T, E>), grid, dim3(256), 0, s, static_cast<const T*>(x), ln, static_cast<T*>(y), \
+  NT_LAUNCH((ln_kernel<T, E>), grid, dim3(256), 0, s, static_cast<const T*>(x), ln, static_cast<T*>(y), \
                      rows, d, eps, ctl, ctl_rows)
   NT_EPL_SWITCH(d, NT_CALL)
 #undef NT_CALL
@@ -183,7 +183,7 @@ hipError_t emb_t(const int* cur_tok, const int* sent_list, int beam, const void*
                  float scale, const float* ln, void* z, void* u, int rows, int d, float eps, hipStream_t s) {
   const dim3 grid((rows + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
 #define NT_CALL(EP)                                                                                            \
-  hipLaunchKernelGGL((dec_embed_kernel<T, EP>), grid, dim3(256), 0, s, cur_tok, sent_list, beam,               \
+  NT_LAUNCH((dec_embed_kernel<T, EP>), grid, dim3(256), 0, s, cur_tok, sent_list, beam,               \
                      static_cast<const T*>(E), pe, ctl, scale, ln, static_cast<T*>(z), static_cast<T*>(u), rows, \
                      d, eps)
   NT_EPL_SWITCH(d, NT_CALL)
@@ -222,14 +222,14 @@ hipError_t dec_embed_ln(DT dt, const int* cur_tok, const int* sent_list, int bea
 namespace {
 template <typename T>
 hipError_t transpose_t(const float* src, void* dst, int K, int N, hipStream_t s) {
-  hipLaunchKernelGGL(transpose_kernel<T>, dim3((N + 31) / 32, (K + 31) / 32), dim3(256), 0, s, src,
+  NT_LAUNCH(transpose_kernel<T>, dim3((N + 31) / 32, (K + 31) / 32), dim3(256), 0, s, src,
                      static_cast<T*>(dst), K, N);
   return hipGetLastError();
 }
 template <typename T>
 hipError_t convert_t(const float* src, void* dst, size_t n, hipStream_t s) {
   const size_t blocks = std::min<size_t>((n + 255) / 256, 65536);
-  hipLaunchKernelGGL(convert_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, src, static_cast<T*>(dst), n);
+  NT_LAUNCH(convert_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, src, static_cast<T*>(dst), n);
   return hipGetLastError();
 }
 }  // namespace

@@ -28,6 +28,10 @@
 
 using nt::DT;
 
+namespace nt {
+thread_local LaunchEvents g_launch_events;
+}
+
 // --------------------------------------------------------------------------------------
 // errors
 namespace {
@@ -59,7 +63,7 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // --------------------------------------------------------------------------------------
-// kernel timing
+// kernel timing: each timed launch records its dispatch's start / stop into an event pair
 struct ProfRec {
   int cls;
   hipEvent_t a, b;
@@ -84,12 +88,13 @@ hipEvent_t prof_event() {
 }
 
 // How launches of enabled classes are timed on this thread: every stride-th launch of a
-// class (direct launches), never (while a step is being captured into a graph), or every
-// launch (a sampled step of a graph-replayed decode, issued directly).
+// class (the step-level entry points), never (nt_translate outside its samples, and
+// graph capture), or every launch (a sampled unit of nt_translate).
 enum ProfMode { PROF_STRIDE = 0, PROF_NONE = 1, PROF_ALL = 2 };
 thread_local int g_prof_mode = PROF_STRIDE;
-int64_t g_prof_steps = 0;   // decode steps seen while profiling (graph mode samples every stride-th)
-std::atomic<bool> g_use_graphs{false};  // nt_translate replays a captured decode step
+int64_t g_prof_enc_units = 0, g_prof_step_units = 0;   // nt_translate units seen while profiling
+std::atomic<bool> g_use_graphs{true};   // nt_translate replays a captured decode step
+std::atomic<int> g_streams{3};          // batches nt_translate decodes concurrently
 
 struct ProfModeScope {
   int saved;
@@ -97,9 +102,19 @@ struct ProfModeScope {
   ~ProfModeScope() { g_prof_mode = saved; }
 };
 
-bool prof_step_sampled() {
+// Whether the next nt_translate unit (a batch encode, or a decoder step) is a timing
+// sample: every stride-th unit of its kind while a class that kind launches is enabled.
+// A sample runs alone on the GPU (the other batches' streams are drained first), so its
+// kernel times are those of the kernels by themselves.
+constexpr uint32_t kEncClasses = (1u << NT_K_GEMM_ENC) | (1u << NT_K_DLCL) | (1u << NT_K_LN) | (1u << NT_K_ATTN_ENC);
+constexpr uint32_t kStepClasses = (1u << NT_K_GEMM_DEC) | (1u << NT_K_GEMM_VOCAB) | (1u << NT_K_LN) |
+                                  (1u << NT_K_ATTN_SELF) | (1u << NT_K_ATTN_CROSS) | (1u << NT_K_SELECT) |
+                                  (1u << NT_K_SEARCH);
+bool prof_unit_sampled(bool encode) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  return g_prof_mask != 0 && g_prof_steps++ % g_prof_stride == 0;
+  if (!(g_prof_mask & (encode ? kEncClasses : kStepClasses))) return false;
+  int64_t& n = encode ? g_prof_enc_units : g_prof_step_units;
+  return n++ % g_prof_stride == 0;
 }
 
 template <typename F>
@@ -109,11 +124,17 @@ hipError_t timed(int cls, hipStream_t s, double bytes, double flops, F&& launch)
   if (g_prof_mode == PROF_STRIDE && g_prof_seen[cls]++ % g_prof_stride != 0) return launch();
   hipEvent_t a = prof_event(), b = prof_event();
   if (!a || !b) return hipErrorOutOfMemory;
-  hipError_t e = hipEventRecord(a, s);
-  if (e != hipSuccess) return e;
-  e = launch();
-  if (e != hipSuccess) return e;
-  e = hipEventRecord(b, s);
+  // the launch writes its dispatch's own start / stop times into a and b
+  nt::g_launch_events = nt::LaunchEvents{a, b};
+  const hipError_t e = launch();
+  const bool launched = nt::g_launch_events.start == nullptr;
+  nt::g_launch_events = nt::LaunchEvents{};
+  if (e != hipSuccess || !launched) {   // nothing was launched (or it failed): no record
+    g_prof_pool.push_back(a);
+    g_prof_pool.push_back(b);
+    return e;
+  }
+  (void)s;
   g_prof.push_back({cls, a, b, bytes, flops});
   return e;
 }
@@ -394,6 +415,7 @@ struct nt_dec_state {
   char* ws;
   int* h_ctl = nullptr;   // pinned mirror [CTL_MIRROR_SLOTS][CTL_WORDS], written by the step-end kernel
   int* d_hctl = nullptr;  // its device-side address
+  bool own_ctl = true;    // the mirror was allocated for this state (else borrowed)
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
   int* list() const { return at<int>(plan.list); }
   int* ctl() const { return at<int>(plan.ctl); }
@@ -748,73 +770,38 @@ nt_status run_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, h
   return absorb_step(st, step);
 }
 
-// Every remaining step of a batch from one captured step: the graph is replayed with up
-// to two steps in flight, the host reading step i's outcome from the mirror while step
-// i+1 runs (a step issued after the last one finished everything does nothing).  A step
-// sampled for timing is issued directly, with its kernel events, once nothing is in flight.
-struct GraphCtx {
-  hipStream_t cs = nullptr;     // capture stream (default priority, non-blocking)
-  hipEvent_t done[2] = {nullptr, nullptr};
-  ~GraphCtx() {
-    for (auto e : done)
-      if (e) (void)hipEventDestroy(e);
-    if (cs) (void)hipStreamDestroy(cs);
-  }
-  nt_status init() {
-    NT_HIP(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
-    for (auto& e : done) NT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming | hipEventReleaseToSystem));
-    return NT_OK;
-  }
-};
-
-nt_status decode_graph(nt_dec_state* st, GraphCtx& g, hipStream_t s) {
+// One step captured into an executable graph (on a private capture stream; nothing runs).
+nt_status capture_step(nt_dec_state* st, hipStream_t cs, hipGraphExec_t* exec) {
   hipGraph_t graph = nullptr;
   nt_status r;
   {
     ProfModeScope nop(PROF_NONE);
-    NT_HIP(hipStreamBeginCapture(g.cs, hipStreamCaptureModeThreadLocal));
-    r = enqueue_step(st, nullptr, nullptr, g.cs);
-    const hipError_t e = hipStreamEndCapture(g.cs, &graph);
+    NT_HIP(hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal));
+    r = enqueue_step(st, nullptr, nullptr, cs);
+    const hipError_t e = hipStreamEndCapture(cs, &graph);
     if (r == NT_OK && e != hipSuccess) r = fail(NT_E_DEVICE, "hipStreamEndCapture: %s", hipGetErrorString(e));
   }
   if (r != NT_OK) {
     if (graph) (void)hipGraphDestroy(graph);
     return r;
   }
-  struct Exec {
-    hipGraphExec_t x = nullptr;
-    ~Exec() { if (x) (void)hipGraphExecDestroy(x); }
-  } exec;
-  const hipError_t ie = hipGraphInstantiate(&exec.x, graph, nullptr, nullptr, 0);
+  const hipError_t ie = hipGraphInstantiate(exec, graph, nullptr, nullptr, 0);
   (void)hipGraphDestroy(graph);
   NT_HIP(ie);
-
-  int issued = st->t, read = st->t;
-  bool sampled = prof_step_sampled();
-  while (!st->finished) {
-    if (issued - read < 2 && (!sampled || issued == read)) {
-      if (sampled) {
-        ProfModeScope all(PROF_ALL);
-        NT_TRY(enqueue_step(st, nullptr, nullptr, s));
-      } else {
-        NT_HIP(hipGraphLaunch(exec.x, s));
-      }
-      NT_HIP(hipEventRecord(g.done[issued % 2], s));
-      ++issued;
-      sampled = prof_step_sampled();
-      continue;
-    }
-    NT_HIP(hipEventSynchronize(g.done[read % 2]));
-    NT_TRY(absorb_step(st, read));
-    ++read;
-  }
-  // a step still in flight found nothing live; let it finish before its graph goes
-  if (issued > read) NT_HIP(hipEventSynchronize(g.done[(issued - 1) % 2]));
   return NT_OK;
 }
 
+// Pinned host memory an encode may borrow instead of allocating: with it, nt_encode's work
+// is fully asynchronous on the stream (no allocation, no synchronisation).
+struct EncodeHost {
+  int* maxlen;   // >= B ints; read by a copy on the stream, so left untouched until it ran
+  int* h_ctl;    // control-block mirror and its device-side address
+  int* d_hctl;
+};
+
 nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, const int32_t* h_len, int B, int S,
-                      const nt_search_cfg* sc, void* d_ws, size_t ws_bytes, hipStream_t s, nt_dec_state** out) {
+                      const nt_search_cfg* sc, void* d_ws, size_t ws_bytes, hipStream_t s, nt_dec_state** out,
+                      const EncodeHost* hx = nullptr) {
   if (!m || !d_src || !d_len || !out || !d_ws) return fail(NT_E_INVALID, "null argument to nt_encode");
   NT_TRY(validate_search(*m, sc));
   if (B <= 0 || S <= 0) return fail(NT_E_INVALID, "empty batch (B=%d, S=%d)", B, S);
@@ -827,7 +814,8 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
     NT_HIP(hipStreamSynchronize(s));
   }
   int Tcap = 0;
-  std::vector<int> maxlen(B);
+  std::vector<int> maxlen_own(hx ? 0 : B);
+  int* maxlen = hx ? hx->maxlen : maxlen_own.data();
   for (int b = 0; b < B; ++b) {
     if (lens[b] < 1 || lens[b] > S) return fail(NT_E_INVALID, "sentence %d has length %d outside [1, %d]", b, lens[b], S);
     maxlen[b] = max_tgt_of(*sc, lens[b]);
@@ -852,15 +840,19 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
   st->ws = static_cast<char*>(d_ws);
   st->n_live = B;
   st->n_alive = B;
-  if (hipHostMalloc((void**)&st->h_ctl, sizeof(int) * nt::CTL_MIRROR_SLOTS * nt::CTL_WORDS,
-                    hipHostMallocCoherent | hipHostMallocMapped) != hipSuccess ||
-      hipHostGetDevicePointer((void**)&st->d_hctl, st->h_ctl, 0) != hipSuccess) {
+  if (hx) {
+    st->h_ctl = hx->h_ctl;
+    st->d_hctl = hx->d_hctl;
+    st->own_ctl = false;
+  } else if (hipHostMalloc((void**)&st->h_ctl, sizeof(int) * nt::CTL_MIRROR_SLOTS * nt::CTL_WORDS,
+                           hipHostMallocCoherent | hipHostMallocMapped) != hipSuccess ||
+             hipHostGetDevicePointer((void**)&st->d_hctl, st->h_ctl, 0) != hipSuccess) {
     if (st->h_ctl) (void)hipHostFree(st->h_ctl);
     delete st;
     return fail(NT_E_DEVICE, "pinned control-block mirror: hipHostMalloc / hipHostGetDevicePointer failed");
   }
   auto bail = [&](nt_status code) {
-    (void)hipHostFree(st->h_ctl);
+    if (st->own_ctl) (void)hipHostFree(st->h_ctl);
     delete st;
     return code;
   };
@@ -876,7 +868,7 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
   if (d_len != st->at<int>(plan.len) &&
       (r = chk(hipMemcpyAsync(st->at<int>(plan.len), d_len, sizeof(int) * B, hipMemcpyDeviceToDevice, s), "copy len")) != NT_OK)
     return r;
-  if ((r = chk(hipMemcpyAsync(st->at<int>(plan.maxlen), maxlen.data(), sizeof(int) * B, hipMemcpyHostToDevice, s),
+  if ((r = chk(hipMemcpyAsync(st->at<int>(plan.maxlen), maxlen, sizeof(int) * B, hipMemcpyHostToDevice, s),
                "copy maxlen")) != NT_OK)
     return r;
   if (st->K > 1 &&
@@ -884,8 +876,8 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
     return r;
   if ((r = run_encoder(st, s)) != NT_OK) return bail(r);
   if ((r = chk(nt::search_init(st->search(), st->list(), st->ctl(), m->cfg.bos_id, s), "search init")) != NT_OK) return r;
-  // the host copy of maxlen must not be freed before the copy has run
-  if ((r = chk(hipStreamSynchronize(s), "sync")) != NT_OK) return r;
+  // an owned host copy of maxlen must not be freed before the copy has run
+  if (!hx && (r = chk(hipStreamSynchronize(s), "sync")) != NT_OK) return r;
   *out = st;
   return NT_OK;
 }
@@ -908,7 +900,7 @@ nt_status read_impl(nt_dec_state* st, int32_t* h_tokens, int32_t* h_lens, float*
 
 void free_state(nt_dec_state* st) {
   if (!st) return;
-  if (st->h_ctl) (void)hipHostFree(st->h_ctl);
+  if (st->own_ctl && st->h_ctl) (void)hipHostFree(st->h_ctl);
   delete st;
 }
 
@@ -1120,10 +1112,10 @@ nt_status nt_translate_workspace_size(const nt_model* m, const nt_search_cfg* se
   std::vector<int> lens;
   NT_TRY(validate_sources(*m, *search, nullptr, h_src_off, n_sent, lens, false));
   const auto order = length_order(lens);
-  size_t need = 0;
-  for (const Batch& b : plan_batches(order, lens, *search))
-    need = std::max(need, ws_plan(*m, b.count, b.S, search->beam, b.Tcap).total);
-  *bytes = need;
+  const auto batches = plan_batches(order, lens, *search);
+  size_t slot = 0;
+  for (const Batch& b : batches) slot = std::max(slot, align_up(ws_plan(*m, b.count, b.S, search->beam, b.Tcap).total));
+  *bytes = slot * (size_t)std::min<int>(g_streams.load(), (int)batches.size());
   return NT_OK;
 }
 
@@ -1194,72 +1186,212 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
   NT_TRY(validate_search(*m, search));
   std::vector<int> lens;
   NT_TRY(validate_sources(*m, *search, h_src, h_src_off, n_sent, lens, true));
+  if ((reinterpret_cast<uintptr_t>(d_ws) & (kAlign - 1)) != 0) return fail(NT_E_INVALID, "workspace must be 256-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const auto order = length_order(lens);
   const auto batches = plan_batches(order, lens, *search);
-  size_t need = 0;
+  const int nb = (int)batches.size();
+  size_t slot_bytes = 0;
   int maxB = 0, maxBS = 0, maxBT = 0;
   for (const Batch& b : batches) {
-    need = std::max(need, ws_plan(*m, b.count, b.S, search->beam, b.Tcap).total);
+    slot_bytes = std::max(slot_bytes, align_up(ws_plan(*m, b.count, b.S, search->beam, b.Tcap).total));
     maxB = std::max(maxB, b.count);
     maxBS = std::max(maxBS, b.count * b.S);
     maxBT = std::max(maxBT, b.count * b.Tcap);
   }
-  if (ws_bytes < need) return fail(NT_E_WORKSPACE, "workspace too small: %zu bytes given, %zu required", ws_bytes, need);
+  if (ws_bytes < slot_bytes)
+    return fail(NT_E_WORKSPACE, "workspace too small: %zu bytes given, %zu required", ws_bytes, slot_bytes);
+  // batches decoded at once: as many as the setting asks and the workspace holds
+  const int NS = (int)std::min<size_t>({(size_t)g_streams.load(), ws_bytes / slot_bytes, (size_t)nb});
+  const bool graphs = g_use_graphs;
 
-  // pinned staging for one batch's inputs and outputs
-  struct Pinned {
-    void* p = nullptr;
-    ~Pinned() { if (p) (void)hipHostFree(p); }
-  } pin;
-  const size_t pin_bytes = (size_t)maxBS * 4 + (size_t)maxB * 4 * 3 + (size_t)maxBT * 8;
-  NT_HIP(hipHostMalloc(&pin.p, pin_bytes, hipHostMallocDefault));
-  int* p_src = static_cast<int*>(pin.p);
-  int* p_len = p_src + maxBS;
-  int* p_olen = p_len + maxB;
-  float* p_oscore = reinterpret_cast<float*>(p_olen + maxB);
-  int* p_otok = reinterpret_cast<int*>(p_oscore + maxB);
-  float* p_olp = reinterpret_cast<float*>(p_otok + maxBT);
-
-  GraphCtx graphs;
-  if (g_use_graphs) NT_TRY(graphs.init());
+  // per-slot resources: stream, step events, workspace slice, pinned staging and mirror
+  struct Slot {
+    hipStream_t s = nullptr;
+    hipStream_t cs = nullptr;           // graph capture stream
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    hipGraphExec_t exec = nullptr;
+    char* ws = nullptr;
+    int *p_src, *p_len, *p_maxlen, *p_olen, *p_otok, *h_ctl, *d_hctl;
+    float *p_oscore, *p_olp;
+    nt_dec_state* st = nullptr;
+    int batch = -1, issued = 0, read = 0;
+    bool sampled = false;               // the next step is a timing sample
+  };
+  struct Res {
+    std::vector<Slot> slots;
+    void* pin = nullptr;
+    int* mirror = nullptr;
+    hipEvent_t start = nullptr;
+    ~Res() {
+      for (Slot& sl : slots) {
+        if (sl.st) free_state(sl.st);
+        if (sl.exec) (void)hipGraphExecDestroy(sl.exec);
+        for (auto e : sl.ev)
+          if (e) (void)hipEventDestroy(e);
+        if (sl.cs) (void)hipStreamDestroy(sl.cs);
+        if (sl.s) {
+          (void)hipStreamSynchronize(sl.s);
+          (void)hipStreamDestroy(sl.s);
+        }
+      }
+      if (start) (void)hipEventDestroy(start);
+      if (pin) (void)hipHostFree(pin);
+      if (mirror) (void)hipHostFree(mirror);
+    }
+  } res;
+  const size_t stage_ints = (size_t)maxBS + 4 * (size_t)maxB + 2 * (size_t)maxBT;
+  NT_HIP(hipHostMalloc(&res.pin, stage_ints * 4 * NS, hipHostMallocDefault));
+  const size_t mir_ints = (size_t)nt::CTL_MIRROR_SLOTS * nt::CTL_WORDS;
+  NT_HIP(hipHostMalloc((void**)&res.mirror, mir_ints * 4 * NS, hipHostMallocCoherent | hipHostMallocMapped));
+  int* d_mirror = nullptr;
+  NT_HIP(hipHostGetDevicePointer((void**)&d_mirror, res.mirror, 0));
+  NT_HIP(hipEventCreateWithFlags(&res.start, hipEventDisableTiming));
+  NT_HIP(hipEventRecord(res.start, s));   // work already on the caller's stream comes first
+  res.slots.resize(NS);
+  for (int i = 0; i < NS; ++i) {
+    Slot& sl = res.slots[i];
+    NT_HIP(hipStreamCreateWithFlags(&sl.s, hipStreamNonBlocking));
+    if (graphs) NT_HIP(hipStreamCreateWithFlags(&sl.cs, hipStreamNonBlocking));
+    for (auto& e : sl.ev) NT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming | hipEventReleaseToSystem));
+    NT_HIP(hipStreamWaitEvent(sl.s, res.start, 0));
+    sl.ws = static_cast<char*>(d_ws) + (size_t)i * slot_bytes;
+    int* q = static_cast<int*>(res.pin) + (size_t)i * stage_ints;
+    sl.p_src = q;
+    sl.p_len = sl.p_src + maxBS;
+    sl.p_maxlen = sl.p_len + maxB;
+    sl.p_olen = sl.p_maxlen + maxB;
+    sl.p_oscore = reinterpret_cast<float*>(sl.p_olen + maxB);
+    sl.p_otok = reinterpret_cast<int*>(sl.p_oscore + maxB);
+    sl.p_olp = reinterpret_cast<float*>(sl.p_otok + maxBT);
+    sl.h_ctl = res.mirror + (size_t)i * mir_ints;
+    sl.d_hctl = d_mirror + (size_t)i * mir_ints;
+  }
 
   std::vector<std::vector<int>> res_tok(n_sent);
   std::vector<std::vector<float>> res_lp(n_sent);
   std::vector<float> res_score(n_sent);
-  char* ws = static_cast<char*>(d_ws);
 
-  for (const Batch& bt : batches) {
+  // inputs of a batch into its slot's staging and workspace, then the (asynchronous) encode
+  auto start_batch = [&](Slot& sl, int bi) -> nt_status {
+    const Batch& bt = batches[bi];
     const int B = bt.count, S = bt.S;
     for (int i = 0; i < B; ++i) {
       const int sid = order[bt.first + i];
       const int L = lens[sid];
-      p_len[i] = L;
-      std::memcpy(p_src + (size_t)i * S, h_src + h_src_off[sid], sizeof(int) * L);
-      std::fill(p_src + (size_t)i * S + L, p_src + (size_t)(i + 1) * S, m->cfg.pad_id);
+      sl.p_len[i] = L;
+      std::memcpy(sl.p_src + (size_t)i * S, h_src + h_src_off[sid], sizeof(int) * L);
+      std::fill(sl.p_src + (size_t)i * S + L, sl.p_src + (size_t)(i + 1) * S, m->cfg.pad_id);
     }
-    // inputs go straight into the workspace slots nt_encode copies them to
     const WsPlan plan = ws_plan(*m, B, S, search->beam, bt.Tcap);
-    NT_HIP(hipMemcpyAsync(ws + plan.src, p_src, sizeof(int) * (size_t)B * S, hipMemcpyHostToDevice, s));
-    NT_HIP(hipMemcpyAsync(ws + plan.len, p_len, sizeof(int) * B, hipMemcpyHostToDevice, s));
-    nt_dec_state* st = nullptr;
-    NT_TRY(encode_impl(m, reinterpret_cast<int*>(ws + plan.src), reinterpret_cast<int*>(ws + plan.len), p_len, B, S,
-                       search, d_ws, ws_bytes, s, &st));
-    nt_status r = NT_OK;
-    if (g_use_graphs)
-      r = decode_graph(st, graphs, s);
-    else
-      while (!st->finished && r == NT_OK) r = run_step(st, nullptr, nullptr, s);
-    if (r == NT_OK) r = read_impl(st, p_otok, p_olen, p_oscore, p_olp, s);
-    const int Tcap = st->Tcap;
-    free_state(st);
-    if (r != NT_OK) return r;
-    for (int i = 0; i < B; ++i) {
+    NT_HIP(hipMemcpyAsync(sl.ws + plan.src, sl.p_src, sizeof(int) * (size_t)B * S, hipMemcpyHostToDevice, sl.s));
+    NT_HIP(hipMemcpyAsync(sl.ws + plan.len, sl.p_len, sizeof(int) * B, hipMemcpyHostToDevice, sl.s));
+    const EncodeHost hx{sl.p_maxlen, sl.h_ctl, sl.d_hctl};
+    NT_TRY(encode_impl(m, reinterpret_cast<int*>(sl.ws + plan.src), reinterpret_cast<int*>(sl.ws + plan.len), sl.p_len,
+                       B, S, search, sl.ws, slot_bytes, sl.s, &sl.st, &hx));
+    if (graphs) NT_TRY(capture_step(sl.st, sl.cs, &sl.exec));
+    sl.batch = bi;
+    sl.issued = sl.read = 0;
+    sl.sampled = prof_unit_sampled(false);
+    return NT_OK;
+  };
+  // results of a finished batch back to the host, in input order
+  auto finish_batch = [&](Slot& sl) -> nt_status {
+    const Batch& bt = batches[sl.batch];
+    NT_TRY(read_impl(sl.st, sl.p_otok, sl.p_olen, sl.p_oscore, sl.p_olp, sl.s));
+    const int Tcap = sl.st->Tcap;
+    for (int i = 0; i < bt.count; ++i) {
       const int sid = order[bt.first + i];
-      res_tok[sid].assign(p_otok + (size_t)i * Tcap, p_otok + (size_t)i * Tcap + p_olen[i]);
-      res_lp[sid].assign(p_olp + (size_t)i * Tcap, p_olp + (size_t)i * Tcap + p_olen[i]);
-      res_score[sid] = p_oscore[i];
+      res_tok[sid].assign(sl.p_otok + (size_t)i * Tcap, sl.p_otok + (size_t)i * Tcap + sl.p_olen[i]);
+      res_lp[sid].assign(sl.p_olp + (size_t)i * Tcap, sl.p_olp + (size_t)i * Tcap + sl.p_olen[i]);
+      res_score[sid] = sl.p_oscore[i];
     }
+    free_state(sl.st);
+    sl.st = nullptr;
+    if (sl.exec) {
+      (void)hipGraphExecDestroy(sl.exec);
+      sl.exec = nullptr;
+    }
+    return NT_OK;
+  };
+
+  // Outcome of a slot's oldest step in flight (which must have completed or be waited for).
+  int finished = 0;
+  auto absorb_oldest = [&](Slot& sl) -> nt_status {
+    NT_HIP(hipEventSynchronize(sl.ev[sl.read % 2]));
+    NT_TRY(absorb_step(sl.st, sl.st->t));
+    ++sl.read;
+    if (sl.st->finished) {
+      NT_TRY(finish_batch(sl));
+      ++finished;
+    }
+    return NT_OK;
+  };
+  // Everything queued on every slot completes (before a timing sample runs alone).
+  auto drain = [&]() -> nt_status {
+    for (Slot& o : res.slots) {
+      NT_HIP(hipStreamSynchronize(o.s));
+      while (o.st && o.issued > o.read) NT_TRY(absorb_oldest(o));
+    }
+    return NT_OK;
+  };
+
+  // Scheduler: every slot keeps up to two decoder steps in flight on its own stream, so
+  // the small kernels of one batch's step overlap those of the others; the host reads a
+  // step's outcome (the control-block mirror) while later steps run.  A step issued after
+  // its batch's last one finds nothing live and does nothing.  Kernel timing (when
+  // enabled) only ever covers sampled units, each run alone.
+  ProfModeScope untimed(PROF_NONE);
+  int next = 0, rr = 0;
+  while (finished < nb) {
+    bool progressed = false;
+    for (Slot& sl : res.slots) {
+      if (!sl.st && next < nb) {
+        if (prof_unit_sampled(true)) {
+          NT_TRY(drain());
+          ProfModeScope all(PROF_ALL);
+          NT_TRY(start_batch(sl, next++));
+          NT_HIP(hipStreamSynchronize(sl.s));
+        } else {
+          NT_TRY(start_batch(sl, next++));
+        }
+        progressed = true;
+      }
+      if (!sl.st || sl.st->finished || sl.issued - sl.read >= 2) continue;
+      if (sl.sampled) {
+        if (sl.issued != sl.read) continue;          // wait for this slot's steps first
+        NT_TRY(drain());
+        if (!sl.st || sl.st->finished) continue;
+        {
+          ProfModeScope all(PROF_ALL);
+          NT_TRY(enqueue_step(sl.st, nullptr, nullptr, sl.s));
+        }
+        NT_HIP(hipEventRecord(sl.ev[sl.issued % 2], sl.s));
+        ++sl.issued;
+        NT_TRY(absorb_oldest(sl));
+      } else {
+        if (graphs) NT_HIP(hipGraphLaunch(sl.exec, sl.s));
+        else NT_TRY(enqueue_step(sl.st, nullptr, nullptr, sl.s));
+        NT_HIP(hipEventRecord(sl.ev[sl.issued % 2], sl.s));
+        ++sl.issued;
+      }
+      if (sl.st) sl.sampled = prof_unit_sampled(false);
+      progressed = true;
+    }
+    if (progressed) continue;
+    // wait for the oldest step of the next slot (round robin) that has one in flight
+    for (int k = 0; k < NS; ++k) {
+      Slot& sl = res.slots[(rr + k) % NS];
+      if (!sl.st || sl.issued == sl.read) continue;
+      rr = (rr + k + 1) % NS;
+      NT_TRY(absorb_oldest(sl));
+      break;
+    }
+  }
+  for (Slot& sl : res.slots) {
+    hipEvent_t e = sl.ev[0];
+    NT_HIP(hipEventRecord(e, sl.s));
+    NT_HIP(hipStreamWaitEvent(s, e, 0));   // later work on the caller's stream follows ours
   }
 
   int64_t total = 0;
@@ -1308,13 +1440,28 @@ nt_status nt_prof_config(uint32_t class_mask, int32_t stride) {
   g_prof_mask = class_mask & ((1u << NT_K_COUNT) - 1);
   g_prof_stride = stride;
   for (auto& c : g_prof_seen) c = 0;
-  g_prof_steps = 0;
+  g_prof_enc_units = g_prof_step_units = 0;
+  return NT_OK;
+}
+
+nt_status nt_prof_units(int64_t* encodes, int64_t* steps) {
+  g_err.clear();
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (encodes) *encodes = g_prof_enc_units;
+  if (steps) *steps = g_prof_step_units;
   return NT_OK;
 }
 
 nt_status nt_set_graphs(int32_t enable) {
   g_err.clear();
   g_use_graphs = enable != 0;
+  return NT_OK;
+}
+
+nt_status nt_set_streams(int32_t n) {
+  g_err.clear();
+  if (n < 1 || n > 8) return fail(NT_E_INVALID, "stream count %d outside [1, 8]", n);
+  g_streams = n;
   return NT_OK;
 }
 

@@ -21,6 +21,7 @@ namespace nt {
 namespace {
 
 constexpr int SEL_THREADS = 256;
+constexpr int SEL_BATCH = 8;      // row loads in flight per thread
 
 struct MaxSum {
   float m, s;
@@ -224,20 +225,33 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
   for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
   const bool vec = (V % 4) == 0 && ((reinterpret_cast<uintptr_t>(x) & 15) == 0);
   if (vec) {
+    // SEL_BATCH loads of a thread are issued together before any is used (one memory
+    // latency per batch instead of per element group)
     const float4* x4 = reinterpret_cast<const float4*>(x);
-    for (int i = tid; i < V / 4; i += SEL_THREADS) {
-      const float4 q = x4[i];
-      const float mx = fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w));
-      if (mx > acc.m) {
-        acc.s = acc.m == -INFINITY ? 0.f : acc.s * __expf(acc.m - mx);
-        acc.m = mx;
+    const int nv = V / 4;
+    for (int i0 = tid; i0 < nv; i0 += SEL_THREADS * SEL_BATCH) {
+      float4 qs[SEL_BATCH];
+#pragma unroll
+      for (int u = 0; u < SEL_BATCH; ++u) {
+        const int i = i0 + u * SEL_THREADS;
+        qs[u] = i < nv ? x4[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
       }
-      acc.s += __expf(q.x - acc.m) + __expf(q.y - acc.m) + __expf(q.z - acc.m) + __expf(q.w - acc.m);
-      if (mx > v[K2 - 1]) {
-        list_insert<K2>(v, ix, q.x, 4 * i);
-        list_insert<K2>(v, ix, q.y, 4 * i + 1);
-        list_insert<K2>(v, ix, q.z, 4 * i + 2);
-        list_insert<K2>(v, ix, q.w, 4 * i + 3);
+#pragma unroll
+      for (int u = 0; u < SEL_BATCH; ++u) {
+        const int i = i0 + u * SEL_THREADS;
+        const float4 q = qs[u];
+        const float mx = fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w));
+        if (mx > acc.m) {
+          acc.s = acc.m == -INFINITY ? 0.f : acc.s * __expf(acc.m - mx);
+          acc.m = mx;
+        }
+        if (i < nv) acc.s += __expf(q.x - acc.m) + __expf(q.y - acc.m) + __expf(q.z - acc.m) + __expf(q.w - acc.m);
+        if (mx > v[K2 - 1]) {
+          list_insert<K2>(v, ix, q.x, 4 * i);
+          list_insert<K2>(v, ix, q.y, 4 * i + 1);
+          list_insert<K2>(v, ix, q.z, 4 * i + 2);
+          list_insert<K2>(v, ix, q.w, 4 * i + 3);
+        }
       }
     }
   } else {
@@ -503,11 +517,24 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   // ancestor table of the new beam: slot s < t lives where the parent's slot s lives;
   // slot t is the parent's own row (written this step)
-  const int nk = nk_cnt[wave];
-  for (int k = 0; k < nk; ++k) {
-    const int p = b * K + k, par = nk_par[wave][k];
-    for (int s = lane; s <= t; s += kWave)
-      anc_next[(size_t)p * st.Tcap + s] = s < t ? anc_cur[(size_t)par * st.Tcap + s] : par;
+  // (k, s) pairs spread over the lanes; each lane's reads are issued together
+  const int nk = nk_cnt[wave], n_pairs = nk * (t + 1);
+  constexpr int AB = 4;
+  for (int i0 = lane; i0 < n_pairs; i0 += kWave * AB) {
+    int val[AB];
+#pragma unroll
+    for (int u = 0; u < AB; ++u) {
+      const int i = i0 + u * kWave;
+      const int k = i / (t + 1), s = i - k * (t + 1);
+      val[u] = 0;
+      if (i < n_pairs) val[u] = s < t ? anc_cur[(size_t)nk_par[wave][k] * st.Tcap + s] : nk_par[wave][k];
+    }
+#pragma unroll
+    for (int u = 0; u < AB; ++u) {
+      const int i = i0 + u * kWave;
+      const int k = i / (t + 1), s = i - k * (t + 1);
+      if (i < n_pairs) anc_next[(size_t)(b * K + k) * st.Tcap + s] = val[u];
+    }
   }
 }
 
@@ -620,14 +647,14 @@ __global__ void scatter_logits_kernel(const float* __restrict__ src, const int* 
 hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, hipStream_t s) {
   const int rows = st.B * st.beam;
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(greedy_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, logits, forced, st);
+  NT_LAUNCH(greedy_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, logits, forced, st);
   return hipGetLastError();
 }
 
 hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, hipStream_t s) {
   const int rows = st.B * st.beam;
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(greedy_fused_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, st);
+  NT_LAUNCH(greedy_fused_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, st);
   return hipGetLastError();
 }
 
@@ -635,7 +662,7 @@ hipError_t beam_merge(const float* part, int n_tiles, const int* ctl, int beam, 
                       int* topi, float* lse, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (k2 > TOPK_MAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(beam_merge_kernel<TOPK_MAX>, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, ctl, beam, k2,
+  NT_LAUNCH(beam_merge_kernel<TOPK_MAX>, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, ctl, beam, k2,
                      topv, topi, lse);
   return hipGetLastError();
 }
@@ -644,7 +671,7 @@ hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, 
                        float* lse, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
 #define NT_SEL(K2)                                                                                          \
-  hipLaunchKernelGGL(beam_select_kernel<K2>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, ctl, beam, V, k2, topv, \
+  NT_LAUNCH(beam_select_kernel<K2>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, ctl, beam, V, k2, topv, \
                      topi, lse)
   if (k2 <= 4) NT_SEL(4);
   else if (k2 <= 8) NT_SEL(8);
@@ -658,33 +685,33 @@ hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, 
 hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, hipStream_t s) {
   if (st.B <= 0) return hipSuccess;
   if (st.beam * 2 * st.beam > MAXC * kWave || st.beam > 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(beam_update_kernel, dim3((st.B + 3) / 4), dim3(256), 0, s, topv, topi, lse, st);
+  NT_LAUNCH(beam_update_kernel, dim3((st.B + 3) / 4), dim3(256), 0, s, topv, topi, lse, st);
   return hipGetLastError();
 }
 
 hipError_t step_end(int* list, const int* done, int* ctl, int* host_ctl, int prune, int beam, int Tcap,
                     hipStream_t s) {
-  hipLaunchKernelGGL(step_end_kernel, dim3(1), dim3(1024), 0, s, list, done, ctl, host_ctl, prune, beam, Tcap);
+  NT_LAUNCH(step_end_kernel, dim3(1), dim3(1024), 0, s, list, done, ctl, host_ctl, prune, beam, Tcap);
   return hipGetLastError();
 }
 
 hipError_t finalize(const SearchState& st, int* out_tok, float* out_lp, int* out_len, float* out_score,
                     hipStream_t s) {
-  hipLaunchKernelGGL(finalize_kernel, dim3((st.B + 127) / 128), dim3(128), 0, s, st, out_tok, out_lp, out_len,
+  NT_LAUNCH(finalize_kernel, dim3((st.B + 127) / 128), dim3(128), 0, s, st, out_tok, out_lp, out_len,
                      out_score);
   return hipGetLastError();
 }
 
 hipError_t search_init(const SearchState& st, int* list, int* ctl, int bos, hipStream_t s) {
   const int n = st.B * st.beam;
-  hipLaunchKernelGGL(init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, st, list, ctl, bos);
+  NT_LAUNCH(init_kernel, dim3((n + 255) / 256), dim3(256), 0, s, st, list, ctl, bos);
   return hipGetLastError();
 }
 
 hipError_t scatter_logits(const float* logits, const int* sent_list, const int* ctl, int beam, int rows, int V,
                           float* dst, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(scatter_logits_kernel, dim3((V + 255) / 256 < 64 ? (V + 255) / 256 : 64, rows), dim3(256), 0,
+  NT_LAUNCH(scatter_logits_kernel, dim3((V + 255) / 256 < 64 ? (V + 255) / 256 : 64, rows), dim3(256), 0,
                      s, logits, sent_list, ctl, beam, V, dst);
   return hipGetLastError();
 }

@@ -29,7 +29,7 @@ EXPORTS = [
     "nt_weights_size", "nt_load_weights", "nt_free_model", "nt_workspace_size", "nt_translate_workspace_size",
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
-    "nt_op_gemm", "nt_prof_config", "nt_set_graphs",
+    "nt_op_gemm", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units",
 ]
 
 
@@ -86,6 +86,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_prof_enable": (c_int32, [c_uint32]),
         "nt_prof_config": (c_int32, [c_uint32, c_int32]),
         "nt_set_graphs": (c_int32, [c_int32]),
+        "nt_set_streams": (c_int32, [c_int32]),
+        "nt_prof_units": (c_int32, [POINTER(c_int64), POINTER(c_int64)]),
         "nt_prof_reset": (c_int32, []),
         "nt_prof_get": (c_int32, [c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
         "nt_op_gemm": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, P, P, c_int32, c_int32, c_int32,
@@ -241,6 +243,17 @@ def nt_prof_config(mask: int, stride: int):
 
 def nt_set_graphs(enable: bool):
     _check(load_library().nt_set_graphs(int(bool(enable))))
+
+
+def nt_set_streams(n: int):
+    _check(load_library().nt_set_streams(int(n)))
+
+
+def nt_prof_units() -> tuple:
+    """(batch encodes, decoder steps) counted by nt_translate since nt_prof_config."""
+    e, s = c_int64(), c_int64()
+    _check(load_library().nt_prof_units(ctypes.byref(e), ctypes.byref(s)))
+    return e.value, s.value
 
 
 def nt_prof_reset():

@@ -134,10 +134,10 @@ def test_batching_and_pruning_do_not_change_results(dtype, beam):
 
 
 @pytest.mark.parametrize("beam,prune", [(1, 1), (1, 0), (4, 1), (4, 0)])
-def test_graph_replay_matches_direct_launches(beam, prune):
-    """Launched kernel by kernel (the default), replayed as one captured decoder step per
-    batch, or replayed with every third step issued directly for event timing: the
-    results are bitwise the same."""
+def test_concurrency_and_graph_replay_do_not_change_results(beam, prune):
+    """Batches decoded one or several at a time, steps replayed as one captured decoder
+    step per batch (the default) or launched kernel by kernel, with or without every
+    third step issued directly for event timing: the results are bitwise the same."""
     from paper_2109_08008_amd import nt
     shape = SHAPES["d128"]
     blob = synth.make_weights(shape, seed=33, lively=True, eos_boost=4.0)
@@ -148,14 +148,21 @@ def test_graph_replay_matches_direct_launches(beam, prune):
     assert any(len(t) < synth.max_target_len(search, len(s)) for t, s in zip(ref_t, srcs)), "nothing finished early"
     runs = []
     try:
+        nt.nt_set_graphs(False)
+        for streams in (1, 2):
+            nt.nt_set_streams(streams)
+            runs.append(model.translate(ids, offs, search))
         nt.nt_set_graphs(True)
+        nt.nt_set_streams(1)
         runs.append(model.translate(ids, offs, search))
+        nt.nt_set_streams(3)
         nt.nt_prof_reset()
         nt.nt_prof_config((1 << len(nt.KERNEL_CLASSES)) - 1, 3)
         runs.append(model.translate(ids, offs, search))
         timed = nt.nt_prof_get(nt.KERNEL_CLASSES.index("gemm_vocab"))
     finally:
-        nt.nt_set_graphs(False)
+        nt.nt_set_graphs(True)
+        nt.nt_set_streams(3)
         nt.nt_prof_enable(0)
         nt.nt_prof_reset()
     assert timed["launches"] > 0
