@@ -37,6 +37,33 @@ PEAK = {  # MI355X published peaks (dense)
     "mfma_TFLOPs": {"f16": 2500.0, "bf16": 2500.0, "f32": 157.3},
 }
 GEMM_CLASSES = (0, 1, 2)
+
+# HBM-side bytes per launch of a kernel class on a workload, from two rocprofv3 --pmc
+# passes (FETCH_SIZE, WRITE_SIZE; KiB per dispatch averaged over every dispatch of the
+# class) scaled by what the same counters read for a plain 512 MiB device copy (FETCH_SIZE
+# reads half the bytes moved, WRITE_SIZE all of them).  Valid only for the kernel source
+# the counters were taken on (sha256 over `files`); otherwise the bench reports null.
+TRAFFIC = {
+    ("gemm_dec", "base-6-6"): {
+        "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
+        "sha256": "419085aae36f857770013f3d9a4d8095513520877d12b884a8e977c9f82e292a",
+        "fetch_kib": 3822.96, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+}
+
+
+def traffic_bytes(kernel: str, workload: str):
+    import hashlib
+    t = TRAFFIC.get((kernel, workload))
+    if t is None:
+        return None
+    h = hashlib.sha256()
+    for f in t["files"]:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != t["sha256"]:
+        return None   # the kernel changed since the counters were taken
+    return round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024)
 ENCODE_ONLY_CLASSES = (0, 3, 5)   # launched only by batch encodes (GEMM_ENC, DLCL, ATTN_ENC)
 
 
@@ -55,7 +82,7 @@ def parse_args():
     return ap.parse_args()
 
 
-def roofline_entry(cls: int, prof: dict, dtype: str) -> dict:
+def roofline_entry(cls: int, prof: dict, dtype: str, workload: str) -> dict:
     """Roofline of one kernel class from its event timings and algorithmic work."""
     from paper_2109_08008_amd import nt
     n = max(prof["launches"], 1)
@@ -72,7 +99,8 @@ def roofline_entry(cls: int, prof: dict, dtype: str) -> dict:
         bound, unit = "hbm", "GB/s"
     return {
         "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-        "frac": round(achieved / peak, 4), "traffic": None,
+        "frac": round(achieved / peak, 4), "traffic": traffic_bytes(nt.KERNEL_CLASSES[cls], workload),
+        "traffic_unit": "HBM-side bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
         "kernel": nt.KERNEL_CLASSES[cls], "launches": prof["launches"],
         "avg_us": round(prof["ms"] * 1e3 / n, 2),
         "alg_bytes_per_launch": round(prof["bytes"] / n), "alg_flops_per_launch": round(prof["flops"] / n),
@@ -203,7 +231,7 @@ def main():
             "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
             "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 3,
         },
-        "roofline": dict(roofline_entry(dominant, prof, w.dtype), sampled_units_stride=stride),
+        "roofline": dict(roofline_entry(dominant, prof, w.dtype, w.name), sampled_units_stride=stride),
         "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},
     }
     if not args.no_cpu_baseline:
