@@ -7,7 +7,7 @@ memory), with inputs and weights generated beforehand.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload base-6-6]
 
-Batches are decoded three at a time on their own streams (the library default), each
+Batches are decoded four at a time on their own streams (the library default), each
 decoder step replayed from a captured HIP graph.  The line carries a roofline entry for
 the dominant kernel class, timed with HIP events on the launch stream inside the timed
 region: about 12 units (decoder steps or batch encodes) are sampled, and each sample
@@ -229,7 +229,7 @@ def main():
             "source_tokens": int(offs[-1]), "target_tokens_per_step": n_tokens,
             "beam": w.search.beam, "token_budget": w.search.token_budget,
             "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
-            "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 3,
+            "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 4,
         },
         "roofline": dict(roofline_entry(dominant, prof, w.dtype, w.name), sampled_units_stride=stride),
         "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},

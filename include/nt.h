@@ -215,9 +215,9 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
  * with 0, every step is launched kernel by kernel). */
 nt_status nt_set_graphs(int32_t enable);
 
-/* Process-wide number of batches nt_translate decodes concurrently, 1..8 (default 3: with
- * HIP's four hardware queues per process, a fourth batch stream shares a queue with the
- * caller's and measured slower). */
+/* Process-wide number of batches nt_translate decodes concurrently, 1..8 (default 4: on
+ * MI355X with HIP's default of four hardware queues per process, 4 measured best with
+ * graph replay; 3 without it). */
 nt_status nt_set_streams(int32_t n);
 
 /* Thread-local message of the last failing call on this thread ("" if none). */

@@ -94,7 +94,7 @@ enum ProfMode { PROF_STRIDE = 0, PROF_NONE = 1, PROF_ALL = 2 };
 thread_local int g_prof_mode = PROF_STRIDE;
 int64_t g_prof_enc_units = 0, g_prof_step_units = 0;   // nt_translate units seen while profiling
 std::atomic<bool> g_use_graphs{true};   // nt_translate replays a captured decode step
-std::atomic<int> g_streams{3};          // batches nt_translate decodes concurrently
+std::atomic<int> g_streams{4};          // batches nt_translate decodes concurrently
 
 struct ProfModeScope {
   int saved;
@@ -1209,7 +1209,7 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
   struct Slot {
     hipStream_t s = nullptr;
     hipStream_t cs = nullptr;           // graph capture stream
-    hipEvent_t ev[2] = {nullptr, nullptr};
+    hipEvent_t ev[nt::CTL_MIRROR_SLOTS] = {};
     hipGraphExec_t exec = nullptr;
     char* ws = nullptr;
     int *p_src, *p_len, *p_maxlen, *p_olen, *p_otok, *h_ctl, *d_hctl;
@@ -1318,7 +1318,7 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
   // Outcome of a slot's oldest step in flight (which must have completed or be waited for).
   int finished = 0;
   auto absorb_oldest = [&](Slot& sl) -> nt_status {
-    NT_HIP(hipEventSynchronize(sl.ev[sl.read % 2]));
+    NT_HIP(hipEventSynchronize(sl.ev[sl.read % nt::CTL_MIRROR_SLOTS]));
     NT_TRY(absorb_step(sl.st, sl.st->t));
     ++sl.read;
     if (sl.st->finished) {
@@ -1342,6 +1342,7 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
   // its batch's last one finds nothing live and does nothing.  Kernel timing (when
   // enabled) only ever covers sampled units, each run alone.
   ProfModeScope untimed(PROF_NONE);
+  constexpr int depth = 2;   // steps in flight per slot (3 or 4 measured the same)
   int next = 0, rr = 0;
   while (finished < nb) {
     bool progressed = false;
@@ -1357,7 +1358,7 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
         }
         progressed = true;
       }
-      if (!sl.st || sl.st->finished || sl.issued - sl.read >= 2) continue;
+      if (!sl.st || sl.st->finished || sl.issued - sl.read >= depth) continue;
       if (sl.sampled) {
         if (sl.issued != sl.read) continue;          // wait for this slot's steps first
         NT_TRY(drain());
@@ -1366,13 +1367,13 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
           ProfModeScope all(PROF_ALL);
           NT_TRY(enqueue_step(sl.st, nullptr, nullptr, sl.s));
         }
-        NT_HIP(hipEventRecord(sl.ev[sl.issued % 2], sl.s));
+        NT_HIP(hipEventRecord(sl.ev[sl.issued % nt::CTL_MIRROR_SLOTS], sl.s));
         ++sl.issued;
         NT_TRY(absorb_oldest(sl));
       } else {
         if (graphs) NT_HIP(hipGraphLaunch(sl.exec, sl.s));
         else NT_TRY(enqueue_step(sl.st, nullptr, nullptr, sl.s));
-        NT_HIP(hipEventRecord(sl.ev[sl.issued % 2], sl.s));
+        NT_HIP(hipEventRecord(sl.ev[sl.issued % nt::CTL_MIRROR_SLOTS], sl.s));
         ++sl.issued;
       }
       if (sl.st) sl.sampled = prof_unit_sampled(false);

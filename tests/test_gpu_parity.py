@@ -162,7 +162,7 @@ def test_concurrency_and_graph_replay_do_not_change_results(beam, prune):
         timed = nt.nt_prof_get(nt.KERNEL_CLASSES.index("gemm_vocab"))
     finally:
         nt.nt_set_graphs(True)
-        nt.nt_set_streams(3)
+        nt.nt_set_streams(4)
         nt.nt_prof_enable(0)
         nt.nt_prof_reset()
     assert timed["launches"] > 0
