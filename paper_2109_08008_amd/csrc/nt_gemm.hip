@@ -133,41 +133,50 @@ __device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
   asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
   return v;
 }
+// LdsWait<FM, FN>::run<N>(a, b): wait until at most N LDS operations of this wave are
+// outstanding (reads complete in order, so every read issued before the last N has
+// landed), naming the fragments a and b as its operands.
 template <int FM, int FN> struct LdsWait;
 template <> struct LdsWait<1, 1> {
+  template <int N = 0>
   static __device__ __forceinline__ void run(u32x4 (&a)[1], u32x4 (&b)[1]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(b[0]));
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(b[0]) : [n] "i"(N));
   }
 };
 template <> struct LdsWait<1, 2> {
+  template <int N = 0>
   static __device__ __forceinline__ void run(u32x4 (&a)[1], u32x4 (&b)[2]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(b[0]), "+v"(b[1]));
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(b[0]), "+v"(b[1]) : [n] "i"(N));
   }
 };
 template <> struct LdsWait<2, 1> {
+  template <int N = 0>
   static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[1]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]));
-  }
-};
-template <> struct LdsWait<2, 4> {
-  static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[4]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
-  }
-};
-template <> struct LdsWait<4, 2> {
-  static __device__ __forceinline__ void run(u32x4 (&a)[4], u32x4 (&b)[2]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]));
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]) : [n] "i"(N));
   }
 };
 template <> struct LdsWait<2, 2> {
+  template <int N = 0>
   static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[2]) {
-    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]));
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]) : [n] "i"(N));
+  }
+};
+template <> struct LdsWait<2, 4> {
+  template <int N = 0>
+  static __device__ __forceinline__ void run(u32x4 (&a)[2], u32x4 (&b)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(a[1]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]) : [n] "i"(N));
+  }
+};
+template <> struct LdsWait<4, 2> {
+  template <int N = 0>
+  static __device__ __forceinline__ void run(u32x4 (&a)[4], u32x4 (&b)[2]) {
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]) : [n] "i"(N));
   }
 };
 template <> struct LdsWait<4, 4> {
+  template <int N = 0>
   static __device__ __forceinline__ void run(u32x4 (&a)[4], u32x4 (&b)[4]) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]));
+    asm volatile("s_waitcnt lgkmcnt(%[n])" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]), "+v"(b[2]), "+v"(b[3]) : [n] "i"(N));
   }
 };
 
@@ -331,19 +340,28 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     if (kt + STAGES - 1 < nk) NT_ISSUE(kt + STAGES - 1, slot == 0 ? STAGES - 1 : slot - 1)
     const unsigned char* As = lds + slot * STAGE_BYTES;
     const unsigned char* Bs = As + BM_ * ROWB;
+    // both halves of the k-step are read back to back; the second half's reads land
+    // while the first half's MFMAs run
+    u32x4 af0[FM], bf0[FN], af1[FM], bf1[FN];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      u32x4 af[FM], bf[FN];
+    for (int i = 0; i < FM; ++i) af0[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, fc));
 #pragma unroll
-      for (int i = 0; i < FM; ++i) af[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, kk * 4 + fc));
+    for (int j = 0; j < FN; ++j) bf0[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, fc));
 #pragma unroll
-      for (int j = 0; j < FN; ++j) bf[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, kk * 4 + fc));
-      LdsWait<FM, FN>::run(af, bf);
+    for (int i = 0; i < FM; ++i) af1[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, 4 + fc));
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+    for (int j = 0; j < FN; ++j) bf1[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, 4 + fc));
+    LdsWait<FM, FN>::template run<FM + FN>(af0, bf0);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af[i], bf[j], acc[i][j]);
-    }
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af0[i], bf0[j], acc[i][j]);
+    __builtin_amdgcn_sched_barrier(0);   // keep the second wait behind the first half's MFMAs
+    LdsWait<FM, FN>::template run<0>(af1, bf1);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af1[i], bf1[j], acc[i][j]);
     slot = slot == STAGES - 1 ? 0 : slot + 1;
   }
 #undef NT_ISSUE
@@ -397,9 +415,12 @@ hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int
 
 // Tile choice by problem size (measured on MI355X): LDS footprint matters more than
 // pipeline depth, so big tiles use two stages (two workgroups per CU).
-//   128x128, 2 stages (64 KB)  when that gives >= 512 tiles (vocabulary, encoder);
-//   128x64,  2 stages (48 KB)  when that gives >= 256 tiles;
-//   64x32,   3 stages (36 KB)  otherwise (skinny decode-step shapes, ~5 us).
+//   128x64,  2 stages (48 KB)  for N <= 2048 when that gives >= 320 tiles (encoder
+//                               projections at M = 8192: 5-15% faster than 128x128);
+//   128x128, 2 stages (64 KB)  when that gives >= 512 tiles (vocabulary, wide FFN);
+//   128x64                     when that gives >= 320 tiles;
+//   64x32,   3 stages (36 KB)  otherwise (skinny decode-step shapes, ~5 us; at M = 1300,
+//                               N = 1536 it beats 128x64 by 12%).
 // All reduce each output over K in the same order, so the choice never changes a result.
 template <typename T, int ROLE>
 hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi, hipStream_t s,
@@ -407,7 +428,7 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
   if (M <= 0 || N <= 0) return hipSuccess;
   const long long t128 = (long long)((M + 127) / 128) * ((N + 127) / 128);
   const long long t12864 = (long long)((M + 127) / 128) * ((N + 63) / 64);
-  if (tile == 0) tile = t128 >= 512 ? 2 : t12864 >= 256 ? 3 : 1;
+  if (tile == 0) tile = (N <= 2048 && t12864 >= 320) ? 3 : t128 >= 512 ? 2 : t12864 >= 320 ? 3 : 1;
   switch (tile) {
     case 2: return launch_tile<T, 128, 128, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
     case 3: return launch_tile<T, 128, 64, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
