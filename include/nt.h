@@ -211,6 +211,16 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
                      const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
                      int32_t relu, int32_t tile, void* stream);
 
+/* One selection step as the beam search runs it (Sec. 4.1, "Faster Beam Search" keeps 2K
+ * candidates per hypothesis; Sec. 4.4 drops log_softmax): for each of `rows` rows of
+ * d_logits [rows, V] fp32 (rows 16-byte aligned when V % 4 == 0), the k largest logits in
+ * (value desc, index asc) order into d_topv / d_topi [rows, k], and the row's log-sum-exp
+ * into d_lse [rows].  A logit of -inf is never selected: slots beyond a row's finite
+ * logits hold (-inf, INT32_MAX).  1 <= k <= 32 and k <= V.  Device pointers;
+ * asynchronous.  For tests. */
+nt_status nt_op_select(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv, int32_t* d_topi,
+                       float* d_lse, void* stream);
+
 /* Process-wide switch for nt_translate's graph replay of the decoder step (default on;
  * with 0, every step is launched kernel by kernel). */
 nt_status nt_set_graphs(int32_t enable);

@@ -202,6 +202,7 @@ hipError_t greedy_step(const float* logits, const int* forced, const SearchState
 
 // Beam: per live row, log-sum-exp and the 2K largest logits; then per live sentence the
 // candidate ranking, the walk, the stop rule and the ancestor-table update.
+// ctl may be null: then all `rows` rows are selected (kernel-level entry point).
 hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, int V, int k2, float* topv, int* topi,
                        float* lse, hipStream_t s);
 hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, hipStream_t s);

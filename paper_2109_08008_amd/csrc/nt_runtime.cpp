@@ -1434,6 +1434,16 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
   return NT_OK;
 }
 
+nt_status nt_op_select(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv, int32_t* d_topi,
+                       float* d_lse, void* stream) {
+  g_err.clear();
+  if (!d_logits || !d_topv || !d_topi || !d_lse) return fail(NT_E_INVALID, "null argument to nt_op_select");
+  if (rows < 0 || V <= 0) return fail(NT_E_INVALID, "rows must be >= 0 and V > 0");
+  if (k < 1 || k > 32 || k > V) return fail(NT_E_UNSUPPORTED, "k must be in [1, min(32, V)]");
+  NT_HIP(nt::beam_select(d_logits, nullptr, 1, rows, V, k, d_topv, d_topi, d_lse, static_cast<hipStream_t>(stream)));
+  return NT_OK;
+}
+
 nt_status nt_prof_config(uint32_t class_mask, int32_t stride) {
   g_err.clear();
   if (stride < 1) return fail(NT_E_INVALID, "stride must be >= 1");

@@ -212,7 +212,7 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
   __shared__ int wi[SEL_THREADS / kWave][K2];
   __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
   const int r = blockIdx.x;
-  if (r >= ctl[CTL_NLIVE] * beam) return;
+  if (ctl && r >= ctl[CTL_NLIVE] * beam) return;
   const float* x = logits + (size_t)r * V;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
 
@@ -299,6 +299,149 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
         if (head[q] >= K2 || wi[q][head[q]] == INT_MAX) continue;     // list exhausted
         if (bi == INT_MAX || better(wv[q][head[q]], wi[q][head[q]], bv, bi)) {
           bv = wv[q][head[q]]; bi = wi[q][head[q]]; w = q;
+        }
+      }
+      head[w]++;
+      topv[(size_t)r * k2 + j] = bv;
+      topi[(size_t)r * k2 + j] = bi;
+    }
+    MaxSum tot{sm[0], ss[0]};
+#pragma unroll
+    for (int w = 1; w < SEL_THREADS / kWave; ++w) tot = ms_merge(tot, MaxSum{sm[w], ss[w]});
+    lse_out[r] = tot.m + logf(tot.s);
+  }
+}
+
+// Beam selection for rows of at most SEL_THREADS * 4 * SEL_REG logits, held in registers:
+// pass 1 forms the online (max, sum exp) and each thread's maximum; the K2-th largest
+// thread maximum is a threshold that every one of the row's K2 best logits reaches (the
+// K2 largest thread maxima are K2 distinct logits at or above it); pass 2 inserts only
+// logits at or above it into the thread lists, which are then merged as in
+// beam_select_kernel.  Same result, without a list insertion for most logits.
+constexpr int SEL_REG = 32;        // float4 per thread -> rows up to 32768 logits
+template <int K2>
+__global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const float* __restrict__ logits,
+                                                                      const int* __restrict__ ctl, int beam, int V,
+                                                                      int k2, float* __restrict__ topv,
+                                                                      int* __restrict__ topi,
+                                                                      float* __restrict__ lse_out) {
+  __shared__ float wv[SEL_THREADS / kWave][K2];
+  __shared__ int wi[SEL_THREADS / kWave][K2];
+  __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
+  __shared__ float wmax[SEL_THREADS / kWave][K2];
+  __shared__ float thr_s;
+  const int r = blockIdx.x;
+  if (ctl && r >= ctl[CTL_NLIVE] * beam) return;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const float4* x4 = reinterpret_cast<const float4*>(logits + (size_t)r * V);
+  const int nv = V / 4;
+  float4 q[SEL_REG];
+#pragma unroll
+  for (int u = 0; u < SEL_REG; ++u) {
+    const int i = tid + u * SEL_THREADS;
+    q[u] = i < nv ? x4[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+  }
+  // pass 1: thread maximum, then the sum of exp against it
+  float tmax = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < SEL_REG; ++u) tmax = fmaxf(tmax, fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)));
+  MaxSum acc{tmax, 0.f};
+  if (tmax != -INFINITY) {
+#pragma unroll
+    for (int u = 0; u < SEL_REG; ++u)
+      acc.s += (__expf(q[u].x - tmax) + __expf(q[u].y - tmax)) + (__expf(q[u].z - tmax) + __expf(q[u].w - tmax));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; }
+  // the K2 largest thread maxima of each wave (K2 rounds of a wave max; one lane drops out)
+  {
+    float mine = tmax;
+    for (int j = 0; j < K2; ++j) {
+      float best = mine;
+      int bl = lane;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(best, o, kWave);
+        const int ol = __shfl_xor(bl, o, kWave);
+        if (ov > best || (ov == best && ol < bl)) { best = ov; bl = ol; }
+      }
+      if (lane == 0) wmax[wave][j] = best;
+      if (lane == bl) mine = -INFINITY;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // K2-th largest of the per-wave sorted lists
+    int head[SEL_THREADS / kWave] = {0, 0, 0, 0};
+    float t = -INFINITY;
+    for (int j = 0; j < K2; ++j) {
+      int w = 0;
+      float bv = -INFINITY;
+      for (int q2 = 0; q2 < SEL_THREADS / kWave; ++q2)
+        if (head[q2] < K2 && (wmax[q2][head[q2]] > bv || w < 0)) { bv = wmax[q2][head[q2]]; w = q2; }
+      head[w]++;
+      t = bv;
+    }
+    thr_s = t;
+  }
+  __syncthreads();
+  const float thr = thr_s;
+  // pass 2: bit masks of the logits at or above the threshold (bit 4*(u%8)+c of word u/8),
+  // then the few candidates go into the thread list in increasing index order, re-read
+  // from memory (the register copy cannot be indexed by a run-time position)
+  unsigned cand[SEL_REG / 8] = {};
+#pragma unroll
+  for (int u = 0; u < SEL_REG; ++u) {
+    const float4 x = q[u];
+    const unsigned bits = (x.x >= thr ? 1u : 0u) | (x.y >= thr ? 2u : 0u) | (x.z >= thr ? 4u : 0u) |
+                          (x.w >= thr ? 8u : 0u);
+    if (tid + u * SEL_THREADS < nv) cand[u / 8] |= bits << (4 * (u % 8));   // padding never re-read
+  }
+  float v[K2];
+  int ix[K2];
+#pragma unroll
+  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
+  const float* row = logits + (size_t)r * V;
+#pragma unroll
+  for (int wd = 0; wd < SEL_REG / 8; ++wd) {
+    unsigned m = cand[wd];
+    while (m) {
+      const int b = __builtin_ctz(m);
+      m &= m - 1;
+      const int idx = 4 * (tid + (wd * 8 + b / 4) * SEL_THREADS) + (b & 3);
+      list_insert<K2>(v, ix, row[idx], idx);
+    }
+  }
+  // merge: per wave K2 rounds of a (value desc, index asc) argmax, then thread 0 over waves
+  for (int round = 0; round < K2; ++round) {
+    float bv = v[0];
+    int bi = ix[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+    }
+    if (lane == 0) { wv[wave][round] = bv; wi[wave][round] = bi; }
+    if (ix[0] == bi && v[0] == bv && bi != INT_MAX) {
+#pragma unroll
+      for (int j = 0; j < K2 - 1; ++j) { v[j] = v[j + 1]; ix[j] = ix[j + 1]; }
+      v[K2 - 1] = -INFINITY;
+      ix[K2 - 1] = INT_MAX;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int head[SEL_THREADS / kWave] = {0, 0, 0, 0};
+    for (int j = 0; j < k2; ++j) {
+      int w = 0;
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+      for (int q2 = 0; q2 < SEL_THREADS / kWave; ++q2) {
+        if (head[q2] >= K2 || wi[q2][head[q2]] == INT_MAX) continue;
+        if (bi == INT_MAX || better(wv[q2][head[q2]], wi[q2][head[q2]], bv, bi)) {
+          bv = wv[q2][head[q2]]; bi = wi[q2][head[q2]]; w = q2;
         }
       }
       head[w]++;
@@ -670,6 +813,14 @@ hipError_t beam_merge(const float* part, int n_tiles, const int* ctl, int beam, 
 hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, int V, int k2, float* topv, int* topi,
                        float* lse, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  const bool reg = (V % 4) == 0 && V <= SEL_THREADS * 4 * SEL_REG && (reinterpret_cast<uintptr_t>(logits) & 15) == 0;
+  if (reg && k2 <= 8) {
+    if (k2 <= 4) NT_LAUNCH(beam_select_reg_kernel<4>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, ctl, beam, V, k2,
+                           topv, topi, lse);
+    else NT_LAUNCH(beam_select_reg_kernel<8>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, ctl, beam, V, k2, topv,
+                   topi, lse);
+    return hipGetLastError();
+  }
 #define NT_SEL(K2)                                                                                          \
   NT_LAUNCH(beam_select_kernel<K2>, dim3(rows), dim3(SEL_THREADS), 0, s, logits, ctl, beam, V, k2, topv, \
                      topi, lse)
