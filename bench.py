@@ -107,6 +107,57 @@ def roofline_entry(cls: int, prof: dict, dtype: str, workload: str) -> dict:
     }
 
 
+DECODE_CLASSES = (1, 2, 4, 6, 7, 8, 9)   # decoder-step kernels (LN also counts the encoder's LN2)
+
+
+def phase_rooflines(breakdown: dict, dtype: str) -> dict:
+    """The metric's two fractions from the all-class profile (every unit run alone):
+    encoder GEMM MFMA utilisation and the decode step's effective HBM rate (algorithmic
+    bytes / kernel time), both against MI355X's published peaks."""
+    from paper_2109_08008_amd import nt
+    enc = breakdown[nt.KERNEL_CLASSES[0]]
+    dec = [breakdown[nt.KERNEL_CLASSES[c]] for c in DECODE_CLASSES]
+    enc_tf = enc["flops"] / max(enc["ms"], 1e-9) / 1e9
+    dec_gbs = sum(x["bytes"] for x in dec) / max(sum(x["ms"] for x in dec), 1e-9) / 1e6
+    return {
+        "encoder_gemm_mfma": {"achieved": round(enc_tf, 2), "peak": PEAK["mfma_TFLOPs"][dtype], "unit": "TFLOP/s",
+                              "frac": round(enc_tf / PEAK["mfma_TFLOPs"][dtype], 4)},
+        "decode_step_hbm": {"achieved": round(dec_gbs, 2), "peak": PEAK["hbm_GBps"], "unit": "GB/s",
+                            "frac": round(dec_gbs / PEAK["hbm_GBps"], 4),
+                            "note": "algorithmic bytes of the decoder-step kernel classes / their kernel time"},
+    }
+
+
+def achievable_peaks() -> dict:
+    """Probes of what this GPU delivers: a 1 GiB device copy (GB/s of read + write) and a
+    large fp16 matrix product through the vendor library (torch.matmul -> hipBLASLt)."""
+    import torch
+    n = 1 << 28
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, dtype=torch.float16, device="cuda")
+    b = torch.randn(8192, 8192, dtype=torch.float16, device="cuda")
+
+    def timeit(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / 1e3 / reps
+
+    copy_s = timeit(lambda: dst.copy_(src), 10)
+    mm_s = timeit(lambda: torch.matmul(a, b), 10)
+    out = {"copy_GBps": round(2 * n * 4 / copy_s / 1e9, 1), "gemm_fp16_TFLOPs": round(2 * 8192 ** 3 / mm_s / 1e12, 1),
+           "note": "1 GiB device copy; torch.matmul 8192^3 fp16"}
+    del src, dst, a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 # ---- CPU oracle baseline ------------------------------------------------------------------
 _ORACLE = {}
 
@@ -162,6 +213,7 @@ def main():
     from paper_2109_08008_amd import nt
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    peaks = achievable_peaks()
     w = synth.WORKLOADS[args.workload]
     blob = synth.make_weights(w.model, seed=w.weights_seed)
     ids, offs = synth.make_sentences(w.data, w.model.vocab, seed=w.data_seed)
@@ -232,6 +284,8 @@ def main():
             "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 4,
         },
         "roofline": dict(roofline_entry(dominant, prof, w.dtype, w.name), sampled_units_stride=stride),
+        "phase_rooflines": phase_rooflines(breakdown, w.dtype),
+        "achievable_peaks": peaks,
         "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},
     }
     if not args.no_cpu_baseline:
