@@ -23,6 +23,11 @@ Readings of what the paper leaves open (each is also listed in the design notes)
 * Embedding: y_0 = sqrt(d) E[id] + PE(pos), PE interleaved sin/cos from position 0.
 * Attention scale 1/sqrt(d_head); ReLU FFN; biases on every projection except the
   tied output projection; LayerNorm with biased variance and eps = 1e-5.
+* Relative positions (the teachers are "Transformer-DLCL-RPR" with a maximum relative
+  length of 8, Sec. 3.1; the method is Shaw et al., 2018), optional and in encoder
+  self-attention only: per layer, key and value tables of 2k+1 rows of d_head shared by
+  the heads; query i and key j use row clip(j - i, -k, k) + k; the key row is added to
+  the key inside the scaled score, the value row to the value inside the weighted sum.
 """
 from __future__ import annotations
 
@@ -65,22 +70,39 @@ def logsumexp(x, axis=-1):
     return (m + np.log(np.exp(x - m).sum(axis=axis, keepdims=True))).squeeze(axis)
 
 
-def attention(q, k, v, n_heads, allowed=None):
+def rel_index(tq, tk, rel_k):
+    """Table row of query i and key j: clip(j - i, -rel_k, rel_k) + rel_k."""
+    return np.clip(np.arange(tk)[None, :] - np.arange(tq)[:, None], -rel_k, rel_k) + rel_k
+
+
+def attention(q, k, v, n_heads, allowed=None, rel=None):
     """Multi-head scaled dot-product attention on already-projected q [Tq,d], k/v [Tk,d].
 
     Head h uses columns h*dh..(h+1)*dh.  ``allowed`` [Tq,Tk] (bool) masks keys with -inf.
+    ``rel`` = (table_k, table_v, rel_k) adds relative position representations (shared
+    by the heads): score_ij = q_i . (k_j + table_k[r_ij]) / sqrt(dh) and
+    out_i = sum_j p_ij (v_j + table_v[r_ij]), r_ij = rel_index(...)[i, j].
     Returns the concatenated head outputs [Tq, d] (before the output projection).
     """
     tq, d = q.shape
     dh = d // n_heads
     out = np.empty((tq, d), dtype=q.dtype)
     scale = 1.0 / math.sqrt(dh)
+    if rel is not None:
+        ridx = rel_index(tq, k.shape[0], rel[2])
+        ak, av = rel[0][ridx], rel[1][ridx]          # [Tq, Tk, dh]
     for h in range(n_heads):
         sl = slice(h * dh, (h + 1) * dh)
-        s = (q[:, sl] @ k[:, sl].T) * q.dtype.type(scale)
+        s = q[:, sl] @ k[:, sl].T
+        if rel is not None:
+            s = s + np.einsum("id,ijd->ij", q[:, sl], ak)
+        s = s * q.dtype.type(scale)
         if allowed is not None:
             s = np.where(allowed, s, -np.inf)
-        out[:, sl] = softmax(s, axis=-1) @ v[:, sl]
+        p = softmax(s, axis=-1)
+        out[:, sl] = p @ v[:, sl]
+        if rel is not None:
+            out[:, sl] += np.einsum("ij,ijd->id", p, av)
     return out
 
 
@@ -158,7 +180,8 @@ class OracleModel:
         d = self.d
         u = self.ln(x, p + "ln1")
         qkv = u @ self.p[p + "W_qkv"] + self.p[p + "b_qkv"]
-        att = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], self.H)
+        rel = (self.p[p + "rel_k"], self.p[p + "rel_v"], self.shape.rel_k) if self.shape.rel_k > 0 else None
+        att = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], self.H, rel=rel)
         a = x + att @ self.p[p + "W_o"] + self.p[p + "b_o"]
         u = self.ln(a, p + "ln2")
         f = np.maximum(u @ self.p[p + "W_1"] + self.p[p + "b_1"], 0)

@@ -35,6 +35,7 @@ class ModelShape:
     n_dec: int
     vocab: int
     max_positions: int = MAX_POSITIONS
+    rel_k: int = 0          # relative positions in encoder self-attention: clip distance (0 = off)
 
     @property
     def d_head(self) -> int:
@@ -159,6 +160,9 @@ def weight_layout(m: ModelShape) -> list[Entry]:
             Entry(p + "W_1", (d, F), "normal"), Entry(p + "b_1", (F,), "normal"),
             Entry(p + "W_2", (F, d), "normal"), Entry(p + "b_2", (d,), "normal"),
         ]
+        if m.rel_k > 0:   # relative key / value tables [2k+1, d_head], shared by the heads
+            out += [Entry(p + "rel_k", (2 * m.rel_k + 1, m.d_head), "normal"),
+                    Entry(p + "rel_v", (2 * m.rel_k + 1, m.d_head), "normal")]
     out += [Entry("enc_out_ln.gamma", (d,), "gamma"), Entry("enc_out_ln.beta", (d,), "normal")]
     for j in range(Ld):
         p = f"dec.{j}."
@@ -192,6 +196,8 @@ def _lively_std(e: Entry, m: ModelShape, std: float) -> float:
         return 0.01 * r
     if e.name.startswith("dec.") and e.name.endswith(_LIVELY_DEC_ATTN):
         return 0.4 * r
+    if e.name.endswith((".rel_k", ".rel_v")):
+        return 0.5
     return std
 
 
