@@ -58,13 +58,20 @@ typedef struct nt_dec_state nt_dec_state;
  *  (Sec. 4.2 "FP16 Inference": reductions run in a wider type to avoid overflow).
  *  dlcl_hist_norm: 1 = each history entry is LayerNorm'd as in Eq. 2 (the default);
  *  0 = identity, so that one-hot DLCL weights give the plain pre-norm stack.
- *  ln_eps: LayerNorm epsilon (1e-5). */
+ *  ln_eps: LayerNorm epsilon (1e-5).
+ *  rel_pos_k: 0, or 1..16: relative position representations in encoder self-attention
+ *    (the teachers' RPR, Sec. 3.1, maximum relative length 8; Shaw et al. 2018): every
+ *    encoder layer then has a key and a value table of 2k+1 rows of d_head (fp32, shared
+ *    by the heads, after b_2 in the weight blob); query i and key j use row
+ *    clip(j - i, -k, k) + k, added to the key inside the scaled score and to the value
+ *    inside the weighted sum. */
 typedef struct {
   int32_t d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_positions;
   int32_t pad_id, bos_id, eos_id;
   int32_t dtype;
   int32_t dlcl_hist_norm;
   float ln_eps;
+  int32_t rel_pos_k;
 } nt_model_cfg;
 
 /* Search and batching options.

@@ -29,7 +29,16 @@ constexpr int KC = 64;       // keys per chunk of the one-wave-per-row self-atte
 // exact within chunks of 128 keys (scores kept in registers) with an online rescale
 // between chunks; exponentials and sums are fp32, P enters P.V in the model dtype.  Keys
 // past the group's length get -inf scores (their value rows are clamped to a valid one).
-template <typename T, int DH, int ROLE>
+//
+// RPR (relative positions, self-attention): before the keys, the wave forms
+// qa[i][m] = q_i . table_k[m] for its 16 queries in fp32, and each score gains
+// qa[i][clip(j - i) + k] before the scale.  The value rows' share,
+// sum_j p_ij table_v[clip(j - i) + k], is sum_m B_i[m] table_v[m] with B_i[m] the
+// probability mass of query i at relative row m: per chunk the probabilities go through
+// LDS and each (query, row) pair sums its keys in increasing order (rows inside the
+// clip have one key, the two edge rows every key beyond it); B is rescaled with O.
+constexpr int RPR_MAX = 33;     // 2k+1 for k <= 16
+template <typename T, int DH, int ROLE, bool RPR>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
   constexpr int EB = sizeof(T);
   constexpr int FE = 16 / EB;            // elements per 16-byte fragment
@@ -42,6 +51,12 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
   constexpr int VSTR = DH * EB / 4 + (EB == 2 ? 2 : 4);   // LDS row stride (dwords), spreads banks
   static_assert(DH % KSTEP == 0 && NSB % SB == 0, "head dim must fill whole MFMA steps");
   __shared__ __attribute__((aligned(16))) unsigned Vs[4][KSTEP][VSTR];
+  constexpr int RW = RPR ? 4 : 1;   // per-wave RPR buffers (1 placeholder when unused)
+  constexpr int RQ = RPR ? 16 : 1;
+  __shared__ float rp_qa[RW][RQ][RPR ? RPR_MAX : 1];        // q_i . table_k[m]
+  __shared__ float rp_p[RW][RQ][RPR ? NSB * 16 : 1];        // this chunk's probabilities
+  __shared__ float rp_b[RW][RQ][RPR ? RPR_MAX : 1];         // B_i[m]
+  __shared__ float rp_alpha[RW][RQ];
 
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int grp = lane >> 4, ln = lane & 15;
@@ -79,6 +94,26 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
 #pragma unroll
   for (int st = 0; st < QK; ++st) qf[st] = *reinterpret_cast<const u32x4*>(qrow + st * 64 + grp * 16);
 
+  const int RT = RPR ? 2 * a.rel_k + 1 : 0;
+  constexpr int RITEMS = RPR ? (16 * RPR_MAX + kWave - 1) / kWave : 1;   // (query, row) pairs per lane
+  float bacc[RITEMS];
+  if constexpr (RPR) {
+    // qa[i][m] = q_{q0+i} . table_k[m] over the full head, one pair per lane at a time
+    for (int it = lane; it < 16 * RT; it += kWave) {
+      const int i = it / RT, m = it - i * RT;
+      const T* qr = static_cast<const T*>(a.q) + (size_t)(g * a.q_per_group + min(q0 + i, nq - 1)) * a.q_ld + h * DH;
+      const float* tk = a.relk + (size_t)m * DH;
+      float dot = 0.f;
+#pragma unroll 8
+      for (int e = 0; e < DH; ++e) dot += to_f32(qr[e]) * tk[e];
+      rp_qa[wave][i][m] = dot;
+    }
+#pragma unroll
+    for (int t2 = 0; t2 < RITEMS; ++t2) bacc[t2] = 0.f;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  }
+
   float m = -INFINITY, lsum = 0.f;   // running max / sum of query q0+ln (same in all 4 groups)
   floatx4 o[CB];                     // O[q0 + 4*grp + r][c*16 + ln]
 #pragma unroll
@@ -101,7 +136,9 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int key = c0 + kb * 16 + 4 * grp + r;
-          sc[kb][r] = key < len ? acc[r] * a.scale : -INFINITY;
+          float raw = acc[r];
+          if constexpr (RPR) raw += rp_qa[wave][ln][min(max(key - (q0 + ln), -a.rel_k), a.rel_k) + a.rel_k];
+          sc[kb][r] = key < len ? raw * a.scale : -INFINITY;
           cmax = fmaxf(cmax, sc[kb][r]);
         }
       }
@@ -127,6 +164,34 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
       const float ar = __shfl(alpha, 4 * grp + r, kWave);   // alpha of query q0 + 4*grp + r
 #pragma unroll
       for (int c = 0; c < CB; ++c) o[c][r] *= ar;
+    }
+    if constexpr (RPR) {
+      // this chunk's probability mass of every (query, relative row) pair
+#pragma unroll
+      for (int kb = 0; kb < NSB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) rp_p[wave][ln][kb * 16 + 4 * grp + r] = sc[kb][r];
+      if (grp == 0) rp_alpha[wave][ln] = alpha;
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+#pragma unroll
+      for (int t2 = 0; t2 < RITEMS; ++t2) {
+        const int it = lane + t2 * kWave;
+        if (it >= 16 * RT) continue;
+        const int i = it / RT, rel = it - i * RT - a.rel_k;
+        const int jq = q0 + i - c0;                 // the query's own position in chunk coordinates
+        int lo, hi;                                 // chunk keys of this row: [lo, hi)
+        if (rel == -a.rel_k) { lo = 0; hi = jq - a.rel_k + 1; }
+        else if (rel == a.rel_k) { lo = jq + a.rel_k; hi = NSB * 16; }
+        else { lo = jq + rel; hi = lo + 1; }
+        lo = max(lo, 0);
+        hi = min(hi, NSB * 16);
+        float sum = 0.f;
+        for (int j = lo; j < hi; ++j) sum += rp_p[wave][i][j];
+        bacc[t2] = bacc[t2] * rp_alpha[wave][i] + sum;
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     }
 
     for (int kb = 0; kb < nb; kb += SB) {
@@ -175,6 +240,25 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
     }
   }
 
+  if constexpr (RPR) {
+    // the value tables' share: O[i][ch] += sum_m B_i[m] table_v[m][ch]
+#pragma unroll
+    for (int t2 = 0; t2 < RITEMS; ++t2) {
+      const int it = lane + t2 * kWave;
+      if (it < 16 * RT) rp_b[wave][it / RT][it % RT] = bacc[t2];
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    for (int m = 0; m < RT; ++m) {
+      const float* tv = a.relv + (size_t)m * DH;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float bm = rp_b[wave][4 * grp + r][m];
+#pragma unroll
+        for (int c = 0; c < CB; ++c) o[c][r] += bm * tv[c * 16 + ln];
+      }
+    }
+  }
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int i = q0 + 4 * grp + r;
@@ -310,17 +394,26 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   }
 }
 
-template <typename T, int ROLE>
-hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
+template <typename T, int ROLE, bool RPR>
+hipError_t mha_launch(const MhaArgs& a, hipStream_t s) {
   const long long tasks = (long long)a.n_groups * a.H * ((a.q_per_group + 15) / 16);
   const dim3 grid((unsigned)((tasks + 3) / 4));
   switch (a.dh) {
-    case 32: NT_LAUNCH((attn_mfma_kernel<T, 32, ROLE>), grid, dim3(256), 0, s, a); break;
-    case 64: NT_LAUNCH((attn_mfma_kernel<T, 64, ROLE>), grid, dim3(256), 0, s, a); break;
-    case 128: NT_LAUNCH((attn_mfma_kernel<T, 128, ROLE>), grid, dim3(256), 0, s, a); break;
+    case 32: NT_LAUNCH((attn_mfma_kernel<T, 32, ROLE, RPR>), grid, dim3(256), 0, s, a); break;
+    case 64: NT_LAUNCH((attn_mfma_kernel<T, 64, ROLE, RPR>), grid, dim3(256), 0, s, a); break;
+    case 128: NT_LAUNCH((attn_mfma_kernel<T, 128, ROLE, RPR>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <typename T, int ROLE>
+hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
+  if (ROLE == 0 && a.rel_k > 0) {
+    if (!a.relk || !a.relv || a.rel_k > (RPR_MAX - 1) / 2 || !a.self_queries) return hipErrorInvalidValue;
+    return mha_launch<T, 0, true>(a, s);
+  }
+  return mha_launch<T, ROLE, false>(a, s);
 }
 
 template <typename T, int DH>

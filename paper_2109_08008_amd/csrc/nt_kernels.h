@@ -153,6 +153,11 @@ struct MhaArgs {
   int n_groups, H, dh;           // n_groups: launch maximum when ctl is set
   float scale;
   const int* ctl = nullptr;      // if set, the live group count is ctl[CTL_NLIVE]
+  // relative positions (self-attention only): tables [2*rel_k+1][dh] fp32 shared by the
+  // heads; query i, key j use row clip(j - i, -rel_k, rel_k) + rel_k
+  const float* relk = nullptr;
+  const float* relv = nullptr;
+  int rel_k = 0;
 };
 // role: 0 encoder self-attention, 1 encoder-decoder attention (symbol name only).
 hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s, int role = 0);

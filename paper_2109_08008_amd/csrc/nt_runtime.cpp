@@ -146,6 +146,7 @@ hipError_t timed(int cls, hipStream_t s, double bytes, double flops, F&& launch)
 struct EncLayerW {
   const float *ln1, *bqkv, *bo, *ln2, *b1, *b2;
   const void *Wqkv, *Wo, *W1, *W2;
+  const float *relk, *relv;   // [2k+1][d_head] relative-position tables, or null
 };
 struct DecLayerW {
   const float *ln1, *bqkv, *bo, *ln2, *bq, *boc, *ln3, *b1, *b2;
@@ -190,6 +191,7 @@ nt_status validate_cfg(const nt_model_cfg* c) {
   if (c->d_ffn % 64 != 0) return fail(NT_E_UNSUPPORTED, "d_ffn %% 64 != 0 (d_ffn=%d)", c->d_ffn);
   if (c->max_positions > 1024) return fail(NT_E_UNSUPPORTED, "max_positions > 1024");
   if (!(c->ln_eps > 0.f)) return fail(NT_E_INVALID, "ln_eps must be > 0");
+  if (c->rel_pos_k < 0 || c->rel_pos_k > 16) return fail(NT_E_UNSUPPORTED, "rel_pos_k %d outside [0, 16]", c->rel_pos_k);
   return NT_OK;
 }
 
@@ -197,13 +199,13 @@ nt_status validate_cfg(const nt_model_cfg* c) {
 struct ModelLayout {
   size_t total = 0;
   size_t E, pe, hist_ln, dlcl, enc_out_ln, Wkv_all, bkv_all, dec_out_ln;
-  struct Enc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2; };
+  struct Enc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2, relk, relv; };
   struct Dec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Woc, boc, ln3, W1, b1, W2, b2; };
   std::vector<Enc> enc;
   std::vector<Dec> dec;
   // host blob (fp32) offsets
   size_t hE, hhist, hdlcl, henc_out, hdec_out, host_floats;
-  struct HEnc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2; };
+  struct HEnc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2, relk, relv; };
   struct HDec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Wkv, bkv, Woc, boc, ln3, W1, b1, W2, b2; };
   std::vector<HEnc> henc;
   std::vector<HDec> hdec;
@@ -213,6 +215,7 @@ ModelLayout layout_of(const nt_model_cfg& c) {
   ModelLayout Lo;
   const size_t d = c.d_model, F = c.d_ffn, V = c.vocab, L = c.n_enc, Ld = c.n_dec;
   const size_t eb = c.dtype == NT_F32 ? 4 : 2;
+  const size_t dh = d / c.n_heads, rt = c.rel_pos_k > 0 ? 2 * (size_t)c.rel_pos_k + 1 : 0;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -235,6 +238,8 @@ ModelLayout layout_of(const nt_model_cfg& c) {
     e.b1 = take(F * 4);
     e.W2 = take(d * F * eb);
     e.b2 = take(d * 4);
+    e.relk = rt ? take(rt * dh * 4) : 0;
+    e.relv = rt ? take(rt * dh * 4) : 0;
     Lo.enc.push_back(e);
   }
   Lo.enc_out_ln = take(2 * d * 4);
@@ -279,6 +284,8 @@ ModelLayout layout_of(const nt_model_cfg& c) {
     e.b1 = h; h += F;
     e.W2 = h; h += F * d;
     e.b2 = h; h += d;
+    e.relk = h; h += rt * dh;
+    e.relv = h; h += rt * dh;
     Lo.henc.push_back(e);
   }
   Lo.henc_out = h; h += 2 * d;
@@ -519,6 +526,9 @@ nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
     ma.H = m.H;
     ma.dh = m.dh;
     ma.scale = 1.0f / std::sqrt((float)m.dh);
+    ma.relk = w.relk;
+    ma.relv = w.relv;
+    ma.rel_k = m.cfg.rel_pos_k;
     NT_HIP(timed(NT_K_ATTN_ENC, s, 4.0 * T * d * eb, 4.0 * B * (double)S * S * d, [&] { return nt::mha(m.dt, ma, s); }));
 
     e = nt::GemmEpi{};
@@ -1019,6 +1029,11 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     NT_HIP(vec(D.b1, Hh.b1, F));
     NT_HIP(mat(D.W2, Hh.W2, F, d));
     NT_HIP(vec(D.b2, Hh.b2, d));
+    if (cfg->rel_pos_k > 0) {
+      const size_t rn = (2 * (size_t)cfg->rel_pos_k + 1) * (d / cfg->n_heads);
+      NT_HIP(vec(D.relk, Hh.relk, rn));
+      NT_HIP(vec(D.relv, Hh.relv, rn));
+    }
   }
   NT_HIP(vec(Lo.enc_out_ln, Lo.henc_out, 2 * d));
   const size_t eb = dt == DT::F32 ? 4 : 2;
@@ -1076,7 +1091,8 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
   for (int i = 0; i < L; ++i) {
     const auto& D = Lo.enc[i];
     m->enc.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.b1), fp(D.b2), base + D.Wqkv, base + D.Wo,
-                      base + D.W1, base + D.W2});
+                      base + D.W1, base + D.W2, cfg->rel_pos_k > 0 ? fp(D.relk) : nullptr,
+                      cfg->rel_pos_k > 0 ? fp(D.relv) : nullptr});
   }
   m->enc_out_ln = fp(Lo.enc_out_ln);
   for (int j = 0; j < Ld; ++j) {

@@ -38,7 +38,7 @@ def test_every_declared_function_is_exported(nt):
 
 def test_struct_layouts_match_header(nt):
     import ctypes
-    assert ctypes.sizeof(nt.nt_model_cfg) == 13 * 4
+    assert ctypes.sizeof(nt.nt_model_cfg) == 14 * 4
     assert ctypes.sizeof(nt.nt_search_cfg) == 8 * 4
 
 
