@@ -111,6 +111,15 @@ WORKLOADS = {
         "f16",
         "Deep-shallow 35-1, d=512, 8192 sentences, beam 4, length penalty 0.6, budget 16384, fp16",
     ),
+    "base-6-6-rpr": Workload(
+        "base-6-6-rpr",
+        ModelShape(512, 8, 2048, 6, 6, 32000, rel_k=8),
+        DataSetup(2048, "lognormal", 25.0, 100, "zipf"),
+        SearchSetup(beam=4, len_penalty=0.0, max_len_a=1.5, max_len_b=10, token_budget=8192),
+        "f16",
+        "Base 6-6 with relative positions (k = 8) in encoder self-attention, as in the DLCL-RPR teachers; "
+        "otherwise base-6-6",
+    ),
     "wide-30-6": Workload(
         "wide-30-6",
         ModelShape(1024, 16, 4096, 30, 6, 32000),
