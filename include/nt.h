@@ -212,8 +212,8 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
  * ReLU if relu != 0.  A, Bt, resid and out are device arrays in `dtype` (out is fp32
  * if out_f32); rows of A are lda elements apart, rows of out/resid ldc elements apart;
  * Bt is [N][K] contiguous.  K % 64 == 0; rows of A start 16-byte aligned.  tile: 0 = chosen by
- * shape, 1 = 64x32, 2 = 128x128, 3 = 128x64 output tiles (the choice never changes a
- * result).  Asynchronous. */
+ * shape, 1 = 64x32, 2 = 128x128, 3 = 128x64, 4 = 64x128 output tiles (the choice never
+ * changes a result).  Asynchronous. */
 nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N, int32_t K,
                      const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
                      int32_t relu, int32_t tile, void* stream);

@@ -413,25 +413,28 @@ hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int
   return hipGetLastError();
 }
 
-// Tile choice by problem size (measured on MI355X): LDS footprint matters more than
-// pipeline depth, so big tiles use two stages (two workgroups per CU).
-//   128x64,  2 stages (48 KB)  for N <= 2048 when that gives >= 320 tiles (encoder
-//                               projections at M = 8192: 5-15% faster than 128x128);
-//   128x128, 2 stages (64 KB)  when that gives >= 512 tiles (vocabulary, wide FFN);
-//   128x64                     when that gives >= 320 tiles;
-//   64x32,   3 stages (36 KB)  otherwise (skinny decode-step shapes, ~5 us; at M = 1300,
-//                               N = 1536 it beats 128x64 by 12%).
+// Tile choice by problem size, measured on MI355X with four batches' GEMMs in flight at
+// once (how nt_translate runs them).  LDS footprint matters more than pipeline depth, so
+// the big tiles use two stages.
+//   M >= 4096 (encoder, big batches): 128x64 for N <= 2048, else 128x128;
+//   M*N < 1M outputs:  64x32, 3 stages (skinny decode-step shapes);
+//   M*N < 3M outputs:  64x128, 2 stages (1300x1536: 5.6 us against 6.8 at 64x32;
+//                      2160x1024x1024: 8.6 against 12.0);
+//   larger:            128x128, 2 stages (2160x1024x4096: 27.8 us against 43.8 at 64x32).
 // All reduce each output over K in the same order, so the choice never changes a result.
 template <typename T, int ROLE>
 hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi, hipStream_t s,
                   int tile) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  const long long t128 = (long long)((M + 127) / 128) * ((N + 127) / 128);
-  const long long t12864 = (long long)((M + 127) / 128) * ((N + 63) / 64);
-  if (tile == 0) tile = (N <= 2048 && t12864 >= 320) ? 3 : t128 >= 512 ? 2 : t12864 >= 320 ? 3 : 1;
+  if (tile == 0) {
+    const long long mn = (long long)M * N;
+    if (M >= 4096) tile = N <= 2048 ? 3 : 2;
+    else tile = mn < (1ll << 20) ? 1 : mn < (3ll << 20) ? 4 : 2;
+  }
   switch (tile) {
     case 2: return launch_tile<T, 128, 128, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
     case 3: return launch_tile<T, 128, 64, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
+    case 4: return launch_tile<T, 64, 128, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
     default: return launch_tile<T, 64, 32, 3, ROLE>(A, lda, Bt, M, N, K, epi, s);
   }
 }

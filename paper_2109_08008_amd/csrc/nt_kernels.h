@@ -90,7 +90,8 @@ struct GemmEpi {
 
 // role: 0 encoder, 1 decoder step, 2 output projection.  Only the kernel's symbol name
 // depends on it, so profiles separate the three uses.
-// tile: 0 = chosen by shape, 1 = 64x32, 2 = 128x128, 3 = 128x64 (never changes a result).
+// tile: 0 = chosen by shape, 1 = 64x32, 2 = 128x128, 3 = 128x64, 4 = 64x128 (never changes
+// a result).
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                 hipStream_t s, int role = 0, int tile = 0);
 

@@ -1436,7 +1436,7 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
   const int eb = dtype == NT_F32 ? 4 : 2;
   if (lda < K || (lda * eb) % 16 != 0 || ldc < N)
     return fail(NT_E_INVALID, "lda must be >= K with 16-byte rows, ldc >= N");
-  if (tile < 0 || tile > 3) return fail(NT_E_INVALID, "tile must be 0..3");
+  if (tile < 0 || tile > 4) return fail(NT_E_INVALID, "tile must be 0..4");
   if (relu && (d_resid || out_f32)) return fail(NT_E_UNSUPPORTED, "relu combines with neither resid nor fp32 out");
   if (d_resid && out_f32) return fail(NT_E_UNSUPPORTED, "resid needs a model-dtype output");
   nt::GemmEpi e{};

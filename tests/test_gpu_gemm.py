@@ -1,6 +1,6 @@
 """GPU: the MFMA GEMM (nt_op_gemm) against a plain fp64 matrix product.
 
-Covers both tile shapes, every dtype, the bias / ReLU / residual / fp32-output
+Covers every tile shape, every dtype, the bias / ReLU / residual / fp32-output
 epilogues, ragged M and N and K spanning several pipeline stages.  The same rows
 computed with either tile shape, or as part of a larger M, are bitwise identical
 (each output is reduced over K in one fixed order).
@@ -40,7 +40,7 @@ def _run(dtype, A, Bt, bias=None, resid=None, relu=False, out_f32=False, tile=0)
     return out.cpu()
 
 
-@pytest.mark.parametrize("tile", [1, 2, 3])
+@pytest.mark.parametrize("tile", [1, 2, 3, 4])
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("M,N,K", [(1, 8, 64), (37, 100, 512), (200, 520, 128), (300, 1000, 2048), (129, 136, 576)])
 def test_gemm_matches_fp64(dtype, tile, M, N, K):
@@ -78,6 +78,7 @@ def test_gemm_rows_do_not_depend_on_tile_or_batch(dtype):
     full128 = _run(dtype, A, Bt, bias=bias, tile=2)
     assert torch_equal(full64, full128)
     assert torch_equal(_run(dtype, A, Bt, bias=bias, tile=3), full128)
+    assert torch_equal(_run(dtype, A, Bt, bias=bias, tile=4), full128)
     part = _run(dtype, A[100:133].contiguous(), Bt, bias=bias, tile=1)
     assert torch_equal(part, full128[100:133])
     one = _run(dtype, A[5:6].contiguous(), Bt, bias=bias, tile=0)
