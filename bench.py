@@ -46,8 +46,8 @@ GEMM_CLASSES = (0, 1, 2)
 TRAFFIC = {
     ("gemm_dec", "base-6-6"): {
         "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
-        "sha256": "419085aae36f857770013f3d9a4d8095513520877d12b884a8e977c9f82e292a",
-        "fetch_kib": 3822.96, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
+        "sha256": "f22870ddef1b3c7040dd7422faac181d1ab1e60746b990d41c88d0e2d9b18168",
+        "fetch_kib": 3823.27, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 
