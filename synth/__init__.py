@@ -65,6 +65,16 @@ class DataSetup:
 
 
 @dataclass(frozen=True)
+class Member:
+    """One model of an ensemble workload: its shape, its weights' seed, and whether it is
+    a DLCL model (Eq. 2) or a plain pre-norm stack (one-hot DLCL rows with the identity
+    in place of the history LayerNorm, which is exactly the plain stack)."""
+    model: ModelShape
+    weights_seed: int
+    dlcl: bool = True
+
+
+@dataclass(frozen=True)
 class Workload:
     name: str
     model: ModelShape
@@ -74,10 +84,22 @@ class Workload:
     description: str = ""
     weights_seed: int = 0
     data_seed: int = 1
+    members: tuple = ()       # ensemble workloads: the Members (``model`` is the first one's)
+    ensemble_rule: int = 0    # 0: mean of the members' log-probs; 1: log of their mean probability
 
 
 # The five workloads of the benchmark table.  Budgets for the two workloads that
 # name none are 8192 padded source tokens.
+# The teachers of Sec. 2.2 (Table 1): 35 or 40 encoder layers, with or without DLCL, six
+# decoder layers, d = 512, 8 heads, relative positions with maximum distance 8.
+_TEACHER = dict(d_model=512, n_heads=8, d_ffn=2048, n_dec=6, vocab=32000, rel_k=8)
+_TEACHERS = (
+    Member(ModelShape(n_enc=35, **_TEACHER), 10, dlcl=False),
+    Member(ModelShape(n_enc=35, **_TEACHER), 11, dlcl=True),
+    Member(ModelShape(n_enc=40, **_TEACHER), 12, dlcl=False),
+    Member(ModelShape(n_enc=40, **_TEACHER), 13, dlcl=True),
+)
+
 WORKLOADS = {
     "tiny": Workload(
         "tiny",
@@ -119,6 +141,17 @@ WORKLOADS = {
         "f16",
         "Base 6-6 with relative positions (k = 8) in encoder self-attention, as in the DLCL-RPR teachers; "
         "otherwise base-6-6",
+    ),
+    "teacher-ensemble": Workload(
+        "teacher-ensemble",
+        _TEACHERS[0].model,
+        DataSetup(2998, "lognormal", 25.0, 100, "zipf"),
+        SearchSetup(beam=4, len_penalty=0.0, max_len_a=1.5, max_len_b=10, token_budget=8192),
+        "f16",
+        "Ensemble of the four teachers of Table 1 (35-6 and 40-6, each with and without DLCL, "
+        "relative positions k = 8, d=512), 2998 sentences (the size of newstest2018; lognormal mean 25, "
+        "max 100, Zipf(1.1) IDs), beam 4, mean of the members' log-probs, fp16",
+        members=_TEACHERS,
     ),
     "wide-30-6": Workload(
         "wide-30-6",
@@ -211,7 +244,7 @@ def _lively_std(e: Entry, m: ModelShape, std: float) -> float:
 
 
 def make_weights(m: ModelShape, seed: int = 0, eos_boost: float | None = None,
-                 std: float = 0.02, lively: bool = False) -> np.ndarray:
+                 std: float = 0.02, lively: bool = False, plain_stack: bool = False) -> np.ndarray:
     """Draw the fp32 weight blob in canonical order.
 
     Every entry is N(0, std) drawn in fp64; LayerNorm gains get +1 and DLCL row l
@@ -223,7 +256,9 @@ def make_weights(m: ModelShape, seed: int = 0, eos_boost: float | None = None,
     smaller std and the decoder's attention matrices with a larger one, so the
     emitted tokens depend on the source and the step, and boosts the EOS row of E
     (default x5) so hypotheses finish at varied steps.  ``eos_boost`` scales the EOS
-    row of E explicitly.
+    row of E explicitly.  ``plain_stack=True`` makes every DLCL row one-hot on its last
+    entry (W[l, l-1] = 1), the weights of a model without layer combination; it is run
+    with the history LayerNorm off.
     """
     rng = np.random.default_rng(seed)
     lay = weight_layout(m)
@@ -235,7 +270,11 @@ def make_weights(m: ModelShape, seed: int = 0, eos_boost: float | None = None,
         if e.init == "gamma":
             x += 1.0
         elif e.init == "dlcl":
-            x += 1.0 / e.dlcl_row
+            if plain_stack:
+                x = np.zeros(e.size)
+                x[-1] = 1.0
+            else:
+                x += 1.0 / e.dlcl_row
         blob[off:off + e.size] = x
         off += e.size
     if lively and eos_boost is None:
@@ -329,6 +368,11 @@ def stratified_subset(offs: np.ndarray, k: int) -> np.ndarray:
 def small_model(d_model=64, n_heads=4, d_ffn=None, n_enc=3, n_dec=2, vocab=97) -> ModelShape:
     """Shapes for fast tests (several GEMM tiles, a ragged vocab)."""
     return ModelShape(d_model, n_heads, d_ffn or 4 * d_model, n_enc, n_dec, vocab)
+
+
+def member_weights(w: Workload, **kw) -> list:
+    """Weight blobs of an ensemble workload's members, in member order."""
+    return [make_weights(mb.model, seed=mb.weights_seed, plain_stack=not mb.dlcl, **kw) for mb in w.members]
 
 
 def with_search(w: Workload, **kw) -> Workload:
