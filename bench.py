@@ -162,16 +162,21 @@ def achievable_peaks() -> dict:
 _ORACLE = {}
 
 
+def _oracle_translate(src):
+    import oracle
+    from oracle.ensemble import translate_ensemble
+    if isinstance(_ORACLE["model"], list):
+        return translate_ensemble(_ORACLE["model"], src, _ORACLE["search"], _ORACLE["rule"])
+    return oracle.translate(_ORACLE["model"], src, _ORACLE["search"])
+
+
 def _oracle_worker(idx):
     from threadpoolctl import threadpool_limits
-    import oracle
     with threadpool_limits(limits=1):
-        src = _ORACLE["srcs"][idx]
-        h = oracle.translate(_ORACLE["model"], src, _ORACLE["search"])
-        return len(h.tokens)
+        return len(_oracle_translate(_ORACLE["srcs"][idx]).tokens)
 
 
-def cpu_baseline(w: synth.Workload, blob, ids, offs, seconds: float, procs: int) -> dict:
+def cpu_baseline(w: synth.Workload, blobs, ids, offs, seconds: float, procs: int) -> dict:
     """The fp32 oracle on a length-stratified sample, split over processes (one BLAS
     thread each) the way the paper splits CPU decoding by lines."""
     import multiprocessing as mp
@@ -180,14 +185,17 @@ def cpu_baseline(w: synth.Workload, blob, ids, offs, seconds: float, procs: int)
 
     P = procs or min(16, os.cpu_count() or 1)
     srcs = synth.sentence_list(ids, offs)
-    model = oracle.OracleModel(w.model, blob, np.float32)
-    _ORACLE.update(model=model, srcs=srcs, search=w.search)
+    if w.members:
+        model = [oracle.OracleModel(mb.model, b, np.float32, hist_norm=mb.dlcl) for mb, b in zip(w.members, blobs)]
+    else:
+        model = oracle.OracleModel(w.model, blobs[0], np.float32)
+    _ORACLE.update(model=model, srcs=srcs, search=w.search, rule=w.ensemble_rule)
     # calibrate on the median-length sentence, then size the sample to ~`seconds` of work
     order = synth.stratified_subset(offs, len(srcs))
     probe = int(order[len(order) // 2])
     with threadpool_limits(limits=1):
         t0 = time.perf_counter()
-        oracle.translate(model, srcs[probe], w.search)
+        _oracle_translate(srcs[probe])
         t_one = time.perf_counter() - t0
     n = int(min(len(srcs), max(P, P * max(1, math.floor(seconds / max(t_one, 1e-3))))))
     sample = synth.stratified_subset(offs, n)
@@ -215,12 +223,16 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     peaks = achievable_peaks()
     w = synth.WORKLOADS[args.workload]
-    blob = synth.make_weights(w.model, seed=w.weights_seed)
+    blobs = synth.member_weights(w) if w.members else [synth.make_weights(w.model, seed=w.weights_seed)]
     ids, offs = synth.make_sentences(w.data, w.model.vocab, seed=w.data_seed)
     nt.nt_set_graphs(not args.no_graphs)
     if args.streams:
         nt.nt_set_streams(args.streams)
-    model = nt.Model(w.model, blob, w.dtype)
+    if w.members:   # ensemble decoding: every member scores each step
+        model = nt.Ensemble([nt.Model(mb.model, b, w.dtype, hist_norm=mb.dlcl) for mb, b in zip(w.members, blobs)],
+                            w.ensemble_rule)
+    else:
+        model = nt.Model(w.model, blobs[0], w.dtype)
     sc = nt.search_cfg(w.search)
     ws_bytes = nt.nt_translate_workspace_size(model.handle, sc, offs)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
@@ -288,8 +300,12 @@ def main():
         "achievable_peaks": peaks,
         "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},
     }
+    if w.members:
+        line["config"]["members"] = [f"{mb.model.n_enc}-{mb.model.n_dec}{'+DLCL' if mb.dlcl else ''}"
+                                     f"{f'+RPR{mb.model.rel_k}' if mb.model.rel_k else ''}" for mb in w.members]
+        line["config"]["ensemble_rule"] = ["mean log-prob", "log mean prob"][w.ensemble_rule]
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, blob, ids, offs, args.cpu_seconds, args.cpu_procs)
+        line["cpu_baseline"] = cpu_baseline(w, blobs, ids, offs, args.cpu_seconds, args.cpu_procs)
     else:
         line["cpu_baseline"] = None
     model.close()

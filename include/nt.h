@@ -124,7 +124,29 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
                           void* device_buf, size_t device_bytes, void* stream, nt_model** out);
 void nt_free_model(nt_model* m);
 
-/* ---- workspace (the memory pool) -------------------------------------------------------
+/* ---- ensembles -------------------------------------------------------------------------
+ * Ensemble decoding (the teacher ensemble of Sec. 2.2, Table 1): one model handle over
+ * n_members (1..8) loaded models that decode together.  At every step each member runs
+ * its own decoder, over its own encoder output and key/value caches, on the shared
+ * prefix; the search then ranks words by a combination s(w) of the members'
+ * log-probabilities log p_m(w) = logit_m(w) - logsumexp(logit_m), used where one model's
+ * log p(w) would be (hypothesis scores, length penalty, stop rule and the reported
+ * per-token values are all in s):
+ *   NT_ENS_MEAN_LOGP  (0): s(w) = (1/M) sum_m log p_m(w);
+ *   NT_ENS_LOG_MEAN_P (1): s(w) = log((1/M) sum_m p_m(w)).
+ * The paper names the ensemble but not its combination rule; both common readings are
+ * offered.  Members must share vocab, pad/bos/eos IDs and dtype; depth, width, heads,
+ * FFN size, DLCL history norm and relative positions may differ.  The handle borrows
+ * the members (they must outlive it) and is accepted wherever an nt_model* is taken
+ * (workspace sizes, nt_encode, nt_decode_step, nt_translate); nt_free_model frees only
+ * the handle.  An ensemble cannot be a member.  For an ensemble, nt_decode_step's
+ * d_logits receives s, and nt_dec_state_encoder_out reports the first member's encoder
+ * output.  NT_E_INVALID for a null pointer, a member count outside 1..8, an unknown
+ * rule, a nested ensemble or members that disagree. */
+typedef enum { NT_ENS_MEAN_LOGP = 0, NT_ENS_LOG_MEAN_P = 1 } nt_ensemble_rule;
+nt_status nt_ensemble(nt_model* const* members, int32_t n_members, int32_t rule, nt_model** out);
+
+/* ---- workspace (the memory pool)-------------------------------------------------------
  * Bytes of workspace needed to encode and decode one batch of up to max_sents sentences
  * padded to max_src tokens under `search` (beam width and length limits). */
 nt_status nt_workspace_size(const nt_model* m, const nt_search_cfg* search, int32_t max_sents,

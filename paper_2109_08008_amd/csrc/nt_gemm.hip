@@ -280,9 +280,17 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   static_assert((STAGES - 2) * LPW <= 63, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES * STAGE_BYTES];
 
+  // live rows of a decode step: the grid covers the whole batch, and the workgroups past
+  // the live tiles exit.  Live tiles take the lowest workgroup ids, which the dispatcher
+  // deals round-robin over the 8 XCDs, so a shrinking batch still spreads over all of them.
+  if (epi.ctl) {
+    M = min(M, epi.ctl[CTL_NLIVE] * epi.ctl_rows);
+    tiles_m = (M + BM_ - 1) / BM_;
+  }
   // --- tile assignment: XCD-contiguous, then grouped by 8 tile-rows ---
   const int ntiles = tiles_m * tiles_n;
   int pid = blockIdx.x;
+  if (pid >= ntiles) return;
   {
     const int q = ntiles / 8, r = ntiles % 8, xcd = pid % 8, idx = pid / 8;
     pid = xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
@@ -294,9 +302,6 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   const int tm = first_m + (pid % per_group) % gsize;
   const int tn = (pid % per_group) / gsize;
   const int m0 = tm * BM_, n0 = tn * BN_;
-  // live rows of a decode step (the grid covers the whole batch)
-  if (epi.ctl) M = min(M, epi.ctl[CTL_NLIVE] * epi.ctl_rows);
-  if (m0 >= M) return;
   const int t_slot = epi.ctl ? epi.ctl[CTL_T] : epi.t;
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;

@@ -183,6 +183,8 @@ struct SearchState {
   int B, beam, V, eos, Tcap;
   float alpha;
   int early_stop;
+  int logp_input;         // 1: the selection input already holds per-token scores (an
+                          // ensemble's combination), so no log-sum-exp is subtracted
   const int* sent_list;   // live sentences (logical order)
   const int* ctl;         // t = ctl[CTL_T], live list entries = ctl[CTL_NLIVE]
   float* score;           // [R] raw hypothesis scores
@@ -205,6 +207,17 @@ struct SearchState {
 // the update (token, log-prob, EOS / length stop).  forced: [R] (by phys row) or null.
 // Grids cover the whole batch (st.B * st.beam rows); rows past the live count return.
 hipError_t greedy_step(const float* logits, const int* forced, const SearchState& st, hipStream_t s);
+
+// Ensemble decoding: folds member `member` (0-based, of n_members) into the combined
+// per-token scores comb [rows][V] of the live rows (ctl-driven, rows = live sentences x
+// beam).  With lp = logit - logsumexp(row) of this member's fp32 logits:
+//   rule 0: comb = sum of lp over the members so far, divided by n_members after the last;
+//   rule 1: comb = logaddexp of lp over the members so far, minus log(n_members) after
+//           the last.
+// Member 0 initialises comb.  Grid: `rows` blocks (the whole batch); rows past the live
+// count return.
+hipError_t ens_combine(const float* logits, float* comb, const int* ctl, int beam, int rows, int V, int member,
+                       int n_members, int rule, hipStream_t s);
 
 // Beam: per live row, log-sum-exp and the 2K largest logits; then per live sentence the
 // candidate ranking, the walk, the stop rule and the ancestor-table update.

@@ -168,9 +168,16 @@ struct nt_model {
   const void* Wkv_all;    // [Ld*2d][d]
   const float* bkv_all;   // [Ld*2d]
   const float* dec_out_ln;
+  // an ensemble (nt_ensemble): the member models, borrowed, and the combination rule;
+  // empty for a loaded model, whose only member is itself
+  std::vector<nt_model*> members;
+  int rule = 0;
 };
 
 namespace {
+
+int n_members(const nt_model& m) { return m.members.empty() ? 1 : (int)m.members.size(); }
+const nt_model& member(const nt_model& m, int i) { return m.members.empty() ? m : *m.members[i]; }
 
 nt_status validate_cfg(const nt_model_cfg* c) {
   if (!c) return fail(NT_E_INVALID, "null model config");
@@ -317,21 +324,34 @@ ModelLayout layout_of(const nt_model_cfg& c) {
 
 // --------------------------------------------------------------------------------------
 // workspace arena of one batch
+struct MemberPlan {
+  size_t enc_out, cross, kself, vself;   // one model's encoder output and caches
+};
 struct WsPlan {
   size_t total = 0;
-  // persistent through the batch
-  size_t src, len, maxlen, enc_out, cross;
-  size_t kself, vself, score, cur_tok, tok_hist, par_hist, lp_hist, anc, done, best_score, best_raw, best_step,
+  // persistent through the batch: inputs, every member's caches, the search state
+  size_t src, len, maxlen;
+  std::vector<MemberPlan> mem;
+  size_t score, cur_tok, tok_hist, par_hist, lp_hist, anc, done, best_score, best_raw, best_step,
       best_row, best_nout, list, ctl, out_tok, out_lp, out_len, out_score;
-  // encoder temporaries (union with the decoder buffers below)
+  // encoder temporaries (union with the decoder buffers below); the members encode and
+  // step one after another, so they share both, sized for the largest member
   size_t hist, x, u, qkv, att, a, f, y;
-  // decoder buffers
-  size_t z, du, dq, datt, df, logits, topv, topi, lse;
+  // decoder buffers (comb: an ensemble's combined scores)
+  size_t z, du, dq, datt, df, logits, comb, topv, topi, lse;
 };
 
 WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   WsPlan p;
-  const size_t T = (size_t)B * S, R = (size_t)B * K, d = m.d, eb = m.eb;
+  const int M = n_members(m);
+  const size_t T = (size_t)B * S, R = (size_t)B * K, eb = m.eb;
+  size_t d = 0, F = 0, hist = 0;
+  for (int i = 0; i < M; ++i) {
+    const nt_model& mi = member(m, i);
+    d = std::max<size_t>(d, mi.d);
+    F = std::max<size_t>(F, mi.F);
+    hist = std::max<size_t>(hist, (size_t)(mi.L + 1) * mi.d);
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -341,10 +361,15 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.src = take(T * 4);
   p.len = take(B * 4);
   p.maxlen = take(B * 4);
-  p.enc_out = take(T * d * eb);
-  p.cross = take((size_t)m.Ld * 2 * T * d * eb);
-  p.kself = take((size_t)m.Ld * R * Tcap * d * eb);
-  p.vself = take((size_t)m.Ld * R * Tcap * d * eb);
+  p.mem.resize(M);
+  for (int i = 0; i < M; ++i) {
+    const nt_model& mi = member(m, i);
+    const size_t di = mi.d;
+    p.mem[i].enc_out = take(T * di * eb);
+    p.mem[i].cross = take((size_t)mi.Ld * 2 * T * di * eb);
+    p.mem[i].kself = take((size_t)mi.Ld * R * Tcap * di * eb);
+    p.mem[i].vself = take((size_t)mi.Ld * R * Tcap * di * eb);
+  }
   p.score = take(R * 4);
   p.cur_tok = take(R * 4);
   p.tok_hist = take((size_t)Tcap * R * 4);
@@ -365,13 +390,13 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.out_score = take(B * 4);
   const size_t base = off;
   // encoder temporaries
-  p.hist = take((size_t)(m.L + 1) * T * d * eb);
+  p.hist = take(hist * T * eb);
   p.x = take(T * d * eb);
   p.u = take(T * d * eb);
   p.qkv = take(T * 3 * d * eb);
   p.att = take(T * d * eb);
   p.a = take(T * d * eb);
-  p.f = take(T * m.F * eb);
+  p.f = take(T * F * eb);
   p.y = take(T * d * eb);
   const size_t enc_end = off;
   // decoder buffers reuse the same space
@@ -380,9 +405,10 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.du = take(R * d * eb);
   p.dq = take(R * d * eb);
   p.datt = take(R * d * eb);
-  p.df = take(R * m.F * eb);
+  p.df = take(R * F * eb);
   // fp32 logits, or (fused selection) the per-tile partial records, whichever is larger
   p.logits = take(std::max(R * m.V * 4, R * (size_t)((m.V + 127) / 128) * nt::topk_record(nt::TOPK_MAX) * 4));
+  p.comb = M > 1 ? take(R * m.V * 4) : 0;
   p.topv = take(R * 2 * K * 4);
   p.topi = take(R * 2 * K * 4);
   p.lse = take(R * 4);
@@ -436,6 +462,7 @@ struct nt_dec_state {
     s.Tcap = Tcap;
     s.alpha = sc.len_penalty;
     s.early_stop = sc.early_stop;
+    s.logp_input = n_members(*m) > 1 ? 1 : 0;
     s.sent_list = list();
     s.ctl = ctl();
     s.score = at<float>(plan.score);
@@ -459,8 +486,11 @@ struct nt_dec_state {
 namespace {
 
 // ---- encoder (Eq. 1-2) ---------------------------------------------------------------
-nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
-  const nt_model& m = *st->m;
+// Encoder of member mi (the model itself unless it is an ensemble) into that member's
+// encoder output and cross keys/values.
+nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
+  const nt_model& m = member(*st->m, mi);
+  const MemberPlan& mp = st->plan.mem[mi];
   const int B = st->B, S = st->S, d = m.d, L = m.L;
   const int T = B * S;
   const double eb = (double)m.eb;
@@ -492,7 +522,7 @@ nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
     a.w = m.dlcl + (size_t)l * (l - 1) / 2;
     a.x_out = l <= L ? at(p.x) : nullptr;
     a.ln = l <= L ? m.enc[l - 1].ln1 : m.enc_out_ln;
-    a.u_out = l <= L ? at(p.u) : at(p.enc_out);
+    a.u_out = l <= L ? at(p.u) : at(mp.enc_out);
     a.rows = T;
     a.d = d;
     a.eps = eps;
@@ -562,13 +592,13 @@ nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
   nt::GemmEpi e{};
   e.mode = nt::EPI_CROSS_KV;
   e.bias = m.bkv_all;
-  e.cross = at(p.cross);
+  e.cross = at(mp.cross);
   e.d = d;
   e.H = m.H;
   e.dh = m.dh;
   e.B = B;
   e.S = S;
-  NT_HIP(gemm_enc(at(p.enc_out), d, m.Wkv_all, 2 * d * m.Ld, d, e));
+  NT_HIP(gemm_enc(at(mp.enc_out), d, m.Wkv_all, 2 * d * m.Ld, d, e));
   return NT_OK;
 }
 
@@ -578,174 +608,211 @@ nt_status run_encoder(nt_dec_state* st, hipStream_t s) {
 // the same sequence serves every step and can be captured once and replayed.  R and t
 // below are the host's copy of the block and only feed the work figures of the timing.
 nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logits, hipStream_t s) {
-  const nt_model& m = *st->m;
+  const nt_model& top = *st->m;
+  const int M = n_members(top);
   const WsPlan& p = st->plan;
-  const int K = st->K, d = m.d, R = st->n_live * K, t = st->t;
+  const int K = st->K, R = st->n_live * K, t = st->t;
   const int Rp = st->B * K;
-  const double eb = (double)m.eb;
-  const float eps = m.cfg.ln_eps;
   auto at = [&](size_t o) { return st->ws + o; };
   int* list = st->list();
   int* ctl = st->ctl();
-
-  auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
-    const double ob = e.mode == nt::EPI_TOPK ? 0.0 : e.out_f32 ? 4.0 : eb;
-    const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
-    const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
-    const int tile = e.mode == nt::EPI_TOPK ? 2 : 0;   // the partial records assume 128-column tiles
-    nt::GemmEpi ec = e;
-    ec.ctl = ctl;
-    ec.ctl_rows = K;
-    return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, Rp, N, Kd, ec, s, role, tile); });
-  };
-
-  NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
-    return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, ctl, std::sqrt((float)d), m.dec[0].ln1,
-                            at(p.z), at(p.du), Rp, d, eps, s);
-  }));
-
-  for (int j = 0; j < m.Ld; ++j) {
-    const DecLayerW& w = m.dec[j];
-    char* kc = at(p.kself) + (size_t)j * Rp * st->Tcap * d * m.eb;
-    char* vc = at(p.vself) + (size_t)j * Rp * st->Tcap * d * m.eb;
-
-    nt::GemmEpi e{};
-    e.mode = nt::EPI_SELF_QKV;
-    e.bias = w.bqkv;
-    e.out = at(p.dq);
-    e.ldc = d;
-    e.sent_list = list;
-    e.beam = K;
-    e.kcache = kc;
-    e.vcache = vc;
-    e.Tcap = st->Tcap;
-    e.d = d;
-    e.H = m.H;
-    e.dh = m.dh;
-    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wqkv, 3 * d, d, e));
-
-    nt::SelfAttnArgs sa{};
-    sa.q = at(p.dq);
-    sa.kcache = kc;
-    sa.vcache = vc;
-    sa.sent_list = list;
-    sa.beam = K;
-    sa.anc = K > 1 ? st->at<int>(p.anc) : nullptr;
-    sa.anc_stride = st->anc_stride();
-    sa.out = at(p.datt);
-    sa.rows = Rp;
-    sa.H = m.H;
-    sa.dh = m.dh;
-    sa.Tcap = st->Tcap;
-    sa.scale = 1.0f / std::sqrt((float)m.dh);
-    sa.ctl = ctl;
-    NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * (2.0 + 2.0 * (t + 1)), 4.0 * R * (t + 1) * (double)d,
-                 [&] { return nt::self_attn(m.dt, sa, s); }));
-
-    e = nt::GemmEpi{};
-    e.mode = nt::EPI_RESID;
-    e.bias = w.bo;
-    e.resid = at(p.z);
-    e.out = at(p.z);
-    e.ldc = d;
-    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Wo, d, d, e));
-
-    NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), Rp, d, eps, s, ctl, K); }));
-
-    e = nt::GemmEpi{};
-    e.mode = nt::EPI_STORE;
-    e.bias = w.bq;
-    e.out = at(p.dq);
-    e.ldc = d;
-    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wq, d, d, e));
-
-    const size_t cross_layer = (size_t)2 * st->B * st->S * d;   // elements per layer (K and V)
-    nt::MhaArgs ma{};
-    ma.q = at(p.dq);
-    ma.q_ld = d;
-    ma.k = at(p.cross) + (size_t)j * cross_layer * m.eb;
-    ma.v = at(p.cross) + ((size_t)j * cross_layer + (size_t)st->B * st->S * d) * m.eb;
-    ma.kb = (long long)m.H * st->S * m.dh;
-    ma.kh = (long long)st->S * m.dh;
-    ma.ks = m.dh;
-    ma.out = at(p.datt);
-    ma.out_ld = d;
-    ma.group_map = list;
-    ma.lens = st->at<int>(p.len);
-    ma.q_per_group = K;
-    ma.self_queries = 0;
-    ma.n_groups = st->B;
-    ma.H = m.H;
-    ma.dh = m.dh;
-    ma.scale = 1.0f / std::sqrt((float)m.dh);
-    ma.ctl = ctl;
-    NT_HIP(timed(NT_K_ATTN_CROSS, s, ((double)st->n_live * 2 * st->S * d + 2.0 * R * d) * eb,
-                 4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s, 1); }));
-
-    e = nt::GemmEpi{};
-    e.mode = nt::EPI_RESID;
-    e.bias = w.boc;
-    e.resid = at(p.z);
-    e.out = at(p.z);
-    e.ldc = d;
-    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Woc, d, d, e));
-
-    NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                 [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), Rp, d, eps, s, ctl, K); }));
-
-    e = nt::GemmEpi{};
-    e.mode = nt::EPI_RELU;
-    e.bias = w.b1;
-    e.out = at(p.df);
-    e.ldc = m.F;
-    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.W1, m.F, d, e));
-
-    e = nt::GemmEpi{};
-    e.mode = nt::EPI_RESID;
-    e.bias = w.b2;
-    e.resid = at(p.z);
-    e.out = at(p.z);
-    e.ldc = d;
-    NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.df), m.F, w.W2, d, m.F, e));
-
-    const float* next_ln = j + 1 < m.Ld ? m.dec[j + 1].ln1 : m.dec_out_ln;
-    NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                 [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), Rp, d, eps, s, ctl, K); }));
-  }
-
   nt::SearchState ss = st->search();
-  // Tied output projection.  Normally the projection's epilogue reduces each row to
-  // per-tile (max, sum exp, best) partials and the logits never reach HBM; teacher
-  // forcing and the logits copy-out use the plain path that writes fp32 logits.
-  // (measured: the fused epilogue pays for itself for greedy's argmax; a top-8 per tile
-  // row costs more than writing and re-reading the logits, so beam keeps the plain path)
-  if (!d_logits && !d_forced && K == 1) {
-    const int n_tiles = (m.V + 127) / 128;
-    nt::GemmEpi e{};
-    e.mode = nt::EPI_TOPK;
-    e.part = st->at<float>(p.logits);
-    e.k2 = 1;
-    e.n_tiles = n_tiles;
-    NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
-    const float* part = st->at<float>(p.logits);
-    const double pbytes = (double)R * n_tiles * nt::topk_record(1) * 4;
-    NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, s); }));
-  } else {
-    nt::GemmEpi e{};
-    e.mode = nt::EPI_STORE;
-    e.out = at(p.logits);
-    e.ldc = m.V;
-    e.out_f32 = 1;
-    NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
-    if (d_logits) NT_HIP(nt::scatter_logits(st->at<float>(p.logits), list, ctl, K, Rp, m.V, d_logits, s));
-    if (K == 1) {
-      NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V,
-                   [&] { return nt::greedy_step(st->at<float>(p.logits), d_forced, ss, s); }));
+
+  // every member's decoder on the shared prefix (one member unless an ensemble)
+  for (int mi = 0; mi < M; ++mi) {
+    const nt_model& m = member(top, mi);
+    const MemberPlan& mp = p.mem[mi];
+    const int d = m.d;
+    const double eb = (double)m.eb;
+    const float eps = m.cfg.ln_eps;
+
+    auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
+      const double ob = e.mode == nt::EPI_TOPK ? 0.0 : e.out_f32 ? 4.0 : eb;
+      const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
+      const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
+      const int tile = e.mode == nt::EPI_TOPK ? 2 : 0;   // the partial records assume 128-column tiles
+      nt::GemmEpi ec = e;
+      ec.ctl = ctl;
+      ec.ctl_rows = K;
+      return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, Rp, N, Kd, ec, s, role, tile); });
+    };
+
+    NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
+      return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, ctl, std::sqrt((float)d), m.dec[0].ln1,
+                              at(p.z), at(p.du), Rp, d, eps, s);
+    }));
+
+    for (int j = 0; j < m.Ld; ++j) {
+      const DecLayerW& w = m.dec[j];
+      char* kc = at(mp.kself) + (size_t)j * Rp * st->Tcap * d * m.eb;
+      char* vc = at(mp.vself) + (size_t)j * Rp * st->Tcap * d * m.eb;
+
+      nt::GemmEpi e{};
+      e.mode = nt::EPI_SELF_QKV;
+      e.bias = w.bqkv;
+      e.out = at(p.dq);
+      e.ldc = d;
+      e.sent_list = list;
+      e.beam = K;
+      e.kcache = kc;
+      e.vcache = vc;
+      e.Tcap = st->Tcap;
+      e.d = d;
+      e.H = m.H;
+      e.dh = m.dh;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wqkv, 3 * d, d, e));
+
+      nt::SelfAttnArgs sa{};
+      sa.q = at(p.dq);
+      sa.kcache = kc;
+      sa.vcache = vc;
+      sa.sent_list = list;
+      sa.beam = K;
+      sa.anc = K > 1 ? st->at<int>(p.anc) : nullptr;
+      sa.anc_stride = st->anc_stride();
+      sa.out = at(p.datt);
+      sa.rows = Rp;
+      sa.H = m.H;
+      sa.dh = m.dh;
+      sa.Tcap = st->Tcap;
+      sa.scale = 1.0f / std::sqrt((float)m.dh);
+      sa.ctl = ctl;
+      NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * (2.0 + 2.0 * (t + 1)), 4.0 * R * (t + 1) * (double)d,
+                   [&] { return nt::self_attn(m.dt, sa, s); }));
+
+      e = nt::GemmEpi{};
+      e.mode = nt::EPI_RESID;
+      e.bias = w.bo;
+      e.resid = at(p.z);
+      e.out = at(p.z);
+      e.ldc = d;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Wo, d, d, e));
+
+      NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                   [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), Rp, d, eps, s, ctl, K); }));
+
+      e = nt::GemmEpi{};
+      e.mode = nt::EPI_STORE;
+      e.bias = w.bq;
+      e.out = at(p.dq);
+      e.ldc = d;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wq, d, d, e));
+
+      const size_t cross_layer = (size_t)2 * st->B * st->S * d;   // elements per layer (K and V)
+      nt::MhaArgs ma{};
+      ma.q = at(p.dq);
+      ma.q_ld = d;
+      ma.k = at(mp.cross) + (size_t)j * cross_layer * m.eb;
+      ma.v = at(mp.cross) + ((size_t)j * cross_layer + (size_t)st->B * st->S * d) * m.eb;
+      ma.kb = (long long)m.H * st->S * m.dh;
+      ma.kh = (long long)st->S * m.dh;
+      ma.ks = m.dh;
+      ma.out = at(p.datt);
+      ma.out_ld = d;
+      ma.group_map = list;
+      ma.lens = st->at<int>(p.len);
+      ma.q_per_group = K;
+      ma.self_queries = 0;
+      ma.n_groups = st->B;
+      ma.H = m.H;
+      ma.dh = m.dh;
+      ma.scale = 1.0f / std::sqrt((float)m.dh);
+      ma.ctl = ctl;
+      NT_HIP(timed(NT_K_ATTN_CROSS, s, ((double)st->n_live * 2 * st->S * d + 2.0 * R * d) * eb,
+                   4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s, 1); }));
+
+      e = nt::GemmEpi{};
+      e.mode = nt::EPI_RESID;
+      e.bias = w.boc;
+      e.resid = at(p.z);
+      e.out = at(p.z);
+      e.ldc = d;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Woc, d, d, e));
+
+      NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                   [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), Rp, d, eps, s, ctl, K); }));
+
+      e = nt::GemmEpi{};
+      e.mode = nt::EPI_RELU;
+      e.bias = w.b1;
+      e.out = at(p.df);
+      e.ldc = m.F;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.W1, m.F, d, e));
+
+      e = nt::GemmEpi{};
+      e.mode = nt::EPI_RESID;
+      e.bias = w.b2;
+      e.resid = at(p.z);
+      e.out = at(p.z);
+      e.ldc = d;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.df), m.F, w.W2, d, m.F, e));
+
+      const float* next_ln = j + 1 < m.Ld ? m.dec[j + 1].ln1 : m.dec_out_ln;
+      NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                   [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), Rp, d, eps, s, ctl, K); }));
+    }
+
+    // Tied output projection.  Normally the projection's epilogue reduces each row to
+    // per-tile (max, sum exp, best) partials and the logits never reach HBM; teacher
+    // forcing and the logits copy-out use the plain path that writes fp32 logits.
+    // (measured: the fused epilogue pays for itself for greedy's argmax; a top-8 per tile
+    // row costs more than writing and re-reading the logits, so beam keeps the plain path)
+    // An ensemble member writes its logits and folds them into the combined scores.
+    if (M > 1) {
+      nt::GemmEpi e{};
+      e.mode = nt::EPI_STORE;
+      e.out = at(p.logits);
+      e.ldc = m.V;
+      e.out_f32 = 1;
+      NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+      NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4 * (mi == 0 ? 2 : 3), 5.0 * R * m.V, [&] {
+        return nt::ens_combine(st->at<float>(p.logits), st->at<float>(p.comb), ctl, K, Rp, m.V, mi, M, top.rule, s);
+      }));
+    } else if (!d_logits && !d_forced && K == 1) {
+      const int n_tiles = (m.V + 127) / 128;
+      nt::GemmEpi e{};
+      e.mode = nt::EPI_TOPK;
+      e.part = st->at<float>(p.logits);
+      e.k2 = 1;
+      e.n_tiles = n_tiles;
+      NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+      const float* part = st->at<float>(p.logits);
+      const double pbytes = (double)R * n_tiles * nt::topk_record(1) * 4;
+      NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, s); }));
     } else {
-      NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V, [&] {
-        return nt::beam_select(st->at<float>(p.logits), ctl, K, Rp, m.V, 2 * K, st->at<float>(p.topv),
-                               st->at<int>(p.topi), st->at<float>(p.lse), s);
+      nt::GemmEpi e{};
+      e.mode = nt::EPI_STORE;
+      e.out = at(p.logits);
+      e.ldc = m.V;
+      e.out_f32 = 1;
+      NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+      if (d_logits) NT_HIP(nt::scatter_logits(st->at<float>(p.logits), list, ctl, K, Rp, m.V, d_logits, s));
+      if (K == 1) {
+        NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V,
+                     [&] { return nt::greedy_step(st->at<float>(p.logits), d_forced, ss, s); }));
+      } else {
+        NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4, 3.0 * R * m.V, [&] {
+          return nt::beam_select(st->at<float>(p.logits), ctl, K, Rp, m.V, 2 * K, st->at<float>(p.topv),
+                                 st->at<int>(p.topi), st->at<float>(p.lse), s);
+        }));
+        NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
+          return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, s);
+        }));
+      }
+    }
+  }   // members
+
+  if (M > 1) {   // selection over the ensemble's combined scores
+    const float* sc = st->at<float>(p.comb);
+    const int V = top.V;
+    if (d_logits) NT_HIP(nt::scatter_logits(sc, list, ctl, K, Rp, V, d_logits, s));
+    if (K == 1) {
+      NT_HIP(timed(NT_K_SELECT, s, (double)R * V * 4, 3.0 * R * V,
+                   [&] { return nt::greedy_step(sc, d_forced, ss, s); }));
+    } else {
+      NT_HIP(timed(NT_K_SELECT, s, (double)R * V * 4, 3.0 * R * V, [&] {
+        return nt::beam_select(sc, ctl, K, Rp, V, 2 * K, st->at<float>(p.topv), st->at<int>(p.topi),
+                               st->at<float>(p.lse), s);
       }));
       NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
         return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, s);
@@ -884,7 +951,8 @@ nt_status encode_impl(nt_model* m, const int32_t* d_src, const int32_t* d_len, c
   if (st->K > 1 &&
       (r = chk(hipMemsetAsync(st->at<int>(plan.anc), 0, sizeof(int) * 2 * (size_t)B * st->K * Tcap, s), "clear anc")) != NT_OK)
     return r;
-  if ((r = run_encoder(st, s)) != NT_OK) return bail(r);
+  for (int i = 0; i < n_members(*m); ++i)
+    if ((r = run_encoder(st, i, s)) != NT_OK) return bail(r);
   if ((r = chk(nt::search_init(st->search(), st->list(), st->ctl(), m->cfg.bos_id, s), "search init")) != NT_OK) return r;
   // an owned host copy of maxlen must not be freed before the copy has run
   if (!hx && (r = chk(hipStreamSynchronize(s), "sync")) != NT_OK) return r;
@@ -1109,6 +1177,33 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
 
 void nt_free_model(nt_model* m) { delete m; }
 
+nt_status nt_ensemble(nt_model* const* members, int32_t n_members, int32_t rule, nt_model** out) {
+  g_err.clear();
+  if (!members || !out) return fail(NT_E_INVALID, "null argument to nt_ensemble");
+  if (n_members < 1 || n_members > 8) return fail(NT_E_INVALID, "an ensemble has 1..8 members, not %d", n_members);
+  if (rule != NT_ENS_MEAN_LOGP && rule != NT_ENS_LOG_MEAN_P) return fail(NT_E_INVALID, "unknown ensemble rule %d", rule);
+  int max_pos = 0;
+  for (int i = 0; i < n_members; ++i) {
+    const nt_model* mi = members[i];
+    if (!mi) return fail(NT_E_INVALID, "ensemble member %d is null", i);
+    if (!mi->members.empty()) return fail(NT_E_INVALID, "ensemble member %d is itself an ensemble", i);
+    const nt_model_cfg &c = mi->cfg, &c0 = members[0]->cfg;
+    if (c.vocab != c0.vocab || c.pad_id != c0.pad_id || c.bos_id != c0.bos_id || c.eos_id != c0.eos_id ||
+        c.dtype != c0.dtype)
+      return fail(NT_E_INVALID, "ensemble member %d differs from member 0 in vocab, special IDs or dtype", i);
+    max_pos = i == 0 ? c.max_positions : std::min(max_pos, c.max_positions);
+  }
+  nt_model* e = new nt_model();
+  *e = *members[0];   // vocabulary, special IDs and dtype; no weights are used through it
+  e->cfg.max_positions = max_pos;
+  e->enc.clear();
+  e->dec.clear();
+  e->members.assign(members, members + n_members);
+  e->rule = rule;
+  *out = e;
+  return NT_OK;
+}
+
 nt_status nt_workspace_size(const nt_model* m, const nt_search_cfg* search, int32_t max_sents, int32_t max_src,
                             size_t* bytes) {
   g_err.clear();
@@ -1174,10 +1269,10 @@ nt_status nt_dec_state_encoder_out(nt_dec_state* st, float* h_enc, void* stream)
   g_err.clear();
   if (!st || !h_enc) return fail(NT_E_INVALID, "null argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const nt_model& m = *st->m;
+  const nt_model& m = member(*st->m, 0);
   const size_t n = (size_t)st->B * st->S * m.d;
   std::vector<char> raw(n * m.eb);
-  NT_HIP(hipMemcpyAsync(raw.data(), st->ws + st->plan.enc_out, raw.size(), hipMemcpyDeviceToHost, s));
+  NT_HIP(hipMemcpyAsync(raw.data(), st->ws + st->plan.mem[0].enc_out, raw.size(), hipMemcpyDeviceToHost, s));
   NT_HIP(hipStreamSynchronize(s));
   for (size_t i = 0; i < n; ++i) {
     if (m.dt == DT::F32) {

@@ -140,7 +140,40 @@ __global__ __launch_bounds__(SEL_THREADS) void greedy_kernel(const float* __rest
   if (threadIdx.x != 0 || st.done[b]) return;
   int tok = forced ? forced[b] : bidx;
   if (tok < 0 || tok >= st.V) tok = st.eos;   // out-of-range forced ID or an all-NaN row: end the sentence
-  greedy_update(st, b, tok, x[tok] - lse, t);
+  greedy_update(st, b, tok, st.logp_input ? x[tok] : x[tok] - lse, t);
+}
+
+// Ensemble combination of one member's logits into the per-token scores (see
+// ens_combine): the row's log-sum-exp first, then one coalesced pass over the row.
+__global__ __launch_bounds__(SEL_THREADS) void ens_combine_kernel(const float* __restrict__ logits,
+                                                                  float* __restrict__ comb,
+                                                                  const int* __restrict__ ctl, int beam, int V,
+                                                                  int member, int n_members, int rule) {
+  const int r = blockIdx.x;
+  if (r >= ctl[CTL_NLIVE] * beam) return;   // block-uniform
+  const float* x = logits + (size_t)r * V;
+  float* c = comb + (size_t)r * V;
+  float lse, best;
+  int bidx;
+  row_lse_argmax(x, V, lse, best, bidx);
+  const bool first = member == 0, last = member == n_members - 1;
+  const float inv_m = 1.0f / (float)n_members, log_m = logf((float)n_members);
+  for (int v = threadIdx.x; v < V; v += SEL_THREADS) {
+    const float lp = x[v] - lse;
+    float o;
+    if (rule == 0) {
+      o = first ? lp : c[v] + lp;
+      if (last) o *= inv_m;
+    } else {
+      o = lp;
+      if (!first) {
+        const float a = c[v], hi = fmaxf(a, lp), lo = fminf(a, lp);
+        o = hi == -INFINITY ? -INFINITY : hi + log1pf(expf(lo - hi));
+      }
+      if (last) o -= log_m;
+    }
+    c[v] = o;
+  }
 }
 
 // Greedy selection from the projection's per-tile partials [rows][n_tiles][4]
@@ -563,7 +596,7 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
       const float v = topv[(size_t)r * K2 + i];
       const int w = topi[(size_t)r * K2 + i];
       if (w == INT_MAX) continue;           // fewer than 2K words in the vocabulary
-      const float lp = v - lse[r];
+      const float lp = st.logp_input ? v : v - lse[r];
       cv[c] = st.score[p] + lp;
       clp[c] = lp;
       ck[c] = k * V + w;
@@ -791,6 +824,15 @@ hipError_t greedy_step(const float* logits, const int* forced, const SearchState
   const int rows = st.B * st.beam;
   if (rows <= 0) return hipSuccess;
   NT_LAUNCH(greedy_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, logits, forced, st);
+  return hipGetLastError();
+}
+
+hipError_t ens_combine(const float* logits, float* comb, const int* ctl, int beam, int rows, int V, int member,
+                       int n_members, int rule, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (member < 0 || member >= n_members || (rule != 0 && rule != 1)) return hipErrorInvalidValue;
+  NT_LAUNCH(ens_combine_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, logits, comb, ctl, beam, V, member, n_members,
+            rule);
   return hipGetLastError();
 }
 

@@ -30,7 +30,9 @@ EXPORTS = [
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
     "nt_op_gemm", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units", "nt_op_select",
+    "nt_ensemble",
 ]
+NT_ENS_MEAN_LOGP, NT_ENS_LOG_MEAN_P = 0, 1
 
 
 class nt_model_cfg(ctypes.Structure):
@@ -69,6 +71,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_weights_size": (c_int32, [POINTER(nt_model_cfg), POINTER(c_size_t), POINTER(c_size_t)]),
         "nt_load_weights": (c_int32, [POINTER(nt_model_cfg), POINTER(c_float), c_size_t, P, c_size_t, P, POINTER(P)]),
         "nt_free_model": (None, [P]),
+        "nt_ensemble": (c_int32, [POINTER(P), c_int32, c_int32, POINTER(P)]),
         "nt_workspace_size": (c_int32, [P, POINTER(nt_search_cfg), c_int32, c_int32, POINTER(c_size_t)]),
         "nt_translate_workspace_size": (c_int32, [P, POINTER(nt_search_cfg), POINTER(c_int64), c_int32,
                                                   POINTER(c_size_t)]),
@@ -150,6 +153,14 @@ def nt_load_weights(cfg: nt_model_cfg, host_weights: np.ndarray, device_buf: int
 
 def nt_free_model(m):
     load_library().nt_free_model(m)
+
+
+def nt_ensemble(members, rule: int):
+    """Ensemble handle over member model handles (borrowed: they must outlive it)."""
+    arr = (c_void_p * max(len(members), 1))(*[m.value if isinstance(m, c_void_p) else m for m in members])
+    out = c_void_p()
+    _check(load_library().nt_ensemble(arr, len(members), rule, ctypes.byref(out)))
+    return out
 
 
 def nt_workspace_size(m, search: nt_search_cfg, max_sents: int, max_src: int) -> int:
@@ -274,25 +285,16 @@ def nt_prof_get(kernel_class: int) -> dict:
     return {"launches": n.value, "ms": ms.value, "bytes": by.value, "flops": fl.value}
 
 
-# ---- convenience wrapper ----------------------------------------------------------------
-class Model:
-    """A model loaded on the current CUDA (HIP) device; owns its torch weight buffer."""
+# ---- convenience wrappers ---------------------------------------------------------------
+class _Translator:
+    """nt_translate over a handle, with a cached torch workspace (the per-call memory pool)."""
 
-    def __init__(self, shape, blob: np.ndarray, dtype: str = "f16", hist_norm: bool = True, device=None):
-        import torch
-        self.shape = shape
-        self.dtype = dtype
-        self.cfg = model_cfg(shape, dtype, hist_norm)
-        self.host_floats, self.device_bytes = nt_weights_size(self.cfg)
-        if blob.size != self.host_floats:
-            raise ValueError(f"blob has {blob.size} floats, model needs {self.host_floats}")
-        self.device = torch.device(device or "cuda")
-        self.buf = torch.empty(self.device_bytes, dtype=torch.uint8, device=self.device)
-        self.handle = nt_load_weights(self.cfg, blob, self.buf.data_ptr(), self.device_bytes)
-        self._ws = None
+    handle = None
+    device = None
+    _ws = None
 
     def workspace(self, nbytes: int):
-        """A cached torch byte buffer of at least nbytes (the per-call memory pool)."""
+        """A cached torch byte buffer of at least nbytes."""
         import torch
         if self._ws is None or self._ws.numel() < nbytes:
             self._ws = None
@@ -321,3 +323,31 @@ class Model:
             self.close()
         except Exception:
             pass
+
+
+class Model(_Translator):
+    """A model loaded on the current CUDA (HIP) device; owns its torch weight buffer."""
+
+    def __init__(self, shape, blob: np.ndarray, dtype: str = "f16", hist_norm: bool = True, device=None):
+        import torch
+        self.shape = shape
+        self.dtype = dtype
+        self.cfg = model_cfg(shape, dtype, hist_norm)
+        self.host_floats, self.device_bytes = nt_weights_size(self.cfg)
+        if blob.size != self.host_floats:
+            raise ValueError(f"blob has {blob.size} floats, model needs {self.host_floats}")
+        self.device = torch.device(device or "cuda")
+        self.buf = torch.empty(self.device_bytes, dtype=torch.uint8, device=self.device)
+        self.handle = nt_load_weights(self.cfg, blob, self.buf.data_ptr(), self.device_bytes)
+        self._ws = None
+
+
+class Ensemble(_Translator):
+    """Ensemble decoding over loaded Models (kept alive here for the handle's lifetime)."""
+
+    def __init__(self, members: list, rule: int = NT_ENS_MEAN_LOGP):
+        self.members = list(members)
+        self.rule = rule
+        self.device = self.members[0].device
+        self.handle = nt_ensemble([m.handle for m in self.members], rule)
+        self._ws = None

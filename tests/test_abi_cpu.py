@@ -81,3 +81,17 @@ def test_null_arguments_are_errors_not_crashes(nt):
     assert lib.nt_prof_get(0, ctypes.byref(n), None, None, None) == nt.NT_OK
     lib.nt_free_state(None)
     lib.nt_free_model(None)
+
+
+def test_ensemble_arguments_are_checked_on_the_host(nt):
+    import ctypes
+    lib = nt.load_library()
+    out = ctypes.c_void_p()
+    arr = (ctypes.c_void_p * 2)(None, None)
+    assert lib.nt_ensemble(None, 1, 0, ctypes.byref(out)) == nt.NT_E_INVALID
+    assert lib.nt_ensemble(arr, 1, 0, None) == nt.NT_E_INVALID
+    for n, rule in [(0, 0), (9, 0), (1, 2), (1, -1)]:
+        assert lib.nt_ensemble(arr, n, rule, ctypes.byref(out)) == nt.NT_E_INVALID, (n, rule)
+    assert lib.nt_ensemble(arr, 2, 1, ctypes.byref(out)) == nt.NT_E_INVALID
+    assert "null" in lib.nt_last_error().decode()
+    assert out.value is None
