@@ -46,8 +46,8 @@ GEMM_CLASSES = (0, 1, 2)
 TRAFFIC = {
     ("gemm_dec", "base-6-6"): {
         "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
-        "sha256": "f22870ddef1b3c7040dd7422faac181d1ab1e60746b990d41c88d0e2d9b18168",
-        "fetch_kib": 3823.27, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
+        "sha256": "165e96ad91aeb9c69fdac821c94e4e8b155256bc69eaa1d4be44a839dec607bc",
+        "fetch_kib": 3886.29, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 
@@ -294,6 +294,7 @@ def main():
             "beam": w.search.beam, "token_budget": w.search.token_budget,
             "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
             "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 4,
+            "workspace_GB": round(ws_bytes / 1e9, 2),
         },
         "roofline": dict(roofline_entry(dominant, prof, w.dtype, w.name), sampled_units_stride=stride),
         "phase_rooflines": phase_rooflines(breakdown, w.dtype),
