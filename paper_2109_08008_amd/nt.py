@@ -65,6 +65,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with paper_2109_08008_amd.build.build_library()")
+    # torch ships its own HIP runtime.  Loaded first, it provides the libamdhip64.so.7 that
+    # libnt.so links against, so the process has one runtime and torch's device memory and
+    # streams are valid here; loaded after libnt.so, it would bring a second runtime.
+    import torch  # noqa: F401
     L = ctypes.CDLL(path)
     P = c_void_p
     sig = {
