@@ -20,7 +20,7 @@ have no value printed in the paper and are pinned only through those checks.
 """
 from .model import (  # noqa: F401
     OracleModel, layer_norm, positional_encoding, softmax, logsumexp, attention,
-    round_weights, param_count_formula,
+    round_weights, param_count_formula, e4m3_round, quantize_fp8_columns,
 )
 from .search import (  # noqa: F401
     greedy_search, beam_search, length_penalty, Hypothesis, translate, brute_force_best,

@@ -106,13 +106,54 @@ def attention(q, k, v, n_heads, allowed=None, rel=None):
     return out
 
 
+def e4m3_round(x) -> np.ndarray:
+    """Nearest FP8 E4M3 value (the OCP "fn" format: 4 exponent bits with bias 7, 3
+    mantissa bits, subnormals of 2^-9, no infinities, largest finite 448), ties to even;
+    magnitudes beyond 448 saturate to 448.  Returned as float64 values."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.abs(x)
+    _, E = np.frexp(a)                            # a = f * 2^E with f in [0.5, 1)
+    e = np.maximum(E - 1, -6)                     # binade exponent; below 2^-6 the step is 2^-9
+    step = np.ldexp(1.0, e - 3)                   # 3 mantissa bits
+    q = np.minimum(np.round(a / step) * step, 448.0)   # np.round: half to even
+    return np.copysign(q, x)
+
+
+def quantize_fp8_columns(w):
+    """FP8 E4M3 weight quantization with one scale per output column of an [in, out]
+    matrix (the lower-precision weights that the paper leaves to future work, Sec. 6):
+    scale_n = max_k |w[k, n]| / 448 computed in float32 (1 for an all-zero column), and
+    q[k, n] = e4m3_round(float32(w[k, n] / scale_n)), the division in float32 too.
+    Returns (q as float64 values, scale as float32); the weight stands for q * scale."""
+    w = np.asarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=0)
+    scale = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
+    q = e4m3_round((w / scale[None, :]).astype(np.float32))
+    return q, scale
+
+
 def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> np.ndarray:
-    """Return a copy of the fp32 blob whose *matrices* (E and every W_*) are rounded to
-    fp16 or bf16 (round to nearest even) and widened back.  Biases, LayerNorm and DLCL
-    scalars keep fp32: that is what a half-precision model stores in half precision.
+    """Return a copy of the fp32 blob whose *matrices* (E and every W_*) are rounded as
+    the GPU stores them and widened back.  "f16" / "bf16": round to nearest even.
+    "f8": the projection matrices W_* become q * scale of :func:`quantize_fp8_columns`
+    (exact in float64, which is then the returned dtype) and E is rounded to fp16, as
+    an FP8-weight model with fp16 activations stores them.  Biases, LayerNorm and DLCL
+    scalars keep fp32: that is what a reduced-precision model stores at full precision.
     """
     if precision == "f32":
         return blob.copy()
+    if precision == "f8":
+        out = blob.astype(np.float64)
+        off = 0
+        for e in synth.weight_layout(shape):
+            seg = blob[off:off + e.size]
+            if e.name == "E":
+                out[off:off + e.size] = seg.astype(np.float16)
+            elif ".W_" in e.name:
+                q, sc = quantize_fp8_columns(seg.reshape(e.shape))
+                out[off:off + e.size] = (q * sc.astype(np.float64)[None, :]).reshape(-1)
+            off += e.size
+        return out
     out = blob.copy()
     off = 0
     for e in synth.weight_layout(shape):
