@@ -64,7 +64,15 @@ typedef struct nt_dec_state nt_dec_state;
  *    encoder layer then has a key and a value table of 2k+1 rows of d_head (fp32, shared
  *    by the heads, after b_2 in the weight blob); query i and key j use row
  *    clip(j - i, -k, k) + k, added to the key inside the scaled score and to the value
- *    inside the weighted sum. */
+ *    inside the weighted sum.
+ *  fp8_weights: 0, or 1 with dtype NT_F16: FP8 weights (the paper leaves lower precision
+ *    to future work, Sec. 6).  Every projection matrix of the encoder and the decoder
+ *    (W_qkv, W_o, W_1, W_2, W_q, W_kv, W_oc) is stored as OCP FP8 E4M3 with one fp32
+ *    scale per output column: scale_n = max_k |W[k,n]| / 448 and q = the E4M3 value
+ *    nearest (ties to even) to W[k,n] / scale_n, both computed in fp32 by
+ *    nt_load_weights.  The projections multiply fp16 activations by q exactly (every
+ *    E4M3 value is an fp16 value) and scale the fp32 sums.  E (embedding and output
+ *    projection) stays fp16; activations and every reduction are as for NT_F16. */
 typedef struct {
   int32_t d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_positions;
   int32_t pad_id, bos_id, eos_id;
@@ -72,6 +80,7 @@ typedef struct {
   int32_t dlcl_hist_norm;
   float ln_eps;
   int32_t rel_pos_k;
+  int32_t fp8_weights;
 } nt_model_cfg;
 
 /* Search and batching options.
@@ -116,7 +125,8 @@ typedef struct {
 nt_status nt_weights_size(const nt_model_cfg* cfg, size_t* host_floats, size_t* device_bytes);
 
 /* Converts the host blob into the device layout: matrices rounded (nearest even) to the
- * model dtype and stored transposed ([out][in]) for the GEMMs, vectors kept in fp32, a
+ * model dtype (or, with fp8_weights, the projections quantized to FP8 E4M3 with their
+ * column scales) and stored transposed ([out][in]) for the GEMMs, vectors kept in fp32, a
  * sinusoidal position table computed once.  device_buf (>= device_bytes, 256-byte
  * aligned) is borrowed for the model's lifetime.  The host blob may be freed on return.
  * Synchronises `stream` before returning. */
@@ -235,10 +245,19 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
  * if out_f32); rows of A are lda elements apart, rows of out/resid ldc elements apart;
  * Bt is [N][K] contiguous.  K % 64 == 0; rows of A start 16-byte aligned.  tile: 0 = chosen by
  * shape, 1 = 64x32, 2 = 128x128, 3 = 128x64, 4 = 64x128 output tiles (the choice never
- * changes a result).  Asynchronous. */
+ * changes a result).  d_bscale: NULL, or (dtype NT_F16 only) Bt holds FP8 E4M3 bytes and
+ * column n of the product is multiplied by d_bscale[n] (fp32), as for the weights of an
+ * fp8_weights model; tiles 1 and 4 are then 32x64 and 64x64.  Asynchronous. */
 nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N, int32_t K,
                      const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
-                     int32_t relu, int32_t tile, void* stream);
+                     int32_t relu, int32_t tile, const float* d_bscale, void* stream);
+
+/* The FP8 weight quantization nt_load_weights applies with fp8_weights, on the host: W
+ * [in][out] fp32 (row-major, y = x W) -> q [out][in] E4M3 codes (OCP, bias 7, ties to
+ * even, saturating at 448) and scale [out] fp32, with scale[n] = max_k |W[k][n]| / 448
+ * (1 for an all-zero column) and q[n][k] = E4M3(W[k][n] / scale[n]).  Host pointers;
+ * no device work.  For tests. */
+nt_status nt_quantize_fp8(const float* h_W, int32_t in, int32_t out, uint8_t* h_q, float* h_scale);
 
 /* One selection step as the beam search runs it (Sec. 4.1, "Faster Beam Search" keeps 2K
  * candidates per hypothesis; Sec. 4.4 drops log_softmax): for each of `rows` rows of

@@ -21,6 +21,8 @@
 // result does not depend on how many other rows share the launch (batch invariance).
 #include <limits.h>
 
+#include <type_traits>
+
 #include "nt_common.h"
 #include "nt_kernels.h"
 
@@ -34,6 +36,21 @@ constexpr int NTHR = 256;
 
 // Byte offset of 16-byte chunk `ch` of tile row `row` in a swizzled LDS tile.
 __device__ __forceinline__ int swz(int row, int ch) { return row * ROWB + ((ch ^ (row & 7)) << 4); }
+// Same for the 64-byte rows of an FP8 weight tile (64 k-values per step): rows r, r+4,
+// r+8, r+12 fall on the same banks, so the chunk position is XORed with bits 2..3 of
+// the row and 16 consecutive rows read at one chunk hit 16 distinct bank groups.
+constexpr int ROWB8 = 64;
+__device__ __forceinline__ int swz8(int row, int ch) { return row * ROWB8 + ((ch ^ ((row >> 2) & 3)) << 4); }
+
+// Eight FP8 E4M3 weights (two 32-bit words, k in byte order) as eight fp16 values of an
+// MFMA operand.  Every E4M3 value is exact in fp16, so the conversion loses nothing.
+template <bool HI>
+__device__ __forceinline__ unsigned f8x2(unsigned w) {
+  return __builtin_bit_cast(unsigned, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, HI));
+}
+__device__ __forceinline__ u32x4 f8_to_f16x8(unsigned w0, unsigned w1) {
+  return u32x4{f8x2<false>(w0), f8x2<true>(w0), f8x2<false>(w1), f8x2<true>(w1)};
+}
 
 // Applies the epilogue to up to 4 consecutive columns n..n+3 of row m (n % 4 == 0).
 // d, dh and ldc are multiples of 4 in every mode that scatters, so the 4 columns never
@@ -267,11 +284,19 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
   }
 }
 
-template <typename T, int BM_, int BN_, int STAGES, int ROLE>
-__global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int lda, const T* __restrict__ Bt,
+// F8: Bt holds FP8 E4M3 weights ([N][K] bytes) with one fp32 scale per output column
+// (epi.wscale); A stays fp16.  The weight tile then takes 64-byte rows in LDS (a 1 KB
+// wave load moves 16 of them), each lane's 16-byte B fragment carries the 16 k-values
+// of both half-steps, and lane l supplies A k-values 16*(l/16) .. +7 and +8 .. +15 (the
+// two operands agree on the k each lane carries, which is all the MFMA needs).
+template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false>
+__global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int lda, const void* __restrict__ Bt,
                                                     int M, int N, int K, GemmEpi epi, int tiles_m, int tiles_n) {
-  constexpr int STAGE_BYTES = (BM_ + BN_) * ROWB;
-  constexpr int GROUPS = (BM_ + BN_) / 8;          // 8 tile rows = one 1 KB wave load
+  static_assert(!F8 || std::is_same<T, f16>::value, "FP8 weights pair with fp16 activations");
+  constexpr int ROWB_B = F8 ? ROWB8 : ROWB;
+  constexpr int STAGE_BYTES = BM_ * ROWB + BN_ * ROWB_B;
+  constexpr int GROUPS_A = BM_ / 8;                 // 8 A rows = one 1 KB wave load
+  constexpr int GROUPS = GROUPS_A + BN_ * ROWB_B / 1024;
   constexpr int LPW = GROUPS / 4;                   // loads per wave per stage
   constexpr int WM = BM_ / 2, WN = BN_ / 2;         // 2x2 waves
   constexpr int FM = WM / 16, FN = WN / 16;         // 16x16 blocks per wave
@@ -305,25 +330,37 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   const int t_slot = epi.ctl ? epi.ctl[CTL_T] : epi.t;
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  const size_t lda_b = (size_t)lda * sizeof(T), ldb_b = (size_t)K * sizeof(T);
+  const size_t lda_b = (size_t)lda * sizeof(T), ldb_b = (size_t)K * (F8 ? 1 : sizeof(T));
 
   // Direct global -> LDS loads: one instruction moves 8 tile rows (64 lanes x 16 B, lane l
   // to LDS byte 16*l of the group).  Lane l fills LDS chunk (l & 7) of row l/8, which
   // holds global chunk (l & 7) ^ (row & 7) under the swizzle; rows past the edge re-read
   // the last valid row (their results are never stored).
+  // FP8 weight tile: a wave load moves 16 rows of 64 bytes; lane l fills LDS chunk (l & 3)
+  // of row l/4, which holds global chunk (l & 3) ^ ((row >> 2) & 3) = (l & 3) ^ (l >> 4).
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  const int brow8 = lane >> 2, bchunk8 = (lane & 3) ^ (lane >> 4);
   const char* Ab = reinterpret_cast<const char*>(A) + lchunk * 16;
-  const char* Bb = reinterpret_cast<const char*>(Bt) + lchunk * 16;
+  const char* Bb = reinterpret_cast<const char*>(Bt) + (F8 ? bchunk8 : lchunk) * 16;
 #define NT_ISSUE(kt, SL)                                                                          \
   {                                                                                               \
     unsigned char* sb_ = lds + (SL) * STAGE_BYTES;                                                \
-    const size_t kb_ = (size_t)(kt) * ROWB;                                                       \
     _Pragma("unroll") for (int i_ = 0; i_ < LPW; ++i_) {                                          \
       const int g_ = wave * LPW + i_;                                                             \
-      const int row_ = g_ * 8 + lrow;                                                             \
-      const char* src_ = row_ < BM_ ? Ab + (size_t)min(m0 + row_, M - 1) * lda_b + kb_            \
-                                    : Bb + (size_t)min(n0 + row_ - BM_, N - 1) * ldb_b + kb_;     \
-      __builtin_amdgcn_global_load_lds(src_, NT_LDS(sb_ + g_ * 1024), 16, 0, 0);                 \
+      const char* src_;                                                                           \
+      unsigned char* dst_;                                                                        \
+      if (!F8 || g_ < GROUPS_A) {                                                                 \
+        const int row_ = g_ * 8 + lrow;                                                           \
+        const size_t kb_ = (size_t)(kt) * ROWB;                                                   \
+        src_ = row_ < BM_ ? Ab + (size_t)min(m0 + row_, M - 1) * lda_b + kb_                      \
+                          : Bb + (size_t)min(n0 + row_ - BM_, N - 1) * ldb_b + kb_;               \
+        dst_ = sb_ + g_ * 1024;                                                                   \
+      } else {                                                                                    \
+        const int b_ = g_ - GROUPS_A;                                                             \
+        src_ = Bb + (size_t)min(n0 + b_ * 16 + brow8, N - 1) * ldb_b + (size_t)(kt) * ROWB8;      \
+        dst_ = sb_ + BM_ * ROWB + b_ * 1024;                                                      \
+      }                                                                                           \
+      __builtin_amdgcn_global_load_lds(src_, NT_LDS(dst_), 16, 0, 0);                             \
     }                                                                                             \
   }
 
@@ -348,15 +385,31 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     // both halves of the k-step are read back to back; the second half's reads land
     // while the first half's MFMAs run
     u32x4 af0[FM], bf0[FN], af1[FM], bf1[FN];
+    if constexpr (F8) {
+      u32x4 bq[FN];   // 16 FP8 weights: k 16*fc .. 16*fc+15
 #pragma unroll
-    for (int i = 0; i < FM; ++i) af0[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, fc));
+      for (int i = 0; i < FM; ++i) af0[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, 2 * fc));
 #pragma unroll
-    for (int j = 0; j < FN; ++j) bf0[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, fc));
+      for (int j = 0; j < FN; ++j) bq[j] = lds_read16(Bs + swz8(wn * WN + j * 16 + fr, fc));
 #pragma unroll
-    for (int i = 0; i < FM; ++i) af1[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, 4 + fc));
+      for (int i = 0; i < FM; ++i) af1[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, 2 * fc + 1));
+      LdsWait<FM, FN>::template run<FM>(af0, bq);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) bf1[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, 4 + fc));
-    LdsWait<FM, FN>::template run<FM + FN>(af0, bf0);
+      for (int j = 0; j < FN; ++j) {
+        bf0[j] = f8_to_f16x8(bq[j].x, bq[j].y);
+        bf1[j] = f8_to_f16x8(bq[j].z, bq[j].w);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af0[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, fc));
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bf0[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, fc));
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af1[i] = lds_read16(As + swz(wm * WM + i * 16 + fr, 4 + fc));
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bf1[j] = lds_read16(Bs + swz(wn * WN + j * 16 + fr, 4 + fc));
+      LdsWait<FM, FN>::template run<FM + FN>(af0, bf0);
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -381,6 +434,15 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   constexpr int PASSES = BM_ / ER;
   static_assert(ER * CS * 4 <= LDSB && ER % 16 == 0, "epilogue tile fits the LDS ring");
   float* cs = reinterpret_cast<float*>(lds);
+  // FP8 weights: each output column carries its weight scale (a lane's column is fixed
+  // per 16x16 block), applied as the accumulators enter the tile so every epilogue sees
+  // the scaled products
+  float wsc[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int n = n0 + wn * WN + j * 16 + fr;
+    wsc[j] = F8 ? (n < N ? epi.wscale[n] : 0.f) : 1.f;
+  }
 #pragma unroll
   for (int pass = 0; pass < PASSES; ++pass) {
     if (pass) __syncthreads();
@@ -392,7 +454,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
         for (int j = 0; j < FN; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            cs[(rb - pass * ER + fc * 4 + r) * CS + wn * WN + j * 16 + fr] = acc[i][j][r];
+            cs[(rb - pass * ER + fc * 4 + r) * CS + wn * WN + j * 16 + fr] = F8 ? acc[i][j][r] * wsc[j] : acc[i][j][r];
       }
     }
     __syncthreads();
@@ -409,12 +471,12 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   }
 }
 
-template <typename T, int BM_, int BN_, int STAGES, int ROLE>
+template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false>
 hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                        hipStream_t s) {
   const int tm = (M + BM_ - 1) / BM_, tn = (N + BN_ - 1) / BN_;
-  NT_LAUNCH((gemm_kernel<T, BM_, BN_, STAGES, ROLE>), dim3(tm * tn), dim3(NTHR), 0, s,
-                     static_cast<const T*>(A), lda, static_cast<const T*>(Bt), M, N, K, epi, tm, tn);
+  NT_LAUNCH((gemm_kernel<T, BM_, BN_, STAGES, ROLE, F8>), dim3(tm * tn), dim3(NTHR), 0, s,
+                     static_cast<const T*>(A), lda, Bt, M, N, K, epi, tm, tn);
   return hipGetLastError();
 }
 
@@ -435,6 +497,23 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
     const long long mn = (long long)M * N;
     if (M >= 4096) tile = N <= 2048 ? 3 : 2;
     else tile = mn < (1ll << 20) ? 1 : mn < (3ll << 20) ? 4 : 2;
+  }
+  // FP8 weights (fp16 activations only).  A 64-byte weight row moves 16 rows per wave
+  // load, so the narrow tiles change: measured at decode shapes with four GEMMs in flight,
+  // 32x64 (3 stages) is the best small tile (650x512x512: 5.1 us against 6.2 at 64x64;
+  // 1300x512x2048: 13.0 against 15.9) and 64x64 the best middle one (1300x1536x512: 8.2
+  // against 9.1 at 64x128).
+  if (epi.wscale) {
+    if constexpr (!std::is_same<T, f16>::value || ROLE == 2) {
+      return hipErrorInvalidValue;
+    } else {
+      switch (tile) {
+        case 2: return launch_tile<T, 128, 128, 2, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
+        case 3: return launch_tile<T, 128, 64, 2, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
+        case 4: return launch_tile<T, 64, 64, 3, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
+        default: return launch_tile<T, 32, 64, 3, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
+      }
+    }
   }
   switch (tile) {
     case 2: return launch_tile<T, 128, 128, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
@@ -458,6 +537,7 @@ hipError_t launch_role(const void* A, int lda, const void* Bt, int M, int N, int
 
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                 hipStream_t s, int role, int tile) {
+  if (epi.wscale && dt != DT::F16) return hipErrorInvalidValue;   // FP8 weights pair with fp16
   switch (dt) {
     case DT::F32: return launch_role<float>(A, lda, Bt, M, N, K, epi, s, role, tile);
     case DT::F16: return launch_role<f16>(A, lda, Bt, M, N, K, epi, s, role, tile);

@@ -82,6 +82,9 @@ struct GemmEpi {
   // EPI_CROSS_KV
   void* cross = nullptr;           // [Ld][2][B][H][S][dh]
   int B = 0, S = 0;
+  // FP8 weights: Bt is [N][K] FP8 E4M3 bytes and column n of the product is scaled by
+  // wscale[n] (fp32); null for weights in the model dtype.  fp16 activations only.
+  const float* wscale = nullptr;
   // EPI_TOPK (the launch uses 128x128 tiles, so n_tiles = ceil(N / 128))
   float* part = nullptr;           // [M][n_tiles][topk_record(k2)]
   int k2 = 1;

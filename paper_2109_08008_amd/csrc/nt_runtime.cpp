@@ -147,10 +147,13 @@ struct EncLayerW {
   const float *ln1, *bqkv, *bo, *ln2, *b1, *b2;
   const void *Wqkv, *Wo, *W1, *W2;
   const float *relk, *relv;   // [2k+1][d_head] relative-position tables, or null
+  // FP8 weights: the column scales of Wqkv, Wo, W1, W2 (null for weights in the model dtype)
+  const float *sqkv = nullptr, *so = nullptr, *s1 = nullptr, *s2 = nullptr;
 };
 struct DecLayerW {
   const float *ln1, *bqkv, *bo, *ln2, *bq, *boc, *ln3, *b1, *b2;
   const void *Wqkv, *Wo, *Wq, *Woc, *W1, *W2;
+  const float *sqkv = nullptr, *so = nullptr, *sq = nullptr, *soc = nullptr, *s1 = nullptr, *s2 = nullptr;
 };
 
 struct nt_model {
@@ -167,6 +170,7 @@ struct nt_model {
   std::vector<DecLayerW> dec;
   const void* Wkv_all;    // [Ld*2d][d]
   const float* bkv_all;   // [Ld*2d]
+  const float* skv_all = nullptr;   // FP8 weights: column scales of Wkv_all
   const float* dec_out_ln;
   // an ensemble (nt_ensemble): the member models, borrowed, and the combination rule;
   // empty for a loaded model, whose only member is itself
@@ -199,6 +203,8 @@ nt_status validate_cfg(const nt_model_cfg* c) {
   if (c->max_positions > 1024) return fail(NT_E_UNSUPPORTED, "max_positions > 1024");
   if (!(c->ln_eps > 0.f)) return fail(NT_E_INVALID, "ln_eps must be > 0");
   if (c->rel_pos_k < 0 || c->rel_pos_k > 16) return fail(NT_E_UNSUPPORTED, "rel_pos_k %d outside [0, 16]", c->rel_pos_k);
+  if (c->fp8_weights != 0 && c->fp8_weights != 1) return fail(NT_E_INVALID, "fp8_weights must be 0 or 1");
+  if (c->fp8_weights && c->dtype != NT_F16) return fail(NT_E_UNSUPPORTED, "fp8_weights needs dtype NT_F16");
   return NT_OK;
 }
 
@@ -206,8 +212,9 @@ nt_status validate_cfg(const nt_model_cfg* c) {
 struct ModelLayout {
   size_t total = 0;
   size_t E, pe, hist_ln, dlcl, enc_out_ln, Wkv_all, bkv_all, dec_out_ln;
-  struct Enc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2, relk, relv; };
-  struct Dec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Woc, boc, ln3, W1, b1, W2, b2; };
+  struct Enc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2, relk, relv, sqkv, so, s1, s2; };
+  struct Dec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Woc, boc, ln3, W1, b1, W2, b2, sqkv, so, sq, soc, s1, s2; };
+  size_t skv_all = 0;
   std::vector<Enc> enc;
   std::vector<Dec> dec;
   // host blob (fp32) offsets
@@ -222,6 +229,8 @@ ModelLayout layout_of(const nt_model_cfg& c) {
   ModelLayout Lo;
   const size_t d = c.d_model, F = c.d_ffn, V = c.vocab, L = c.n_enc, Ld = c.n_dec;
   const size_t eb = c.dtype == NT_F32 ? 4 : 2;
+  const bool f8 = c.fp8_weights != 0;
+  const size_t mb = f8 ? 1 : eb;   // bytes per projection weight (E keeps eb)
   const size_t dh = d / c.n_heads, rt = c.rel_pos_k > 0 ? 2 * (size_t)c.rel_pos_k + 1 : 0;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -236,15 +245,19 @@ ModelLayout layout_of(const nt_model_cfg& c) {
   for (size_t i = 0; i < L; ++i) {
     ModelLayout::Enc e;
     e.ln1 = take(2 * d * 4);
-    e.Wqkv = take(3 * d * d * eb);
+    e.Wqkv = take(3 * d * d * mb);
     e.bqkv = take(3 * d * 4);
-    e.Wo = take(d * d * eb);
+    e.Wo = take(d * d * mb);
     e.bo = take(d * 4);
     e.ln2 = take(2 * d * 4);
-    e.W1 = take(F * d * eb);
+    e.W1 = take(F * d * mb);
     e.b1 = take(F * 4);
-    e.W2 = take(d * F * eb);
+    e.W2 = take(d * F * mb);
     e.b2 = take(d * 4);
+    e.sqkv = f8 ? take(3 * d * 4) : 0;
+    e.so = f8 ? take(d * 4) : 0;
+    e.s1 = f8 ? take(F * 4) : 0;
+    e.s2 = f8 ? take(d * 4) : 0;
     e.relk = rt ? take(rt * dh * 4) : 0;
     e.relv = rt ? take(rt * dh * 4) : 0;
     Lo.enc.push_back(e);
@@ -253,24 +266,31 @@ ModelLayout layout_of(const nt_model_cfg& c) {
   for (size_t j = 0; j < Ld; ++j) {
     ModelLayout::Dec e;
     e.ln1 = take(2 * d * 4);
-    e.Wqkv = take(3 * d * d * eb);
+    e.Wqkv = take(3 * d * d * mb);
     e.bqkv = take(3 * d * 4);
-    e.Wo = take(d * d * eb);
+    e.Wo = take(d * d * mb);
     e.bo = take(d * 4);
     e.ln2 = take(2 * d * 4);
-    e.Wq = take(d * d * eb);
+    e.Wq = take(d * d * mb);
     e.bq = take(d * 4);
-    e.Woc = take(d * d * eb);
+    e.Woc = take(d * d * mb);
     e.boc = take(d * 4);
     e.ln3 = take(2 * d * 4);
-    e.W1 = take(F * d * eb);
+    e.W1 = take(F * d * mb);
     e.b1 = take(F * 4);
-    e.W2 = take(d * F * eb);
+    e.W2 = take(d * F * mb);
     e.b2 = take(d * 4);
+    e.sqkv = f8 ? take(3 * d * 4) : 0;
+    e.so = f8 ? take(d * 4) : 0;
+    e.sq = f8 ? take(d * 4) : 0;
+    e.soc = f8 ? take(d * 4) : 0;
+    e.s1 = f8 ? take(F * 4) : 0;
+    e.s2 = f8 ? take(d * 4) : 0;
     Lo.dec.push_back(e);
   }
-  Lo.Wkv_all = take(Ld * 2 * d * d * eb);
+  Lo.Wkv_all = take(Ld * 2 * d * d * mb);
   Lo.bkv_all = take(Ld * 2 * d * 4);
+  Lo.skv_all = f8 ? take(Ld * 2 * d * 4) : 0;
   Lo.dec_out_ln = take(2 * d * 4);
   Lo.total = off;
 
@@ -320,6 +340,47 @@ ModelLayout layout_of(const nt_model_cfg& c) {
   Lo.hdec_out = h; h += 2 * d;
   Lo.host_floats = h;
   return Lo;
+}
+
+// --------------------------------------------------------------------------------------
+// FP8 weights: OCP E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa bits; subnormals
+// of 2^-9; no infinities; 0x7F / 0xFF are NaN, so the largest finite value is 448).
+
+// Code of the E4M3 value nearest to x, ties to even; magnitudes beyond 448 saturate.
+uint8_t e4m3_code(float x) {
+  const uint8_t sign = std::signbit(x) ? 0x80 : 0;
+  const float a = std::fabs(x);
+  if (std::isnan(a)) return 0x7F;
+  if (a == 0.f) return sign;
+  int E;
+  (void)std::frexp(a, &E);          // a = f * 2^E, f in [0.5, 1): binade 2^(E-1)
+  int e = std::max(E - 1, -6);      // below 2^-6 the step stays 2^-9 (subnormals)
+  // a in units of the binade's step 2^(e-3) (exact scaling), rounded half to even
+  int m = (int)std::nearbyint(std::ldexp(a, 3 - e));
+  if (e == -6 && m < 8) return sign | (uint8_t)m;   // subnormal: exponent field 0
+  if (m == 16) {                    // rounded up into the next binade
+    m = 8;
+    ++e;
+  }
+  if (e > 8 || (e == 8 && m > 14)) {   // beyond 448 = 1.75 * 2^8
+    e = 8;
+    m = 14;
+  }
+  return sign | (uint8_t)(((e + 7) << 3) | (m - 8));
+}
+
+// Weight matrix W [in][out] (row-major, y = x W) as FP8 codes q [out][in] (the GEMM's
+// K-contiguous layout) with one scale per output column n: scale = max_k |W[k][n]| / 448
+// (1 for an all-zero column) and q = e4m3_code(W[k][n] / scale), both in fp32.
+void quantize_fp8(const float* W, int in, int out, std::vector<uint8_t>& q, std::vector<float>& scale) {
+  std::vector<float> amax(out, 0.f);
+  for (int k = 0; k < in; ++k)
+    for (int n = 0; n < out; ++n) amax[n] = std::max(amax[n], std::fabs(W[(size_t)k * out + n]));
+  scale.resize(out);
+  for (int n = 0; n < out; ++n) scale[n] = amax[n] > 0.f ? amax[n] / 448.0f : 1.0f;
+  q.resize((size_t)in * out);
+  for (int k = 0; k < in; ++k)
+    for (int n = 0; n < out; ++n) q[(size_t)n * in + k] = e4m3_code(W[(size_t)k * out + n] / scale[n]);
 }
 
 // --------------------------------------------------------------------------------------
@@ -500,7 +561,8 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
   const float eps = m.cfg.ln_eps;
 
   auto gemm_enc = [&](const void* A, int lda, const void* W, int N, int K, const nt::GemmEpi& e) -> hipError_t {
-    const double bytes = ((double)T * K + (double)N * K) * eb + (double)T * N * eb * (e.mode == nt::EPI_RESID ? 2 : 1);
+    const double wb = e.wscale ? 1.0 : eb;   // bytes per weight (FP8: one)
+    const double bytes = (double)T * K * eb + (double)N * K * wb + (double)T * N * eb * (e.mode == nt::EPI_RESID ? 2 : 1);
     return timed(NT_K_GEMM_ENC, s, bytes, 2.0 * T * N * K, [&] { return nt::gemm(m.dt, A, lda, W, T, N, K, e, s); });
   };
 
@@ -534,6 +596,7 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
     nt::GemmEpi e{};
     e.mode = nt::EPI_STORE;
     e.bias = w.bqkv;
+    e.wscale = w.sqkv;
     e.out = at(p.qkv);
     e.ldc = 3 * d;
     NT_HIP(gemm_enc(at(p.u), d, w.Wqkv, 3 * d, d, e));
@@ -564,6 +627,7 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
     e = nt::GemmEpi{};
     e.mode = nt::EPI_RESID;
     e.bias = w.bo;
+    e.wscale = w.so;
     e.resid = at(p.x);
     e.out = at(p.a);
     e.ldc = d;
@@ -575,6 +639,7 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
     e = nt::GemmEpi{};
     e.mode = nt::EPI_RELU;
     e.bias = w.b1;
+    e.wscale = w.s1;
     e.out = at(p.f);
     e.ldc = m.F;
     NT_HIP(gemm_enc(at(p.u), d, w.W1, m.F, d, e));
@@ -582,6 +647,7 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
     e = nt::GemmEpi{};
     e.mode = nt::EPI_RESID;
     e.bias = w.b2;
+    e.wscale = w.s2;
     e.resid = at(p.a);
     e.out = at(p.y);
     e.ldc = d;
@@ -592,6 +658,7 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
   nt::GemmEpi e{};
   e.mode = nt::EPI_CROSS_KV;
   e.bias = m.bkv_all;
+  e.wscale = m.skv_all;
   e.cross = at(mp.cross);
   e.d = d;
   e.H = m.H;
@@ -628,7 +695,8 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
 
     auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
       const double ob = e.mode == nt::EPI_TOPK ? 0.0 : e.out_f32 ? 4.0 : eb;
-      const double bytes = ((double)R * Kd + (double)N * Kd) * eb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
+      const double wb = e.wscale ? 1.0 : eb;   // bytes per weight (FP8: one)
+      const double bytes = (double)R * Kd * eb + (double)N * Kd * wb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
       const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
       const int tile = e.mode == nt::EPI_TOPK ? 2 : 0;   // the partial records assume 128-column tiles
       nt::GemmEpi ec = e;
@@ -650,6 +718,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       nt::GemmEpi e{};
       e.mode = nt::EPI_SELF_QKV;
       e.bias = w.bqkv;
+      e.wscale = w.sqkv;
       e.out = at(p.dq);
       e.ldc = d;
       e.sent_list = list;
@@ -683,6 +752,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e = nt::GemmEpi{};
       e.mode = nt::EPI_RESID;
       e.bias = w.bo;
+      e.wscale = w.so;
       e.resid = at(p.z);
       e.out = at(p.z);
       e.ldc = d;
@@ -694,6 +764,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e = nt::GemmEpi{};
       e.mode = nt::EPI_STORE;
       e.bias = w.bq;
+      e.wscale = w.sq;
       e.out = at(p.dq);
       e.ldc = d;
       NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wq, d, d, e));
@@ -724,6 +795,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e = nt::GemmEpi{};
       e.mode = nt::EPI_RESID;
       e.bias = w.boc;
+      e.wscale = w.soc;
       e.resid = at(p.z);
       e.out = at(p.z);
       e.ldc = d;
@@ -735,6 +807,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e = nt::GemmEpi{};
       e.mode = nt::EPI_RELU;
       e.bias = w.b1;
+      e.wscale = w.s1;
       e.out = at(p.df);
       e.ldc = m.F;
       NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.W1, m.F, d, e));
@@ -742,6 +815,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e = nt::GemmEpi{};
       e.mode = nt::EPI_RESID;
       e.bias = w.b2;
+      e.wscale = w.s2;
       e.resid = at(p.z);
       e.out = at(p.z);
       e.ldc = d;
@@ -1078,8 +1152,20 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
   auto vec = [&](size_t dev_off, size_t host_off, size_t n) -> hipError_t {
     return hipMemcpyAsync(base + dev_off, staging + host_off, n * 4, hipMemcpyDeviceToDevice, s);
   };
-  auto mat = [&](size_t dev_off, size_t host_off, int in, int outn) -> hipError_t {
-    return nt::pack_transpose(dt, staging + host_off, base + dev_off, in, outn, s);
+  // a projection matrix: transposed to [out][in] in the model dtype, or quantized to FP8
+  // on the host (its codes and column scales copied in; the buffers stay alive until
+  // the stream is synchronised below)
+  const bool f8 = cfg->fp8_weights != 0;
+  std::vector<std::vector<uint8_t>> keep_q;
+  std::vector<std::vector<float>> keep_s;
+  auto mat = [&](size_t dev_off, size_t host_off, int in, int outn, size_t scale_off) -> hipError_t {
+    if (!f8) return nt::pack_transpose(dt, staging + host_off, base + dev_off, in, outn, s);
+    keep_q.emplace_back();
+    keep_s.emplace_back();
+    quantize_fp8(host_weights + host_off, in, outn, keep_q.back(), keep_s.back());
+    hipError_t e = hipMemcpyAsync(base + dev_off, keep_q.back().data(), keep_q.back().size(), hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
+    return hipMemcpyAsync(base + scale_off, keep_s.back().data(), keep_s.back().size() * 4, hipMemcpyHostToDevice, s);
   };
   NT_HIP(nt::pack_convert(dt, staging + Lo.hE, base + Lo.E, (size_t)V * d, s));
   NT_HIP(vec(Lo.hist_ln, Lo.hhist, (size_t)(L + 1) * 2 * d));
@@ -1088,14 +1174,14 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     const auto& D = Lo.enc[i];
     const auto& Hh = Lo.henc[i];
     NT_HIP(vec(D.ln1, Hh.ln1, 2 * d));
-    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d));
+    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d, D.sqkv));
     NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
-    NT_HIP(mat(D.Wo, Hh.Wo, d, d));
+    NT_HIP(mat(D.Wo, Hh.Wo, d, d, D.so));
     NT_HIP(vec(D.bo, Hh.bo, d));
     NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
-    NT_HIP(mat(D.W1, Hh.W1, d, F));
+    NT_HIP(mat(D.W1, Hh.W1, d, F, D.s1));
     NT_HIP(vec(D.b1, Hh.b1, F));
-    NT_HIP(mat(D.W2, Hh.W2, F, d));
+    NT_HIP(mat(D.W2, Hh.W2, F, d, D.s2));
     NT_HIP(vec(D.b2, Hh.b2, d));
     if (cfg->rel_pos_k > 0) {
       const size_t rn = (2 * (size_t)cfg->rel_pos_k + 1) * (d / cfg->n_heads);
@@ -1109,22 +1195,23 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     const auto& D = Lo.dec[j];
     const auto& Hh = Lo.hdec[j];
     NT_HIP(vec(D.ln1, Hh.ln1, 2 * d));
-    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d));
+    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d, D.sqkv));
     NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
-    NT_HIP(mat(D.Wo, Hh.Wo, d, d));
+    NT_HIP(mat(D.Wo, Hh.Wo, d, d, D.so));
     NT_HIP(vec(D.bo, Hh.bo, d));
     NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
-    NT_HIP(mat(D.Wq, Hh.Wq, d, d));
+    NT_HIP(mat(D.Wq, Hh.Wq, d, d, D.sq));
     NT_HIP(vec(D.bq, Hh.bq, d));
-    NT_HIP(mat(D.Woc, Hh.Woc, d, d));
+    NT_HIP(mat(D.Woc, Hh.Woc, d, d, D.soc));
     NT_HIP(vec(D.boc, Hh.boc, d));
     NT_HIP(vec(D.ln3, Hh.ln3, 2 * d));
-    NT_HIP(mat(D.W1, Hh.W1, d, F));
+    NT_HIP(mat(D.W1, Hh.W1, d, F, D.s1));
     NT_HIP(vec(D.b1, Hh.b1, F));
-    NT_HIP(mat(D.W2, Hh.W2, F, d));
+    NT_HIP(mat(D.W2, Hh.W2, F, d, D.s2));
     NT_HIP(vec(D.b2, Hh.b2, d));
     // cross K/V projections of all layers stacked into one [Ld*2d][d] matrix
-    NT_HIP(nt::pack_transpose(dt, staging + Hh.Wkv, base + Lo.Wkv_all + (size_t)j * 2 * d * d * eb, d, 2 * d, s));
+    const size_t mb = f8 ? 1 : eb;
+    NT_HIP(mat(Lo.Wkv_all + (size_t)j * 2 * d * d * mb, Hh.Wkv, d, 2 * d, Lo.skv_all + (size_t)j * 2 * d * 4));
     NT_HIP(vec(Lo.bkv_all + (size_t)j * 2 * d * 4, Hh.bkv, 2 * d));
   }
   NT_HIP(vec(Lo.dec_out_ln, Lo.hdec_out, 2 * d));
@@ -1161,15 +1248,32 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     m->enc.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.b1), fp(D.b2), base + D.Wqkv, base + D.Wo,
                       base + D.W1, base + D.W2, cfg->rel_pos_k > 0 ? fp(D.relk) : nullptr,
                       cfg->rel_pos_k > 0 ? fp(D.relv) : nullptr});
+    if (f8) {
+      EncLayerW& w = m->enc.back();
+      w.sqkv = fp(D.sqkv);
+      w.so = fp(D.so);
+      w.s1 = fp(D.s1);
+      w.s2 = fp(D.s2);
+    }
   }
   m->enc_out_ln = fp(Lo.enc_out_ln);
   for (int j = 0; j < Ld; ++j) {
     const auto& D = Lo.dec[j];
     m->dec.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.bq), fp(D.boc), fp(D.ln3), fp(D.b1), fp(D.b2),
                       base + D.Wqkv, base + D.Wo, base + D.Wq, base + D.Woc, base + D.W1, base + D.W2});
+    if (f8) {
+      DecLayerW& w = m->dec.back();
+      w.sqkv = fp(D.sqkv);
+      w.so = fp(D.so);
+      w.sq = fp(D.sq);
+      w.soc = fp(D.soc);
+      w.s1 = fp(D.s1);
+      w.s2 = fp(D.s2);
+    }
   }
   m->Wkv_all = base + Lo.Wkv_all;
   m->bkv_all = fp(Lo.bkv_all);
+  m->skv_all = f8 ? fp(Lo.skv_all) : nullptr;
   m->dec_out_ln = fp(Lo.dec_out_ln);
   *out = m;
   return NT_OK;
@@ -1523,7 +1627,7 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
 
 nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N, int32_t K,
                      const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
-                     int32_t relu, int32_t tile, void* stream) {
+                     int32_t relu, int32_t tile, const float* d_bscale, void* stream) {
   g_err.clear();
   if (!d_A || !d_Bt || !d_out) return fail(NT_E_INVALID, "null argument to nt_op_gemm");
   if (dtype < NT_F32 || dtype > NT_BF16) return fail(NT_E_INVALID, "unknown dtype %d", dtype);
@@ -1534,7 +1638,9 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
   if (tile < 0 || tile > 4) return fail(NT_E_INVALID, "tile must be 0..4");
   if (relu && (d_resid || out_f32)) return fail(NT_E_UNSUPPORTED, "relu combines with neither resid nor fp32 out");
   if (d_resid && out_f32) return fail(NT_E_UNSUPPORTED, "resid needs a model-dtype output");
+  if (d_bscale && dtype != NT_F16) return fail(NT_E_UNSUPPORTED, "FP8 weights (d_bscale) need dtype NT_F16");
   nt::GemmEpi e{};
+  e.wscale = d_bscale;
   e.mode = relu ? nt::EPI_RELU : d_resid ? nt::EPI_RESID : nt::EPI_STORE;
   e.bias = d_bias;
   e.resid = d_resid;
@@ -1542,6 +1648,18 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
   e.ldc = ldc;
   e.out_f32 = out_f32 ? 1 : 0;
   NT_HIP(nt::gemm(static_cast<DT>(dtype), d_A, lda, d_Bt, M, N, K, e, static_cast<hipStream_t>(stream), 0, tile));
+  return NT_OK;
+}
+
+nt_status nt_quantize_fp8(const float* h_W, int32_t in, int32_t out, uint8_t* h_q, float* h_scale) {
+  g_err.clear();
+  if (!h_W || !h_q || !h_scale) return fail(NT_E_INVALID, "null argument to nt_quantize_fp8");
+  if (in <= 0 || out <= 0) return fail(NT_E_INVALID, "matrix sizes must be positive");
+  std::vector<uint8_t> q;
+  std::vector<float> sc;
+  quantize_fp8(h_W, in, out, q, sc);
+  std::memcpy(h_q, q.data(), q.size());
+  std::memcpy(h_scale, sc.data(), sc.size() * 4);
   return NT_OK;
 }
 

@@ -30,7 +30,7 @@ EXPORTS = [
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
     "nt_op_gemm", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units", "nt_op_select",
-    "nt_ensemble",
+    "nt_ensemble", "nt_quantize_fp8",
 ]
 NT_ENS_MEAN_LOGP, NT_ENS_LOG_MEAN_P = 0, 1
 
@@ -39,7 +39,7 @@ class nt_model_cfg(ctypes.Structure):
     _fields_ = [("d_model", c_int32), ("n_heads", c_int32), ("d_ffn", c_int32), ("n_enc", c_int32),
                 ("n_dec", c_int32), ("vocab", c_int32), ("max_positions", c_int32), ("pad_id", c_int32),
                 ("bos_id", c_int32), ("eos_id", c_int32), ("dtype", c_int32), ("dlcl_hist_norm", c_int32),
-                ("ln_eps", c_float), ("rel_pos_k", c_int32)]
+                ("ln_eps", c_float), ("rel_pos_k", c_int32), ("fp8_weights", c_int32)]
 
 
 class nt_search_cfg(ctypes.Structure):
@@ -76,6 +76,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_load_weights": (c_int32, [POINTER(nt_model_cfg), POINTER(c_float), c_size_t, P, c_size_t, P, POINTER(P)]),
         "nt_free_model": (None, [P]),
         "nt_ensemble": (c_int32, [POINTER(P), c_int32, c_int32, POINTER(P)]),
+        "nt_quantize_fp8": (c_int32, [POINTER(c_float), c_int32, c_int32, POINTER(ctypes.c_uint8), POINTER(c_float)]),
         "nt_workspace_size": (c_int32, [P, POINTER(nt_search_cfg), c_int32, c_int32, POINTER(c_size_t)]),
         "nt_translate_workspace_size": (c_int32, [P, POINTER(nt_search_cfg), POINTER(c_int64), c_int32,
                                                   POINTER(c_size_t)]),
@@ -99,7 +100,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_prof_reset": (c_int32, []),
         "nt_prof_get": (c_int32, [c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
         "nt_op_gemm": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, P, P, c_int32, c_int32, c_int32,
-                                 c_int32, P]),
+                                 c_int32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -128,10 +129,11 @@ def _stream(stream):
 def model_cfg(shape, dtype: str = "f16", hist_norm: bool = True, ln_eps: float = 1e-5,
               pad_id: int = 0, bos_id: int = 1, eos_id: int = 2) -> nt_model_cfg:
     """nt_model_cfg from any object with d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_positions
-    (and optionally rel_k)."""
+    (and optionally rel_k).  dtype "f8" is fp16 activations with FP8 projection weights."""
+    f8 = dtype == "f8"
     return nt_model_cfg(shape.d_model, shape.n_heads, shape.d_ffn, shape.n_enc, shape.n_dec, shape.vocab,
-                        getattr(shape, "max_positions", 1024), pad_id, bos_id, eos_id, DTYPES[dtype],
-                        1 if hist_norm else 0, ln_eps, int(getattr(shape, "rel_k", 0)))
+                        getattr(shape, "max_positions", 1024), pad_id, bos_id, eos_id, DTYPES["f16" if f8 else dtype],
+                        1 if hist_norm else 0, ln_eps, int(getattr(shape, "rel_k", 0)), int(f8))
 
 
 def search_cfg(s) -> nt_search_cfg:
@@ -244,10 +246,22 @@ def nt_translate(m, search: nt_search_cfg, h_src: np.ndarray, h_src_off: np.ndar
 
 
 def nt_op_gemm(dtype: str, d_A: int, lda: int, d_Bt: int, M: int, N: int, K: int, d_bias, d_resid, d_out: int,
-               ldc: int, out_f32: bool = False, relu: bool = False, tile: int = 0, stream=None):
+               ldc: int, out_f32: bool = False, relu: bool = False, tile: int = 0, d_bscale=None, stream=None):
     _check(load_library().nt_op_gemm(DTYPES[dtype], c_void_p(d_A), lda, c_void_p(d_Bt), M, N, K,
                                      c_void_p(d_bias) if d_bias else None, c_void_p(d_resid) if d_resid else None,
-                                     c_void_p(d_out), ldc, int(out_f32), int(relu), tile, _stream(stream)))
+                                     c_void_p(d_out), ldc, int(out_f32), int(relu), tile,
+                                     c_void_p(d_bscale) if d_bscale else None, _stream(stream)))
+
+
+def nt_quantize_fp8(w: np.ndarray):
+    """The library's FP8 weight quantization of an [in, out] fp32 matrix: (codes [out, in]
+    uint8, scales [out] fp32)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    q = np.zeros((w.shape[1], w.shape[0]), dtype=np.uint8)
+    sc = np.zeros(w.shape[1], dtype=np.float32)
+    _check(load_library().nt_quantize_fp8(_ptr(w, c_float), w.shape[0], w.shape[1], _ptr(q, ctypes.c_uint8),
+                                          _ptr(sc, c_float)))
+    return q, sc
 
 
 def nt_op_select(d_logits: int, rows: int, V: int, k: int, d_topv: int, d_topi: int, d_lse: int, stream=None):

@@ -80,7 +80,7 @@ class Workload:
     model: ModelShape
     data: DataSetup
     search: SearchSetup
-    dtype: str                # "f32" | "f16" | "bf16"
+    dtype: str                # "f32" | "f16" | "bf16" | "f8" (fp16 activations, FP8 E4M3 weights)
     description: str = ""
     weights_seed: int = 0
     data_seed: int = 1
@@ -152,6 +152,22 @@ WORKLOADS = {
         "relative positions k = 8, d=512), 2998 sentences (the size of newstest2018; lognormal mean 25, "
         "max 100, Zipf(1.1) IDs), beam 4, mean of the members' log-probs, fp16",
         members=_TEACHERS,
+    ),
+    "base-6-6-fp8": Workload(
+        "base-6-6-fp8",
+        ModelShape(512, 8, 2048, 6, 6, 32000),
+        DataSetup(2048, "lognormal", 25.0, 100, "zipf"),
+        SearchSetup(beam=4, len_penalty=0.0, max_len_a=1.5, max_len_b=10, token_budget=8192),
+        "f8",
+        "Base 6-6 with FP8 E4M3 projection weights (column scales) and fp16 activations; otherwise base-6-6",
+    ),
+    "wide-30-6-fp8": Workload(
+        "wide-30-6-fp8",
+        ModelShape(1024, 16, 4096, 30, 6, 32000),
+        DataSetup(4096, "lognormal", 30.0, 200, "zipf"),
+        SearchSetup(beam=4, len_penalty=0.0, max_len_a=1.5, max_len_b=10, token_budget=16384),
+        "f8",
+        "Wide 30-6 with FP8 E4M3 projection weights (column scales) and fp16 activations; otherwise wide-30-6",
     ),
     "wide-30-6": Workload(
         "wide-30-6",

@@ -24,7 +24,7 @@ def nt():
 def header_functions():
     src = open(os.path.join(ROOT, "include", "nt.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(nt_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(nt_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_every_declared_function_is_exported(nt):
@@ -38,7 +38,7 @@ def test_every_declared_function_is_exported(nt):
 
 def test_struct_layouts_match_header(nt):
     import ctypes
-    assert ctypes.sizeof(nt.nt_model_cfg) == 14 * 4
+    assert ctypes.sizeof(nt.nt_model_cfg) == 15 * 4
     assert ctypes.sizeof(nt.nt_search_cfg) == 8 * 4
 
 
@@ -95,3 +95,48 @@ def test_ensemble_arguments_are_checked_on_the_host(nt):
     assert lib.nt_ensemble(arr, 2, 1, ctypes.byref(out)) == nt.NT_E_INVALID
     assert "null" in lib.nt_last_error().decode()
     assert out.value is None
+
+
+def test_library_fp8_quantizer_matches_the_oracle(nt):
+    """The host quantization nt_load_weights applies (fp8_weights) gives the oracle's
+    codes and scales bit for bit: random columns, a zero column, an outlier column, a
+    column of hand-placed ties and subnormals (scale exactly 1), a tiny-valued column."""
+    import oracle
+    import torch
+    rng = np.random.default_rng(2)
+    w = rng.normal(0, 0.02, size=(96, 40)).astype(np.float32)
+    w[:, 3] = 0.0
+    w[5, 7] = 3.0
+    w[:, 9] *= np.float32(1e-30)
+    ties = np.array([448.0, 1.0625, 1.1875, 232.0, 1.5 * 2.0 ** -9, 0.5 * 2.0 ** -9, -3.3, -1.0625, 2.5 * 2.0 ** -9],
+                    dtype=np.float32)
+    w[:, 11] = 0.0
+    w[:len(ties), 11] = ties
+    q, sc = nt.nt_quantize_fp8(w)
+    oq, osc = oracle.quantize_fp8_columns(w)
+    np.testing.assert_array_equal(sc.view(np.uint32), osc.view(np.uint32))
+    decoded = torch.from_numpy(q).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(decoded, oq.T)
+    assert sc[11] == 1.0
+    np.testing.assert_array_equal(decoded[11, :len(ties)], [448, 1.0, 1.25, 224, 2.0 ** -8, 0, -3.25, -1.0, 2.0 ** -8])
+
+
+def test_fp8_weight_configs(nt):
+    shape = synth.ModelShape(128, 4, 256, 1, 1, 50)
+    for dt in ("f32", "bf16"):
+        cfg = nt.model_cfg(shape, dt)
+        cfg.fp8_weights = 1
+        with pytest.raises(nt.NTError) as e:
+            nt.nt_weights_size(cfg)
+        assert e.value.status == nt.NT_E_UNSUPPORTED
+    cfg = nt.model_cfg(shape, "f16")
+    cfg.fp8_weights = 2
+    with pytest.raises(nt.NTError) as e:
+        nt.nt_weights_size(cfg)
+    assert e.value.status == nt.NT_E_INVALID
+    hf8, db8 = nt.nt_weights_size(nt.model_cfg(shape, "f8"))
+    hf16, db16 = nt.nt_weights_size(nt.model_cfg(shape, "f16"))
+    mats = sum(e.size for e in synth.weight_layout(shape) if ".W_" in e.name)
+    assert hf8 == hf16 and db16 - db8 >= mats - 4 * 2 * 1024 * 16
+    lib = nt.load_library()
+    assert lib.nt_quantize_fp8(None, 4, 4, None, None) == nt.NT_E_INVALID

@@ -22,7 +22,8 @@ from tests import gpu_util as G
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["base-6-6", "deep-shallow-greedy", "deep-shallow-beam", "wide-30-6", "base-6-6-rpr", "teacher-ensemble"]
+FULL = ["base-6-6", "deep-shallow-greedy", "deep-shallow-beam", "wide-30-6", "base-6-6-rpr", "teacher-ensemble",
+        "base-6-6-fp8", "wide-30-6-fp8"]
 N_SAMPLE = {"teacher-ensemble": 3, "wide-30-6": 4}
 
 
