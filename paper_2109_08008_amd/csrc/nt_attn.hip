@@ -18,8 +18,6 @@
 namespace nt {
 namespace {
 
-constexpr int KC = 64;       // keys per chunk of the one-wave-per-row self-attention
-
 // Grouped attention on the matrix cores: one wave per (group, head, block of 16 queries).
 // Scores are formed transposed, S^T = K.Q^T, so lane l holds the scores of query l%16
 // for keys 4*(l/16)+r of each 16-key block; those are exactly the key slots the lane
@@ -269,128 +267,96 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
   }
 }
 
-// One wave attends KQ queries (held in LDS, pre-scaled) over n keys, streaming the
-// keys in chunks of 64 with an online fp32 softmax.  Lane s loads the key and value
-// rows of key c0+s itself (16-byte loads, all in flight together); the value rows go
-// to LDS so that the P.V product (lane = channel) reads them without waiting on HBM
-// once per key.  row_of(s) maps a key index to the start of its key/value row.
-template <typename T, int DH, int KQ, typename RowFn>
-__device__ __forceinline__ void wave_attend(const float (&Qs)[KQ][DH], float (&Ps)[KQ][KC], T (&Vs)[KC][DH + 8],
-                                            int n, const T* __restrict__ Kbase, const T* __restrict__ Vbase,
-                                            RowFn row_of, float (&o)[KQ][DH > 64 ? DH / 64 : 1], float (&l)[KQ]) {
-  constexpr int CPL = DH > 64 ? DH / 64 : 1;
-  const int lane = threadIdx.x % kWave;
-  float m[KQ];
-#pragma unroll
-  for (int i = 0; i < KQ; ++i) {
-    m[i] = -INFINITY;
-    l[i] = 0.f;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) o[i][c] = 0.f;
-  }
-  for (int c0 = 0; c0 < n; c0 += KC) {
-    const int s = c0 + lane;
-    const bool valid = s < n;
-    float sc[KQ];
-#pragma unroll
-    for (int i = 0; i < KQ; ++i) sc[i] = 0.f;
-    if (valid) {
-      const size_t r = row_of(s);
-      const T* kr = Kbase + r;
-      const T* vr = Vbase + r;
-      uint4 kv[DH * sizeof(T) / 16], vv[DH * sizeof(T) / 16];
-#pragma unroll
-      for (int j = 0; j < DH * (int)sizeof(T) / 16; ++j) {
-        kv[j] = reinterpret_cast<const uint4*>(kr)[j];
-        vv[j] = reinterpret_cast<const uint4*>(vr)[j];
-      }
-#pragma unroll
-      for (int j = 0; j < DH * (int)sizeof(T) / 16; ++j) *reinterpret_cast<uint4*>(&Vs[lane][j * Vec<T>::N]) = vv[j];
-#pragma unroll
-      for (int j = 0; j < DH * (int)sizeof(T) / 16; ++j) {
-        const T* ke = reinterpret_cast<const T*>(&kv[j]);
-#pragma unroll
-        for (int x = 0; x < Vec<T>::N; ++x) {
-          const float k = to_f32(ke[x]);
-#pragma unroll
-          for (int i = 0; i < KQ; ++i) sc[i] += Qs[i][j * Vec<T>::N + x] * k;
-        }
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < KQ; ++i) {
-      const float v = valid ? sc[i] : -INFINITY;
-      const float mn = fmaxf(m[i], wave_max(v));
-      const float p = valid ? __expf(v - mn) : 0.f;
-      const float alpha = __expf(m[i] - mn);
-      l[i] = l[i] * alpha + wave_sum(p);
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) o[i][c] *= alpha;
-      m[i] = mn;
-      Ps[i][lane] = p;
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    const int kmax = min(KC, n - c0);
-    for (int k = 0; k < kmax; ++k) {
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        const int e = lane * CPL + c;
-        const float v = e < DH ? to_f32(Vs[k][e]) : 0.f;
-#pragma unroll
-        for (int i = 0; i < KQ; ++i) o[i][c] += Ps[i][k] * v;
-      }
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  }
-}
-
-// Waves per workgroup for the one-wave-per-task attention kernels: as many as fit in
-// 64 KB of LDS (so two workgroups share a CU), at most 4.
-template <typename T, int DH, int KQ>
-constexpr int attn_waves() {
-  constexpr int per_wave = KQ * DH * 4 + KQ * KC * 4 + KC * (DH + 8) * (int)sizeof(T);
-  return per_wave * 4 <= 65536 ? 4 : per_wave * 2 <= 65536 ? 2 : 1;
-}
-
 // Decoder self-attention: one wave per (live row, head) over the row's cached slots
 // 0..t.  Slot s of a beam hypothesis lives in the physical row of its ancestor at step s
 // (anc), so reordering beams never copies the cache.
+//
+// With one query this is a stream over the cache, kept on the vector units and laid out
+// for coalescing: the CPR = 16-byte chunks of a key's row sit on CPR consecutive lanes,
+// so one load instruction of the wave reads whole rows (8 keys of 128 bytes at d_head
+// 64).  Each lane carries KPL = 8 keys of a chunk of GPW * KPL keys (lane group g holds
+// keys g*KPL .. g*KPL+7).  A key's score is its lanes' partial dot products summed by a
+// butterfly inside the group; P.V accumulates per lane over its keys for its 16-byte
+// slice of channels and is summed over the lane groups once, after the last chunk.  The
+// softmax is online across chunks, in fp32.  No LDS, so occupancy is set by registers.
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
-  constexpr int CPL = DH > 64 ? DH / 64 : 1;
-  constexpr int NWV = attn_waves<T, DH, 1>();
-  __shared__ float Qs[NWV][1][DH];
-  __shared__ float Ps[NWV][1][KC];
-  __shared__ __attribute__((aligned(16))) T Vs[NWV][KC][DH + 8];
+  constexpr int VEC = Vec<T>::N, CPR = DH / VEC, GPW = kWave / CPR, KPL = 8, KCH = GPW * KPL;
+  static_assert(CPR >= 1 && CPR <= kWave && (CPR & (CPR - 1)) == 0, "a key's chunks fit in a wave");
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int pair = blockIdx.x * NWV + wave;
+  const int pair = blockIdx.x * 4 + wave;
   const int rows = min(a.rows, a.ctl[CTL_NLIVE] * a.beam);
   if (pair >= rows * a.H) return;              // whole wave exits; no block barrier below
   const int row = pair / a.H, h = pair % a.H;
   const int p = a.sent_list[row / a.beam] * a.beam + row % a.beam;
-  const T* q = static_cast<const T*>(a.q) + (size_t)row * a.H * DH + h * DH;
-  for (int e = lane; e < DH; e += kWave) Qs[wave][0][e] = to_f32(q[e]) * a.scale;
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  const size_t head = (size_t)h * a.Tcap * DH;
-  const size_t row_stride = (size_t)a.H * a.Tcap * DH;
-  const int* anc = a.anc ? a.anc + (size_t)a.ctl[CTL_ANC] * a.anc_stride + (size_t)p * a.Tcap : nullptr;
-  const int t = a.ctl[CTL_T];
-  auto row_of = [&](int s) {
-    const int ph = (anc && s < t) ? anc[s] : p;
-    return (size_t)ph * row_stride + (size_t)s * DH;
-  };
-  float o[1][CPL], l[1];
-  wave_attend<T, DH, 1>(Qs[wave], Ps[wave], Vs[wave], t + 1, static_cast<const T*>(a.kcache) + head,
-                        static_cast<const T*>(a.vcache) + head, row_of, o, l);
-  T* out = static_cast<T*>(a.out) + (size_t)row * a.H * DH + h * DH;
-  const float inv = 1.0f / l[0];
+  const int c = lane % CPR, g = lane / CPR;    // channel chunk and key group of this lane
+  float q[VEC];
+  load16(static_cast<const T*>(a.q) + (size_t)row * a.H * DH + h * DH + c * VEC, q);
 #pragma unroll
-  for (int c = 0; c < CPL; ++c) {
-    const int e = lane * CPL + c;
-    if (e < DH) out[e] = from_f32<T>(o[0][c] * inv);
+  for (int x = 0; x < VEC; ++x) q[x] *= a.scale;
+  const int t = a.ctl[CTL_T], n = t + 1;
+  const int* anc = a.anc ? a.anc + (size_t)a.ctl[CTL_ANC] * a.anc_stride + (size_t)p * a.Tcap : nullptr;
+  const size_t head = (size_t)h * a.Tcap * DH + c * VEC;
+  const T* K = static_cast<const T*>(a.kcache) + head;
+  const T* Vc = static_cast<const T*>(a.vcache) + head;
+  const size_t row_stride = (size_t)a.H * a.Tcap * DH;
+  float m = -INFINITY, lsum = 0.f, o[VEC];
+#pragma unroll
+  for (int x = 0; x < VEC; ++x) o[x] = 0.f;
+  for (int c0 = 0; c0 < n; c0 += KCH) {
+    // every ancestor row first, then all key/value loads with no branch between them, so
+    // the wave has one dependent round trip per chunk; slots past the end re-read the
+    // last one (their scores are masked)
+    int ph[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const int s = min(c0 + g * KPL + j, t);
+      ph[j] = (anc && s < t) ? anc[s] : p;        // slot t was just written by this row
+    }
+    uint4 kr[KPL], vr[KPL];
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const size_t off = (size_t)ph[j] * row_stride + (size_t)min(c0 + g * KPL + j, t) * DH;
+      kr[j] = *reinterpret_cast<const uint4*>(K + off);
+      vr[j] = *reinterpret_cast<const uint4*>(Vc + off);
+    }
+    float sc[KPL], cmax = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const T* ke = reinterpret_cast<const T*>(&kr[j]);
+      float dot = 0.f;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) dot += q[x] * to_f32(ke[x]);
+#pragma unroll
+      for (int ofs = 1; ofs < CPR; ofs <<= 1) dot += __shfl_xor(dot, ofs, kWave);
+      sc[j] = c0 + g * KPL + j < n ? dot : -INFINITY;
+      cmax = fmaxf(cmax, sc[j]);
+    }
+    const float mn = fmaxf(m, wave_max(cmax));   // finite: slot 0 is in the first chunk
+    const float alpha = __expf(m - mn);
+    float ps = 0.f;
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) o[x] *= alpha;
+#pragma unroll
+    for (int j = 0; j < KPL; ++j) {
+      const float pj = __expf(sc[j] - mn);
+      const T* ve = reinterpret_cast<const T*>(&vr[j]);
+      ps += pj;
+#pragma unroll
+      for (int x = 0; x < VEC; ++x) o[x] += pj * to_f32(ve[x]);
+    }
+    lsum = lsum * alpha + (c == 0 ? ps : 0.f);   // one lane per key group counts its keys
+    m = mn;
+  }
+#pragma unroll
+  for (int ofs = CPR; ofs < kWave; ofs <<= 1)
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) o[x] += __shfl_xor(o[x], ofs, kWave);
+  const float inv = 1.0f / wave_sum(lsum);
+  if (g == 0) {
+#pragma unroll
+    for (int x = 0; x < VEC; ++x) o[x] *= inv;
+    store16(static_cast<T*>(a.out) + (size_t)row * a.H * DH + h * DH + c * VEC, o);
   }
 }
 
@@ -418,9 +384,8 @@ hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
 
 template <typename T, int DH>
 void self_launch(const SelfAttnArgs& a, hipStream_t s) {
-  constexpr int NWV = attn_waves<T, DH, 1>();
-  const dim3 grid((a.rows * a.H + NWV - 1) / NWV);
-  NT_LAUNCH((self_attn_kernel<T, DH>), grid, dim3(NWV * kWave), 0, s, a);
+  const dim3 grid((a.rows * a.H + 3) / 4);
+  NT_LAUNCH((self_attn_kernel<T, DH>), grid, dim3(4 * kWave), 0, s, a);
 }
 
 template <typename T>
