@@ -47,7 +47,9 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
   constexpr int NSB = 8;                 // score blocks per softmax chunk (128 keys)
   constexpr int ROWP = DH * EB / 16;     // 16-byte pieces per key row
   constexpr int VSTR = DH * EB / 4 + (EB == 2 ? 2 : 4);   // LDS row stride (dwords), spreads banks
+  constexpr int VPL = KSTEP * ROWP / kWave;   // 16-byte value pieces per lane per P.V step
   static_assert(DH % KSTEP == 0 && NSB % SB == 0, "head dim must fill whole MFMA steps");
+  static_assert(KSTEP * ROWP % kWave == 0, "value rows of a P.V step split evenly over the lanes");
   __shared__ __attribute__((aligned(16))) unsigned Vs[4][KSTEP][VSTR];
   constexpr int RW = RPR ? 4 : 1;   // per-wave RPR buffers (1 placeholder when unused)
   constexpr int RQ = RPR ? 16 : 1;
@@ -118,8 +120,20 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
   for (int c = 0; c < CB; ++c) o[c] = floatx4{0.f, 0.f, 0.f, 0.f};
   const unsigned short* vh = reinterpret_cast<const unsigned short*>(&Vs[wave][0][0]);
 
+  // value rows key0 .. key0 + KSTEP - 1 of this head (rows past len clamped) into registers
+  auto load_v = [&](int key0, u32x4 (&dst)[VPL]) {
+#pragma unroll
+    for (int u = 0; u < VPL; ++u) {
+      const int pc = lane + u * kWave, row = pc / ROWP, col = pc % ROWP;
+      dst[u] = *reinterpret_cast<const u32x4*>(Vb + (size_t)min(key0 + row, len - 1) * ks_b + col * 16);
+    }
+  };
+
   for (int c0 = 0; c0 < len; c0 += NSB * 16) {
     const int nb = min(NSB, (len - c0 + 15) / 16);
+    // the chunk's first P.V values are fetched now, so their latency overlaps the scores
+    u32x4 vcur[VPL];
+    load_v(c0, vcur);
     floatx4 sc[NSB];
     float cmax = -INFINITY;
 #pragma unroll
@@ -193,14 +207,17 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
     }
 
     for (int kb = 0; kb < nb; kb += SB) {
-      // value rows c0 + kb*16 .. + KSTEP -> LDS (8-byte writes; rows past len clamped)
+      // the next step's values are fetched while this step's go through LDS (8-byte
+      // writes) into the P.V product
+      const bool more = kb + SB < nb;
+      u32x4 vnext[VPL];
+      if (more) load_v(c0 + (kb + SB) * 16, vnext);
 #pragma unroll
-      for (int pc = lane; pc < KSTEP * ROWP; pc += kWave) {
-        const int row = pc / ROWP, col = pc % ROWP;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(Vb + (size_t)min(c0 + kb * 16 + row, len - 1) * ks_b + col * 16);
+      for (int u = 0; u < VPL; ++u) {
+        const int pc = lane + u * kWave, row = pc / ROWP, col = pc % ROWP;
         unsigned* dst = &Vs[wave][row][col * 4];
-        *reinterpret_cast<uint2*>(dst) = make_uint2(v.x, v.y);
-        *reinterpret_cast<uint2*>(dst + 2) = make_uint2(v.z, v.w);
+        *reinterpret_cast<uint2*>(dst) = make_uint2(vcur[u].x, vcur[u].y);
+        *reinterpret_cast<uint2*>(dst + 2) = make_uint2(vcur[u].z, vcur[u].w);
       }
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -235,6 +252,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
       }
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < VPL; ++u) vcur[u] = vnext[u];
+      }
     }
   }
 
