@@ -372,6 +372,39 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     for (int j = 0; j < FN; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const int wm = wave >> 1, wn = wave & 1;
+
+  // epilogue geometry (see the epilogue below)
+  constexpr int CS = BN_ + 4;
+  constexpr int LDSB = STAGES * STAGE_BYTES;
+  constexpr int ER = (BM_ * CS * 4 <= LDSB) ? BM_ : (WM * CS * 4 <= LDSB) ? WM : WM / 2;
+  constexpr int PASSES = BM_ / ER;
+  constexpr int EPG = ER * (BN_ / 4);           // 4-column output groups per pass
+  // The epilogue operands that do not depend on the product -- bias and residual -- are
+  // fetched before the k-loop when each thread owns at most 4 output groups (the small
+  // decode-step tiles), so their latency hides behind it.  They are added in the order
+  // the epilogue adds them (bias, then residual), so results are bitwise unchanged.
+  constexpr bool PRE = ROLE != 2 && EPG % NTHR == 0 && PASSES * (EPG / NTHR) <= 4;
+  constexpr int NPRE = PRE ? PASSES * (EPG / NTHR) : 1;
+  float4 pre_b[NPRE], pre_r[NPRE];
+  if constexpr (PRE) {
+#pragma unroll
+    for (int q = 0; q < NPRE; ++q) {
+      const int pass = q / (EPG / NTHR), g = tid + (q % (EPG / NTHR)) * NTHR;
+      const int m = m0 + pass * ER + g / (BN_ / 4), n = n0 + (g % (BN_ / 4)) * 4;
+      float b[4] = {0.f, 0.f, 0.f, 0.f}, rr[4] = {0.f, 0.f, 0.f, 0.f};
+      if (m < M && n < N) {
+        const int cnt = min(4, N - n);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (k < cnt && epi.bias) b[k] = epi.bias[n + k];
+          if (k < cnt && epi.mode == EPI_RESID) rr[k] = to_f32(static_cast<const T*>(epi.resid)[(size_t)m * epi.ldc + n + k]);
+        }
+      }
+      pre_b[q] = make_float4(b[0], b[1], b[2], b[3]);
+      pre_r[q] = make_float4(rr[0], rr[1], rr[2], rr[3]);
+    }
+  }
+
   const int nk = (int)((size_t)K * sizeof(T) / ROWB);
   for (int st = 0; st < STAGES - 1 && st < nk; ++st) NT_ISSUE(st, st)
   int slot = 0;   // slot of k-step kt
@@ -428,10 +461,6 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   // --- epilogue through the LDS ring in passes of ER rows: fragments -> [ER][BN+4] fp32
   // tile (the BN+4 stride keeps the fragment writes conflict-free) -> 4 consecutive
   // columns per thread for coalesced stores ---
-  constexpr int CS = BN_ + 4;
-  constexpr int LDSB = STAGES * STAGE_BYTES;
-  constexpr int ER = (BM_ * CS * 4 <= LDSB) ? BM_ : (WM * CS * 4 <= LDSB) ? WM : WM / 2;
-  constexpr int PASSES = BM_ / ER;
   static_assert(ER * CS * 4 <= LDSB && ER % 16 == 0, "epilogue tile fits the LDS ring");
   float* cs = reinterpret_cast<float*>(lds);
   // FP8 weights: each output column carries its weight scale (a lane's column is fixed
@@ -463,10 +492,26 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       else topk_tile_rows<ER, BN_, TOPK_MAX>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
       continue;
     }
-    for (int g = tid; g < ER * (BN_ / 4); g += NTHR) {
-      const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
-      const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
-      if (m < M && n < N) epilogue4<T>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), t_slot);
+    if constexpr (PRE) {
+      GemmEpi ep = epi;                 // bias and residual are already in pre_b / pre_r
+      ep.bias = nullptr;
+      if (ep.mode == EPI_RESID) ep.mode = EPI_STORE;
+#pragma unroll
+      for (int u = 0; u < EPG / NTHR; ++u) {
+        const int g = tid + u * NTHR, q = pass * (EPG / NTHR) + u;
+        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+        const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
+        float4 v = *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]);
+        if (epi.bias) { v.x += pre_b[q].x; v.y += pre_b[q].y; v.z += pre_b[q].z; v.w += pre_b[q].w; }
+        if (epi.mode == EPI_RESID) { v.x += pre_r[q].x; v.y += pre_r[q].y; v.z += pre_r[q].z; v.w += pre_r[q].w; }
+        if (m < M && n < N) epilogue4<T>(ep, m, n, N, v, t_slot);
+      }
+    } else {
+      for (int g = tid; g < EPG; g += NTHR) {
+        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+        const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
+        if (m < M && n < N) epilogue4<T>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), t_slot);
+      }
     }
   }
 }
