@@ -488,8 +488,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     }
     __syncthreads();
     if (ROLE == 2 && epi.mode == EPI_TOPK) {
-      if (epi.k2 == 1) topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
-      else topk_tile_rows<ER, BN_, TOPK_MAX>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
+      topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
       continue;
     }
     if constexpr (PRE) {

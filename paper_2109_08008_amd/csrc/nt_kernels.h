@@ -56,10 +56,9 @@ enum EpiMode : int {
   EPI_RESID = 2,      // out = resid + acc + bias  (resid may alias out)
   EPI_SELF_QKV = 3,   // decoder: cols [0,d) -> q out; [d,3d) -> K/V cache slot t of phys row
   EPI_CROSS_KV = 4,   // encoder: cols of [Ld][K|V][d] -> cross cache [Ld][2][B][H][S][dh]
-  EPI_TOPK = 5,       // output projection: per row and 128-column tile, the (max, sum exp,
-                      // k2 largest (value, index)) partials instead of the logits
+  EPI_TOPK = 5,       // output projection (greedy): per row and 128-column tile, the (max,
+                      // sum exp, largest (value, index)) partials instead of the logits
 };
-constexpr int TOPK_MAX = 8;   // k2 of the fused selection (greedy 1, beam up to 4 -> 8)
 __host__ __device__ inline int topk_record(int k2) { return 2 + 2 * k2; }   // floats per partial record
 
 struct GemmEpi {
@@ -229,12 +228,9 @@ hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, 
                        float* lse, hipStream_t s);
 hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, hipStream_t s);
 
-// Fused selection after an EPI_TOPK projection: merge the per-tile partials of each live
-// row.  Greedy: argmax + LSE, then the greedy update.  Beam: top-k2 + LSE into
-// topv/topi/lse for beam_update.
+// Fused greedy selection after an EPI_TOPK projection (k2 = 1): merges the per-tile
+// partials of each live row into the argmax and the LSE, then the greedy update.
 hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& st, hipStream_t s);
-hipError_t beam_merge(const float* part, int n_tiles, const int* ctl, int beam, int rows, int k2, float* topv,
-                      int* topi, float* lse, hipStream_t s);
 
 // End of a decode step (one workgroup): counts the unfinished sentences of the live list,
 // drops the finished ones in place when pruning, advances t, flips the ancestor half

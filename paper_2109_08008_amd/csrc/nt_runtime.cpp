@@ -468,7 +468,7 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.datt = take(R * d * eb);
   p.df = take(R * F * eb);
   // fp32 logits, or (fused selection) the per-tile partial records, whichever is larger
-  p.logits = take(std::max(R * m.V * 4, R * (size_t)((m.V + 127) / 128) * nt::topk_record(nt::TOPK_MAX) * 4));
+  p.logits = take(std::max(R * m.V * 4, R * (size_t)((m.V + 127) / 128) * nt::topk_record(1) * 4));
   p.comb = M > 1 ? take(R * m.V * 4) : 0;
   p.topv = take(R * 2 * K * 4);
   p.topi = take(R * 2 * K * 4);

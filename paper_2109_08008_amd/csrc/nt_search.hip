@@ -488,80 +488,6 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const floa
   }
 }
 
-// Beam selection from the projection's per-tile partials [rows][n_tiles][2 + 2*k2]: each
-// tile's k2 best (value desc, index asc) and its (max, sum exp).  Same merge as
-// beam_select_kernel, over tile lists instead of logits.
-template <int K2>
-__global__ __launch_bounds__(SEL_THREADS) void beam_merge_kernel(const float* __restrict__ part, int n_tiles,
-                                                                 const int* __restrict__ ctl, int beam, int k2,
-                                                                 float* __restrict__ topv, int* __restrict__ topi,
-                                                                 float* __restrict__ lse_out) {
-  __shared__ float wv[SEL_THREADS / kWave][K2];
-  __shared__ int wi[SEL_THREADS / kWave][K2];
-  __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave];
-  const int r = blockIdx.x;
-  if (r >= ctl[CTL_NLIVE] * beam) return;
-  const int rs = 2 + 2 * k2;
-  const float* rec = part + (size_t)r * n_tiles * rs;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-  MaxSum acc{-INFINITY, 0.f};
-  float v[K2];
-  int ix[K2];
-#pragma unroll
-  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
-  for (int i = tid; i < n_tiles; i += SEL_THREADS) {
-    const float* q = rec + (size_t)i * rs;
-    acc = ms_merge(acc, MaxSum{q[0], q[1]});
-    for (int j = 0; j < k2; ++j) {
-      const int qi = __float_as_int(q[3 + 2 * j]);
-      if (qi == INT_MAX) break;
-      list_insert<K2>(v, ix, q[2 + 2 * j], qi);
-    }
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
-  if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; }
-  for (int round = 0; round < K2; ++round) {
-    float bv = v[0];
-    int bi = ix[0];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    if (lane == 0) { wv[wave][round] = bv; wi[wave][round] = bi; }
-    if (ix[0] == bi && v[0] == bv && bi != INT_MAX) {
-#pragma unroll
-      for (int j = 0; j < K2 - 1; ++j) { v[j] = v[j + 1]; ix[j] = ix[j + 1]; }
-      v[K2 - 1] = -INFINITY;
-      ix[K2 - 1] = INT_MAX;
-    }
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int head[SEL_THREADS / kWave] = {0, 0, 0, 0};
-    for (int j = 0; j < k2; ++j) {
-      int w = 0;
-      float bv = -INFINITY;
-      int bi = INT_MAX;
-      for (int q = 0; q < SEL_THREADS / kWave; ++q) {
-        if (head[q] >= K2 || wi[q][head[q]] == INT_MAX) continue;
-        if (bi == INT_MAX || better(wv[q][head[q]], wi[q][head[q]], bv, bi)) {
-          bv = wv[q][head[q]]; bi = wi[q][head[q]]; w = q;
-        }
-      }
-      head[w]++;
-      topv[(size_t)r * k2 + j] = bv;
-      topi[(size_t)r * k2 + j] = bi;
-    }
-    MaxSum tot{sm[0], ss[0]};
-#pragma unroll
-    for (int w = 1; w < SEL_THREADS / kWave; ++w) tot = ms_merge(tot, MaxSum{sm[w], ss[w]});
-    lse_out[r] = tot.m + logf(tot.s);
-  }
-}
-
 // ---- beam: per-sentence update (one wave per live sentence) ----------------------------
 constexpr int MAXC = 8;       // candidates per lane: K * 2K <= 512 = 64 * 8
 
@@ -840,15 +766,6 @@ hipError_t greedy_step_fused(const float* part, int n_tiles, const SearchState& 
   const int rows = st.B * st.beam;
   if (rows <= 0) return hipSuccess;
   NT_LAUNCH(greedy_fused_kernel, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, st);
-  return hipGetLastError();
-}
-
-hipError_t beam_merge(const float* part, int n_tiles, const int* ctl, int beam, int rows, int k2, float* topv,
-                      int* topi, float* lse, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
-  if (k2 > TOPK_MAX) return hipErrorInvalidValue;
-  NT_LAUNCH(beam_merge_kernel<TOPK_MAX>, dim3(rows), dim3(SEL_THREADS), 0, s, part, n_tiles, ctl, beam, k2,
-                     topv, topi, lse);
   return hipGetLastError();
 }
 
