@@ -99,6 +99,11 @@ hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int
 
 // ---------------------------------------------------------------------------------
 // Normalisation / embedding kernels (one wave per row of d = 64*EPL elements).
+// Most partial sums a DLCL block start carries.  Two keep the kernel within 64 VGPRs at
+// eight elements a lane (eight waves per SIMD); four would save few more reads and cost
+// occupancy.
+constexpr int DLCL_PARTS = 2;
+
 struct DlclArgs {
   int l;                    // combination row l = 1..L+1; produces history entry l-1
   const void* y_prev;       // [rows][d] model dtype, or null for l = 1 (embedding)
@@ -119,6 +124,18 @@ struct DlclArgs {
   void* u_out;              // [rows][d]
   int rows, d;
   float eps;
+  // Blocked combination (same sums, fewer history reads): at the start of a block of
+  // rows, the pass over the old entries also accumulates the sums of entries 0..l-1 for
+  // the next n_part rows l+1 .. l+n_part (their weights in the triangle w_all, row r at
+  // w_all + r(r-1)/2), stored in fp32 at part_out + i * part_stride; a later row of the
+  // block starts from its partial (part_in) and adds entries k_start..l-1 only.  The fp32
+  // additions happen in the same order either way.
+  int n_part = 0;                 // 0 .. DLCL_PARTS
+  const float* w_all = nullptr;
+  float* part_out = nullptr;
+  size_t part_stride = 0;
+  const float* part_in = nullptr;
+  int k_start = 0;
 };
 hipError_t dlcl_combine(DT dt, const DlclArgs& a, hipStream_t s);
 

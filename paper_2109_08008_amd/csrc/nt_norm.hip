@@ -13,6 +13,12 @@
 namespace nt {
 namespace {
 
+// Holds v as a rounded fp32 register value, so that its conversion to the model dtype is a
+// rounding of its own.  Left alone, the compiler fuses the last multiply-add before a
+// 16-bit store with the conversion (one rounding instead of two) in some instantiations
+// and not in others, which would make the low bits depend on the instantiation.
+__device__ __forceinline__ void fp32_pin(float& v) { asm volatile("" : "+v"(v)); }
+
 constexpr int ROWS_PER_BLOCK = 4;
 
 // Eq. 2 at the end of encoder layer l-1:
@@ -22,8 +28,12 @@ constexpr int ROWS_PER_BLOCK = 4;
 // For l = 1, y_0 = sqrt(d) E[id] + PE(pos) is formed in registers (PAD positions -> 0).
 // Each history entry is read as stored (rounded to the model dtype), including the one
 // just produced, so the result does not depend on whether it came from memory.
-template <typename T, int EPL>
-__global__ __launch_bounds__(256) void dlcl_kernel(DlclArgs a) {
+// NP: most partial sums this instantiation carries (n_part <= NP; 0 for rows that carry
+// none).  With partials and at most eight elements a lane, the kernel is held to 64 VGPRs
+// so that eight waves share a SIMD, as for the other rows.
+template <typename T, int EPL, int NP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NP > 0 && EPL <= 8 ? 8 : 1)))
+void dlcl_kernel(DlclArgs a) {
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
   if (row >= a.rows) return;
   const int lane = threadIdx.x % kWave;
@@ -55,32 +65,69 @@ __global__ __launch_bounds__(256) void dlcl_kernel(DlclArgs a) {
 #pragma unroll
     for (int i = 0; i < EPL; ++i) h[i] = y[i];
   }
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) fp32_pin(h[i]);
   store_row<T, EPL>(hist + (size_t)(a.l - 1) * a.hist_stride + (size_t)row * d + c0, h);
 #pragma unroll
   for (int i = 0; i < EPL; ++i) h[i] = to_f32(from_f32<T>(h[i]));
 
   float acc[EPL];
+  if (a.part_in) {   // this row's sum of entries 0 .. k_start-1, from the block start
+    const float* pr = a.part_in + (size_t)row * d + c0;
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+    for (int i = 0; i < EPL; ++i) acc[i] = pr[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+  }
+  float pacc[NP > 0 ? NP : 1][EPL];
+#pragma unroll
+  for (int j = 0; j < NP; ++j)
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) pacc[j][i] = 0.f;
   const T* hrow = hist + (size_t)row * d + c0;
-#pragma unroll 4
-  for (int k = 0; k < a.l - 1; ++k) {
+#pragma unroll 2
+  for (int k = a.k_start; k < a.l - 1; ++k) {
     float e[EPL];
     load_row<T, EPL>(hrow + (size_t)k * a.hist_stride, e);
     const float w = a.w[k];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) acc[i] += w * e[i];
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      if (j < a.n_part) {
+        const int rj = a.l + 1 + j;
+        const float wj = a.w_all[(size_t)rj * (rj - 1) / 2 + k];
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) pacc[j][i] += wj * e[i];
+      }
+    }
   }
   {
     const float w = a.w[a.l - 1];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) acc[i] += w * h[i];
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+      if (j < a.n_part) {
+        const int rj = a.l + 1 + j;
+        const float wj = a.w_all[(size_t)rj * (rj - 1) / 2 + a.l - 1];
+        float* po = a.part_out + j * a.part_stride + (size_t)row * d + c0;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) po[i] = pacc[j][i] + wj * h[i];
+      }
+    }
   }
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) acc[i] = to_f32(from_f32<T>(acc[i]));
+  for (int i = 0; i < EPL; ++i) {
+    fp32_pin(acc[i]);
+    acc[i] = to_f32(from_f32<T>(acc[i]));
+  }
   if (a.x_out) store_row<T, EPL>(static_cast<T*>(a.x_out) + (size_t)row * d + c0, acc);
   float u[EPL];
   wave_layernorm<EPL>(acc, u, a.ln, a.ln + d, c0, inv_d, a.eps);
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) fp32_pin(u[i]);
   store_row<T, EPL>(static_cast<T*>(a.u_out) + (size_t)row * d + c0, u);
 }
 
@@ -160,7 +207,10 @@ __global__ void convert_kernel(const float* __restrict__ src, T* __restrict__ ds
 template <typename T>
 hipError_t dlcl_t(const DlclArgs& a, hipStream_t s) {
   const dim3 grid((a.rows + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
-#define NT_CALL(E) NT_LAUNCH((dlcl_kernel<T, E>), grid, dim3(256), 0, s, a)
+  if (a.n_part < 0 || a.n_part > DLCL_PARTS) return hipErrorInvalidValue;
+#define NT_CALL(E)                                                                    \
+  if (a.n_part > 0) NT_LAUNCH((dlcl_kernel<T, E, DLCL_PARTS>), grid, dim3(256), 0, s, a); \
+  else NT_LAUNCH((dlcl_kernel<T, E, 0>), grid, dim3(256), 0, s, a)
   NT_EPL_SWITCH(a.d, NT_CALL)
 #undef NT_CALL
   return hipGetLastError();

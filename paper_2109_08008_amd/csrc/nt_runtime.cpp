@@ -384,6 +384,44 @@ void quantize_fp8(const float* W, int in, int out, std::vector<uint8_t>& q, std:
 }
 
 // --------------------------------------------------------------------------------------
+// Blocked DLCL: a block start's pass over the old history entries also sums them for the
+// next n rows (n <= nt::DLCL_PARTS), which then start from those fp32 partial sums and
+// read only the entries after the block start.  The fp32 additions happen in the same
+// order, so the result is the same bit for bit.  The blocks are placed to move the fewest
+// bytes (history entries read and written, an fp32 partial counting as two entries): a
+// row that starts a block at l with n partials costs (l - 1) + 2n, the i-th row inside it
+// 2 + (i - 1).  Shallow encoders come out unblocked.
+// Returns sched[1..L+1]: the partial count of a row that starts a block (0: a plain row),
+// -1 for a row inside a block.
+std::vector<int> dlcl_schedule(int L) {
+  const int R = L + 1, P = nt::DLCL_PARTS;
+  std::vector<long long> f(R + 2, 0);   // f[l]: least cost of rows l..R, row l not in a block
+  std::vector<int> best(R + 2, 0);
+  for (int l = R; l >= 1; --l) {
+    f[l] = -1;
+    long long inside = 0;
+    for (int n = 0; n <= std::min(P, R - l); ++n) {
+      if (n > 0) inside += 2 + (n - 1);
+      const long long c = (l - 1) + 2LL * n + inside + f[l + n + 1];
+      if (f[l] < 0 || c < f[l]) {
+        f[l] = c;
+        best[l] = n;
+      }
+    }
+  }
+  std::vector<int> sched(R + 1, 0);
+  for (int l = 1; l <= R; l += best[l] + 1) {
+    sched[l] = best[l];
+    for (int i = 1; i <= best[l]; ++i) sched[l + i] = -1;
+  }
+  return sched;
+}
+int dlcl_max_parts(int L) {
+  const std::vector<int> s = dlcl_schedule(L);
+  return *std::max_element(s.begin(), s.end());
+}
+
+// --------------------------------------------------------------------------------------
 // workspace arena of one batch
 struct MemberPlan {
   size_t enc_out, cross, kself, vself;   // one model's encoder output and caches
@@ -397,7 +435,7 @@ struct WsPlan {
       best_row, best_nout, list, ctl, out_tok, out_lp, out_len, out_score;
   // encoder temporaries (union with the decoder buffers below); the members encode and
   // step one after another, so they share both, sized for the largest member
-  size_t hist, x, u, qkv, att, a, f, y;
+  size_t hist, x, u, qkv, att, a, f, y, dlcl_part;
   // decoder buffers (comb: an ensemble's combined scores)
   size_t z, du, dq, datt, df, logits, comb, topv, topi, lse;
 };
@@ -406,12 +444,13 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   WsPlan p;
   const int M = n_members(m);
   const size_t T = (size_t)B * S, R = (size_t)B * K, eb = m.eb;
-  size_t d = 0, F = 0, hist = 0;
+  size_t d = 0, F = 0, hist = 0, dlcl_part = 0;
   for (int i = 0; i < M; ++i) {
     const nt_model& mi = member(m, i);
     d = std::max<size_t>(d, mi.d);
     F = std::max<size_t>(F, mi.F);
     hist = std::max<size_t>(hist, (size_t)(mi.L + 1) * mi.d);
+    dlcl_part = std::max<size_t>(dlcl_part, (size_t)dlcl_max_parts(mi.L) * mi.d);
   }
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -459,6 +498,7 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.a = take(T * d * eb);
   p.f = take(T * F * eb);
   p.y = take(T * d * eb);
+  p.dlcl_part = take(dlcl_part * T * 4);   // fp32 partial sums of a DLCL block
   const size_t enc_end = off;
   // decoder buffers reuse the same space
   off = base;
@@ -566,6 +606,9 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
     return timed(NT_K_GEMM_ENC, s, bytes, 2.0 * T * N * K, [&] { return nt::gemm(m.dt, A, lda, W, T, N, K, e, s); });
   };
 
+  const std::vector<int> sched = dlcl_schedule(L);
+  int blk = 0;   // the row that started the current DLCL block
+
   for (int l = 1; l <= L + 1; ++l) {
     nt::DlclArgs a{};
     a.l = l;
@@ -588,7 +631,22 @@ nt_status run_encoder(nt_dec_state* st, int mi, hipStream_t s) {
     a.rows = T;
     a.d = d;
     a.eps = eps;
-    const double bytes = (double)T * d * eb * (l + (l <= L ? 3 : 2));
+    a.w_all = m.dlcl;
+    double hist_reads = l - 1;   // history entries this row reads (fp32 partials count twice)
+    if (sched[l] >= 0) {         // a plain row or a block start
+      blk = l;
+      if (sched[l] > 0) {
+        a.n_part = sched[l];
+        a.part_out = reinterpret_cast<float*>(at(p.dlcl_part));
+        a.part_stride = (size_t)T * d;
+        hist_reads += 2.0 * sched[l];
+      }
+    } else {                     // inside a block: start from the partial of entries < blk
+      a.part_in = reinterpret_cast<const float*>(at(p.dlcl_part)) + (size_t)(l - blk - 1) * T * d;
+      a.k_start = blk;
+      hist_reads = 2.0 + (l - 1 - blk);
+    }
+    const double bytes = (double)T * d * eb * (hist_reads + (l <= L ? 4 : 3));
     NT_HIP(timed(NT_K_DLCL, s, bytes, 2.0 * T * d * l, [&] { return nt::dlcl_combine(m.dt, a, s); }));
     if (l > L) break;
     const EncLayerW& w = m.enc[l - 1];

@@ -51,6 +51,41 @@ def test_encoder_output(name, dtype):
     assert err <= ENC_TOL[dtype]
 
 
+# Deep encoders (Sec. 3.1): at these depths the layer-input combination runs blocked, each
+# block start also summing the older history entries for the next few rows (up to two
+# rows at d <= 512, up to four at d = 1024).
+DEEP = {
+    "d64-L13": synth.ModelShape(64, 2, 256, 13, 1, 101),
+    "d128-L18": synth.ModelShape(128, 4, 512, 18, 1, 203),
+    "d1024-L14": synth.ModelShape(1024, 8, 1024, 14, 1, 101),
+}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+@pytest.mark.parametrize("name", list(DEEP))
+def test_deep_encoder_output_and_logits(name, dtype):
+    from paper_2109_08008_amd import nt
+    shape = DEEP[name]
+    blob = synth.make_weights(shape, seed=13, lively=True)
+    srcs, _, _ = _sentences(10, 1, 29, shape.vocab, seed=6)
+    model = G.new_model(shape, blob, dtype)
+    st, keep = G.gpu_encode(model, srcs, synth.SearchSetup(beam=1, max_len_b=4))
+    try:
+        enc = nt.nt_dec_state_encoder_out(st, shape.d_model)
+    finally:
+        nt.nt_free_state(st)
+    om = G.oracle_model(shape, blob, dtype)
+    enc_err = max(float(np.abs(enc[b, :len(s)] - om.encode(s)).max()) for b, s in enumerate(srcs))
+    rng = np.random.default_rng(7)
+    tgts = [list(rng.integers(3, shape.vocab, size=int(rng.integers(0, 9)))) for _ in srcs]
+    got, _, _ = G.gpu_teacher_forced(model, srcs, tgts, shape.vocab)
+    log_err = max(float(np.abs(got[b] - om.teacher_forced_logits(s, tg)).max())
+                  for b, (s, tg) in enumerate(zip(srcs, tgts)))
+    print(f"{name} {dtype}: encoder max abs err {enc_err:.3g}, logits {log_err:.3g}")
+    assert enc_err <= ENC_TOL[dtype]
+    assert log_err <= LOGIT_TOL[dtype]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("name", list(SHAPES))
 def test_teacher_forced_logits(name, dtype):
