@@ -52,6 +52,23 @@ __device__ __forceinline__ u32x4 f8_to_f16x8(unsigned w0, unsigned w1) {
   return u32x4{f8x2<false>(w0), f8x2<true>(w0), f8x2<false>(w1), f8x2<true>(w1)};
 }
 
+// Four consecutive elements of the model dtype as loaded (raw bits: converted only where
+// they are used, so the load does not have to complete where it is issued).
+template <typename T> struct Raw4 { using type = uint2; };
+template <> struct Raw4<float> { using type = float4; };
+template <typename T>
+__device__ __forceinline__ float4 raw4_to_f32(typename Raw4<T>::type r) {
+  if constexpr (std::is_same<T, float>::value) {
+    return r;
+  } else {
+    // pins the conversion here: the compiler would otherwise move it up to the load and
+    // wait for the data there
+    asm volatile("" : "+v"(r.x), "+v"(r.y));
+    const T* h = reinterpret_cast<const T*>(&r);
+    return make_float4(to_f32(h[0]), to_f32(h[1]), to_f32(h[2]), to_f32(h[3]));
+  }
+}
+
 // Applies the epilogue to up to 4 consecutive columns n..n+3 of row m (n % 4 == 0).
 // d, dh and ldc are multiples of 4 in every mode that scatters, so the 4 columns never
 // straddle a head or a K/V boundary and land on 4 consecutive destination elements.
@@ -308,6 +325,10 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   // live rows of a decode step: the grid covers the whole batch, and the workgroups past
   // the live tiles exit.  Live tiles take the lowest workgroup ids, which the dispatcher
   // deals round-robin over the 8 XCDs, so a shrinking batch still spreads over all of them.
+  // The arguments span three scalar-cache lines; naming fields from each of them here
+  // makes the three misses overlap instead of following one another down the prologue.
+  asm volatile("" ::"s"(epi.ctl), "s"(epi.bias), "s"(epi.out), "s"(epi.ldc), "s"(epi.wscale), "s"(epi.part),
+               "s"(tiles_n), "s"(M), "s"(Bt));
   if (epi.ctl) {
     M = min(M, epi.ctl[CTL_NLIVE] * epi.ctl_rows);
     tiles_m = (M + BM_ - 1) / BM_;
@@ -381,27 +402,33 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   constexpr int EPG = ER * (BN_ / 4);           // 4-column output groups per pass
   // The epilogue operands that do not depend on the product -- bias and residual -- are
   // fetched before the k-loop when each thread owns at most 4 output groups (the small
-  // decode-step tiles), so their latency hides behind it.  They are added in the order
-  // the epilogue adds them (bias, then residual), so results are bitwise unchanged.
+  // decode-step tiles), so their latency hides behind it.  They stay as loaded until the
+  // epilogue: converting them, or loading them under a per-thread branch (whose join
+  // copies the registers), would make the prologue wait for them before the first tile
+  // loads issue.  So every thread loads unconditionally, and a group that is ragged or not
+  // vector-aligned reads the (16-byte aligned) base of A instead and is left to the
+  // epilogue's own loads.  The epilogue adds them in its own order (bias, then residual),
+  // so results are bitwise unchanged.
   constexpr bool PRE = ROLE != 2 && EPG % NTHR == 0 && PASSES * (EPG / NTHR) <= 4;
   constexpr int NPRE = PRE ? PASSES * (EPG / NTHR) : 1;
-  float4 pre_b[NPRE], pre_r[NPRE];
+  using R4 = typename Raw4<T>::type;
+  float4 pre_b[NPRE];
+  R4 pre_r[NPRE];
+  unsigned pre_ok = 0;   // bit q: group q was fetched here
   if constexpr (PRE) {
+    const bool has_b = epi.bias != nullptr, has_r = epi.mode == EPI_RESID;   // the same in every thread
+    const char* safe = reinterpret_cast<const char*>(A);
 #pragma unroll
     for (int q = 0; q < NPRE; ++q) {
       const int pass = q / (EPG / NTHR), g = tid + (q % (EPG / NTHR)) * NTHR;
       const int m = m0 + pass * ER + g / (BN_ / 4), n = n0 + (g % (BN_ / 4)) * 4;
-      float b[4] = {0.f, 0.f, 0.f, 0.f}, rr[4] = {0.f, 0.f, 0.f, 0.f};
-      if (m < M && n < N) {
-        const int cnt = min(4, N - n);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          if (k < cnt && epi.bias) b[k] = epi.bias[n + k];
-          if (k < cnt && epi.mode == EPI_RESID) rr[k] = to_f32(static_cast<const T*>(epi.resid)[(size_t)m * epi.ldc + n + k]);
-        }
-      }
-      pre_b[q] = make_float4(b[0], b[1], b[2], b[3]);
-      pre_r[q] = make_float4(rr[0], rr[1], rr[2], rr[3]);
+      const char* bp = reinterpret_cast<const char*>(epi.bias + n);
+      const char* rp = reinterpret_cast<const char*>(static_cast<const T*>(epi.resid) + (size_t)m * epi.ldc + n);
+      const bool ok = m < M && n + 4 <= N && (!has_b || (reinterpret_cast<uintptr_t>(bp) & 15) == 0) &&
+                      (!has_r || (reinterpret_cast<uintptr_t>(rp) & (sizeof(R4) - 1)) == 0);
+      pre_ok |= (unsigned)ok << q;
+      if (has_b) pre_b[q] = *reinterpret_cast<const float4*>(ok ? bp : safe);
+      if (has_r) pre_r[q] = *reinterpret_cast<const R4*>(ok ? rp : safe);
     }
   }
 
@@ -492,7 +519,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       continue;
     }
     if constexpr (PRE) {
-      GemmEpi ep = epi;                 // bias and residual are already in pre_b / pre_r
+      GemmEpi ep = epi;                 // for groups whose bias and residual are in pre_b / pre_r
       ep.bias = nullptr;
       if (ep.mode == EPI_RESID) ep.mode = EPI_STORE;
 #pragma unroll
@@ -501,9 +528,18 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
         const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
         const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
         float4 v = *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]);
-        if (epi.bias) { v.x += pre_b[q].x; v.y += pre_b[q].y; v.z += pre_b[q].z; v.w += pre_b[q].w; }
-        if (epi.mode == EPI_RESID) { v.x += pre_r[q].x; v.y += pre_r[q].y; v.z += pre_r[q].z; v.w += pre_r[q].w; }
-        if (m < M && n < N) epilogue4<T>(ep, m, n, N, v, t_slot);
+        if (m < M && n < N) {
+          if ((pre_ok >> q) & 1u) {
+            if (epi.bias) { v.x += pre_b[q].x; v.y += pre_b[q].y; v.z += pre_b[q].z; v.w += pre_b[q].w; }
+            if (epi.mode == EPI_RESID) {
+              const float4 r = raw4_to_f32<T>(pre_r[q]);
+              v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+            }
+            epilogue4<T>(ep, m, n, N, v, t_slot);
+          } else {
+            epilogue4<T>(epi, m, n, N, v, t_slot);
+          }
+        }
       }
     } else {
       for (int g = tid; g < EPG; g += NTHR) {
@@ -582,6 +618,8 @@ hipError_t launch_role(const void* A, int lda, const void* Bt, int M, int N, int
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                 hipStream_t s, int role, int tile) {
   if (epi.wscale && dt != DT::F16) return hipErrorInvalidValue;   // FP8 weights pair with fp16
+  // operand rows move in 16-byte pieces, and the kernel reads A's base as a stand-in
+  if (((reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(Bt)) & 15) != 0) return hipErrorInvalidValue;
   switch (dt) {
     case DT::F32: return launch_role<float>(A, lda, Bt, M, N, K, epi, s, role, tile);
     case DT::F16: return launch_role<f16>(A, lda, Bt, M, N, K, epi, s, role, tile);
