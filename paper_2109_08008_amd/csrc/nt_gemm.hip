@@ -170,6 +170,43 @@ __device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
 // LdsWait<FM, FN>::run<N>(a, b): wait until at most N LDS operations of this wave are
 // outstanding (reads complete in order, so every read issued before the last N has
 // landed), naming the fragments a and b as its operands.
+// Bias and residual of the 4-column group (row m, columns n..n+3), fetched ahead of the
+// group's epilogue as raw vectors.  Every thread loads unconditionally (a per-thread
+// branch around the loads makes the compiler wait for them at its join): a group that is
+// out of range, ragged or not vector-aligned reads `safe` (any readable 16-byte aligned
+// address) instead and reports false, and its epilogue then loads for itself.
+template <typename T>
+__device__ __forceinline__ bool fetch_group(const GemmEpi& e, bool has_b, bool has_r, const char* safe, int m,
+                                            int n, int M, int N, float4& b, typename Raw4<T>::type& r) {
+  using R4 = typename Raw4<T>::type;
+  const char* bp = has_b ? reinterpret_cast<const char*>(e.bias + n) : safe;
+  const char* rp = has_r ? reinterpret_cast<const char*>(static_cast<const T*>(e.resid) + (size_t)m * e.ldc + n) : safe;
+  const bool ok = m < M && n + 4 <= N && (!has_b || (reinterpret_cast<uintptr_t>(bp) & 15) == 0) &&
+                  (!has_r || (reinterpret_cast<uintptr_t>(rp) & (sizeof(R4) - 1)) == 0);
+  if (has_b) b = *reinterpret_cast<const float4*>(ok ? bp : safe);
+  if (has_r) r = *reinterpret_cast<const R4*>(ok ? rp : safe);
+  return ok;
+}
+
+// The epilogue of one group: with its operands fetched (ok), adds bias, then residual --
+// the order epilogue4 adds them in -- and stores through `plain` (e without bias, EPI_RESID
+// turned into EPI_STORE); otherwise e's own epilogue.
+template <typename T>
+__device__ __forceinline__ void finish_group(const GemmEpi& e, const GemmEpi& plain, bool ok, int m, int n, int N,
+                                             float4 v, const float4& b, const typename Raw4<T>::type& r,
+                                             int t_slot) {
+  if (ok) {
+    if (e.bias) { v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w; }
+    if (e.mode == EPI_RESID) {
+      const float4 rf = raw4_to_f32<T>(r);
+      v.x += rf.x; v.y += rf.y; v.z += rf.z; v.w += rf.w;
+    }
+    epilogue4<T>(plain, m, n, N, v, t_slot);
+  } else {
+    epilogue4<T>(e, m, n, N, v, t_slot);
+  }
+}
+
 template <int FM, int FN> struct LdsWait;
 template <> struct LdsWait<1, 1> {
   template <int N = 0>
@@ -415,20 +452,14 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   float4 pre_b[NPRE];
   R4 pre_r[NPRE];
   unsigned pre_ok = 0;   // bit q: group q was fetched here
+  const bool has_b = epi.bias != nullptr, has_r = epi.mode == EPI_RESID;   // the same in every thread
+  const char* safe = reinterpret_cast<const char*>(A);
   if constexpr (PRE) {
-    const bool has_b = epi.bias != nullptr, has_r = epi.mode == EPI_RESID;   // the same in every thread
-    const char* safe = reinterpret_cast<const char*>(A);
 #pragma unroll
     for (int q = 0; q < NPRE; ++q) {
       const int pass = q / (EPG / NTHR), g = tid + (q % (EPG / NTHR)) * NTHR;
       const int m = m0 + pass * ER + g / (BN_ / 4), n = n0 + (g % (BN_ / 4)) * 4;
-      const char* bp = reinterpret_cast<const char*>(epi.bias + n);
-      const char* rp = reinterpret_cast<const char*>(static_cast<const T*>(epi.resid) + (size_t)m * epi.ldc + n);
-      const bool ok = m < M && n + 4 <= N && (!has_b || (reinterpret_cast<uintptr_t>(bp) & 15) == 0) &&
-                      (!has_r || (reinterpret_cast<uintptr_t>(rp) & (sizeof(R4) - 1)) == 0);
-      pre_ok |= (unsigned)ok << q;
-      if (has_b) pre_b[q] = *reinterpret_cast<const float4*>(ok ? bp : safe);
-      if (has_r) pre_r[q] = *reinterpret_cast<const R4*>(ok ? rp : safe);
+      pre_ok |= (unsigned)fetch_group<T>(epi, has_b, has_r, safe, m, n, M, N, pre_b[q], pre_r[q]) << q;
     }
   }
 
@@ -499,9 +530,30 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     const int n = n0 + wn * WN + j * 16 + fr;
     wsc[j] = F8 ? (n < N ? epi.wscale[n] : 0.f) : 1.f;
   }
+  // Tiles without the prologue prefetch fetch each pass's bias and residual before staging
+  // the pass through LDS, so the loads are in flight while it is staged; and all of them
+  // before any store: a load issued after a store waits for it (the output may alias the
+  // residual), one round trip per group.  Groups are disjoint between threads, and each
+  // residual element is read by the thread that overwrites it, so reading them all first
+  // is the same computation.
+  constexpr bool BATCH = !PRE && EPG % NTHR == 0;
+  constexpr int GPT = BATCH ? EPG / NTHR : 1;
 #pragma unroll
   for (int pass = 0; pass < PASSES; ++pass) {
     if (pass) __syncthreads();
+    float4 eb[GPT];
+    R4 er[GPT];
+    unsigned eok = 0;
+    if constexpr (BATCH) {
+      if (!(ROLE == 2 && epi.mode == EPI_TOPK)) {
+#pragma unroll
+        for (int u = 0; u < GPT; ++u) {
+          const int g = tid + u * NTHR;
+          const int m = m0 + pass * ER + g / (BN_ / 4), n = n0 + (g % (BN_ / 4)) * 4;
+          eok |= (unsigned)fetch_group<T>(epi, has_b, has_r, safe, m, n, M, N, eb[u], er[u]) << u;
+        }
+      }
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int rb = wm * WM + i * 16;            // first tile row of this block
@@ -518,28 +570,28 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
       continue;
     }
+    GemmEpi plain = epi;   // for groups whose bias and residual were fetched ahead
+    plain.bias = nullptr;
+    if (plain.mode == EPI_RESID) plain.mode = EPI_STORE;
     if constexpr (PRE) {
-      GemmEpi ep = epi;                 // for groups whose bias and residual are in pre_b / pre_r
-      ep.bias = nullptr;
-      if (ep.mode == EPI_RESID) ep.mode = EPI_STORE;
 #pragma unroll
       for (int u = 0; u < EPG / NTHR; ++u) {
         const int g = tid + u * NTHR, q = pass * (EPG / NTHR) + u;
         const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
         const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
-        float4 v = *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]);
-        if (m < M && n < N) {
-          if ((pre_ok >> q) & 1u) {
-            if (epi.bias) { v.x += pre_b[q].x; v.y += pre_b[q].y; v.z += pre_b[q].z; v.w += pre_b[q].w; }
-            if (epi.mode == EPI_RESID) {
-              const float4 r = raw4_to_f32<T>(pre_r[q]);
-              v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
-            }
-            epilogue4<T>(ep, m, n, N, v, t_slot);
-          } else {
-            epilogue4<T>(epi, m, n, N, v, t_slot);
-          }
-        }
+        if (m < M && n < N)
+          finish_group<T>(epi, plain, (pre_ok >> q) & 1u, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]),
+                          pre_b[q], pre_r[q], t_slot);
+      }
+    } else if constexpr (BATCH) {
+#pragma unroll
+      for (int u = 0; u < GPT; ++u) {
+        const int g = tid + u * NTHR;
+        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+        const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
+        if (m < M && n < N)
+          finish_group<T>(epi, plain, (eok >> u) & 1u, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]),
+                          eb[u], er[u], t_slot);
       }
     } else {
       for (int g = tid; g < EPG; g += NTHR) {
