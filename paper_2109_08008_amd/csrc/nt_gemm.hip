@@ -69,74 +69,76 @@ __device__ __forceinline__ float4 raw4_to_f32(typename Raw4<T>::type r) {
   }
 }
 
-// Applies the epilogue to up to 4 consecutive columns n..n+3 of row m (n % 4 == 0).
-// d, dh and ldc are multiples of 4 in every mode that scatters, so the 4 columns never
-// straddle a head or a K/V boundary and land on 4 consecutive destination elements.
-template <typename T>
+// Applies the epilogue MODE to up to 4 consecutive columns n..n+3 of row m (n % 4 == 0).
+// With OPS, it adds the bias (if any) and, for EPI_RESID, the residual itself; without,
+// the caller has added both (an EPI_RESID group is then a plain store).  The mode is a
+// template argument so that a tile's unrolled groups carry only their own mode's code.
+// fp32 output (out_f32) goes with EPI_STORE only.  d, dh and ldc are multiples of 4 in
+// every mode that scatters, so the 4 columns never straddle a head or a K/V boundary and
+// land on 4 consecutive destination elements.
+template <typename T, int MODE, bool OPS>
 __device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N, float4 v4, int t_slot) {
   float v[4] = {v4.x, v4.y, v4.z, v4.w};
   const int cnt = min(4, N - n);
-  if (e.bias) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      if (k < cnt) v[k] += e.bias[n + k];
-  }
-  const bool vec = cnt == 4 && (e.ldc & 3) == 0;
-  if (e.out_f32) {
-    float* o = static_cast<float*>(e.out) + (size_t)m * e.ldc + n;
-    if (vec) {
-      *reinterpret_cast<float4*>(o) = make_float4(v[0], v[1], v[2], v[3]);
-    } else {
+  if constexpr (OPS) {
+    if (e.bias) {
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        if (k < cnt) o[k] = v[k];
+        if (k < cnt) v[k] += e.bias[n + k];
     }
-    return;
+  }
+  const bool vec = cnt == 4 && (e.ldc & 3) == 0;
+  if constexpr (MODE == EPI_STORE) {
+    if (e.out_f32) {
+      float* o = static_cast<float*>(e.out) + (size_t)m * e.ldc + n;
+      if (vec) {
+        *reinterpret_cast<float4*>(o) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (k < cnt) o[k] = v[k];
+      }
+      return;
+    }
   }
   T* o = nullptr;
-  switch (e.mode) {
-    case EPI_STORE:
-      o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
-      break;
-    case EPI_RELU:
+  if constexpr (MODE == EPI_STORE) {
+    o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
+  } else if constexpr (MODE == EPI_RELU) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) v[k] = fmaxf(v[k], 0.f);
-      o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
-      break;
-    case EPI_RESID: {
+    for (int k = 0; k < 4; ++k) v[k] = fmaxf(v[k], 0.f);
+    o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
+  } else if constexpr (MODE == EPI_RESID) {
+    if constexpr (OPS) {
       const T* r = static_cast<const T*>(e.resid) + (size_t)m * e.ldc + n;
 #pragma unroll
       for (int k = 0; k < 4; ++k)
         if (k < cnt) v[k] += to_f32(r[k]);
+    }
+    o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
+  } else if constexpr (MODE == EPI_SELF_QKV) {
+    if (n < e.d) {
       o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
-      break;
-    }
-    case EPI_SELF_QKV: {
-      if (n < e.d) {
-        o = static_cast<T*>(e.out) + (size_t)m * e.ldc + n;
-      } else {
-        int c = n - e.d;
-        const int kv = c >= e.d;
-        c -= kv * e.d;
-        const int h = c / e.dh, x = c - h * e.dh;
-        const int p = e.sent_list[m / e.beam] * e.beam + m % e.beam;
-        o = static_cast<T*>(kv ? e.vcache : e.kcache) + ((size_t)(p * e.H + h) * e.Tcap + t_slot) * e.dh + x;
-      }
-      break;
-    }
-    case EPI_CROSS_KV: {
-      const int j = n / (2 * e.d);
-      int c = n - j * 2 * e.d;
+    } else {
+      int c = n - e.d;
       const int kv = c >= e.d;
       c -= kv * e.d;
       const int h = c / e.dh, x = c - h * e.dh;
-      const int b = m / e.S, s = m - b * e.S;
-      o = static_cast<T*>(e.cross) + ((((size_t)j * 2 + kv) * e.B + b) * e.H + h) * (size_t)e.S * e.dh +
-          (size_t)s * e.dh + x;
-      break;
+      const int p = e.sent_list[m / e.beam] * e.beam + m % e.beam;
+      o = static_cast<T*>(kv ? e.vcache : e.kcache) + ((size_t)(p * e.H + h) * e.Tcap + t_slot) * e.dh + x;
     }
+  } else {
+    static_assert(MODE == EPI_CROSS_KV, "epilogue mode");
+    const int j = n / (2 * e.d);
+    int c = n - j * 2 * e.d;
+    const int kv = c >= e.d;
+    c -= kv * e.d;
+    const int h = c / e.dh, x = c - h * e.dh;
+    const int b = m / e.S, s = m - b * e.S;
+    o = static_cast<T*>(e.cross) + ((((size_t)j * 2 + kv) * e.B + b) * e.H + h) * (size_t)e.S * e.dh +
+        (size_t)s * e.dh + x;
   }
-  if (vec || (e.mode >= EPI_SELF_QKV && cnt == 4)) {
+  if (vec || (MODE >= EPI_SELF_QKV && cnt == 4)) {
     if constexpr (sizeof(T) == 2) {
       T t4[4] = {from_f32<T>(v[0]), from_f32<T>(v[1]), from_f32<T>(v[2]), from_f32<T>(v[3])};
       *reinterpret_cast<uint2*>(o) = *reinterpret_cast<const uint2*>(t4);
@@ -189,21 +191,19 @@ __device__ __forceinline__ bool fetch_group(const GemmEpi& e, bool has_b, bool h
 }
 
 // The epilogue of one group: with its operands fetched (ok), adds bias, then residual --
-// the order epilogue4 adds them in -- and stores through `plain` (e without bias, EPI_RESID
-// turned into EPI_STORE); otherwise e's own epilogue.
-template <typename T>
-__device__ __forceinline__ void finish_group(const GemmEpi& e, const GemmEpi& plain, bool ok, int m, int n, int N,
-                                             float4 v, const float4& b, const typename Raw4<T>::type& r,
-                                             int t_slot) {
+// the order epilogue4 adds them in -- and stores; otherwise epilogue4 loads them itself.
+template <typename T, int MODE>
+__device__ __forceinline__ void finish_group(const GemmEpi& e, bool ok, int m, int n, int N, float4 v,
+                                             const float4& b, const typename Raw4<T>::type& r, int t_slot) {
   if (ok) {
     if (e.bias) { v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w; }
-    if (e.mode == EPI_RESID) {
+    if constexpr (MODE == EPI_RESID) {
       const float4 rf = raw4_to_f32<T>(r);
       v.x += rf.x; v.y += rf.y; v.z += rf.z; v.w += rf.w;
     }
-    epilogue4<T>(plain, m, n, N, v, t_slot);
+    epilogue4<T, MODE, false>(e, m, n, N, v, t_slot);
   } else {
-    epilogue4<T>(e, m, n, N, v, t_slot);
+    epilogue4<T, MODE, true>(e, m, n, N, v, t_slot);
   }
 }
 
@@ -570,35 +570,44 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
       continue;
     }
-    GemmEpi plain = epi;   // for groups whose bias and residual were fetched ahead
-    plain.bias = nullptr;
-    if (plain.mode == EPI_RESID) plain.mode = EPI_STORE;
-    if constexpr (PRE) {
+    // The mode is the same for every thread: one branch per pass, then that mode's groups.
+    auto finish_pass = [&](auto mode_c) {
+      constexpr int MODE = decltype(mode_c)::value;
+      if constexpr (PRE) {
 #pragma unroll
-      for (int u = 0; u < EPG / NTHR; ++u) {
-        const int g = tid + u * NTHR, q = pass * (EPG / NTHR) + u;
-        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
-        const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
-        if (m < M && n < N)
-          finish_group<T>(epi, plain, (pre_ok >> q) & 1u, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]),
-                          pre_b[q], pre_r[q], t_slot);
-      }
-    } else if constexpr (BATCH) {
+        for (int u = 0; u < EPG / NTHR; ++u) {
+          const int g = tid + u * NTHR, q = pass * (EPG / NTHR) + u;
+          const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+          const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
+          if (m < M && n < N)
+            finish_group<T, MODE>(epi, (pre_ok >> q) & 1u, m, n, N,
+                                  *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), pre_b[q], pre_r[q], t_slot);
+        }
+      } else if constexpr (BATCH) {
 #pragma unroll
-      for (int u = 0; u < GPT; ++u) {
-        const int g = tid + u * NTHR;
-        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
-        const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
-        if (m < M && n < N)
-          finish_group<T>(epi, plain, (eok >> u) & 1u, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]),
-                          eb[u], er[u], t_slot);
+        for (int u = 0; u < GPT; ++u) {
+          const int g = tid + u * NTHR;
+          const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+          const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
+          if (m < M && n < N)
+            finish_group<T, MODE>(epi, (eok >> u) & 1u, m, n, N,
+                                  *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), eb[u], er[u], t_slot);
+        }
+      } else {
+        for (int g = tid; g < EPG; g += NTHR) {
+          const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+          const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
+          if (m < M && n < N)
+            epilogue4<T, MODE, true>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), t_slot);
+        }
       }
-    } else {
-      for (int g = tid; g < EPG; g += NTHR) {
-        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
-        const int m = m0 + pass * ER + row, n = n0 + c4 * 4;
-        if (m < M && n < N) epilogue4<T>(epi, m, n, N, *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]), t_slot);
-      }
+    };
+    switch (epi.mode) {
+      case EPI_RELU: finish_pass(std::integral_constant<int, EPI_RELU>{}); break;
+      case EPI_RESID: finish_pass(std::integral_constant<int, EPI_RESID>{}); break;
+      case EPI_SELF_QKV: finish_pass(std::integral_constant<int, EPI_SELF_QKV>{}); break;
+      case EPI_CROSS_KV: finish_pass(std::integral_constant<int, EPI_CROSS_KV>{}); break;
+      default: finish_pass(std::integral_constant<int, EPI_STORE>{}); break;
     }
   }
 }
