@@ -536,7 +536,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   // residual), one round trip per group.  Groups are disjoint between threads, and each
   // residual element is read by the thread that overwrites it, so reading them all first
   // is the same computation.
-  constexpr bool BATCH = !PRE && EPG % NTHR == 0;
+  constexpr bool BATCH = !PRE && EPG % NTHR == 0 && ROLE != 2;   // the projection has no operands to fetch
   constexpr int GPT = BATCH ? EPG / NTHR : 1;
 #pragma unroll
   for (int pass = 0; pass < PASSES; ++pass) {
