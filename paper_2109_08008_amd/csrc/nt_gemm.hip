@@ -173,10 +173,13 @@ __device__ __forceinline__ u32x4 lds_read16(const unsigned char* p) {
 // outstanding (reads complete in order, so every read issued before the last N has
 // landed), naming the fragments a and b as its operands.
 // Bias and residual of the 4-column group (row m, columns n..n+3), fetched ahead of the
-// group's epilogue as raw vectors.  Every thread loads unconditionally (a per-thread
-// branch around the loads makes the compiler wait for them at its join): a group that is
-// out of range, ragged or not vector-aligned reads `safe` (any readable 16-byte aligned
-// address) instead and reports false, and its epilogue then loads for itself.
+// group's epilogue as raw vectors.  Both loads are issued unconditionally, without any
+// branch: a per-thread branch makes the compiler wait for the loads at its join, and even
+// a uniform one per group becomes a jump to out-of-line code, an instruction-cache miss
+// per group in these large unrolled kernels.  An operand the epilogue does not have, and
+// a group that is out of range, ragged or not vector-aligned, read `safe` (any readable
+// 16-byte aligned address; always the same cached line) instead; such a group reports
+// false and its epilogue then loads for itself.
 template <typename T>
 __device__ __forceinline__ bool fetch_group(const GemmEpi& e, bool has_b, bool has_r, const char* safe, int m,
                                             int n, int M, int N, float4& b, typename Raw4<T>::type& r) {
@@ -185,8 +188,8 @@ __device__ __forceinline__ bool fetch_group(const GemmEpi& e, bool has_b, bool h
   const char* rp = has_r ? reinterpret_cast<const char*>(static_cast<const T*>(e.resid) + (size_t)m * e.ldc + n) : safe;
   const bool ok = m < M && n + 4 <= N && (!has_b || (reinterpret_cast<uintptr_t>(bp) & 15) == 0) &&
                   (!has_r || (reinterpret_cast<uintptr_t>(rp) & (sizeof(R4) - 1)) == 0);
-  if (has_b) b = *reinterpret_cast<const float4*>(ok ? bp : safe);
-  if (has_r) r = *reinterpret_cast<const R4*>(ok ? rp : safe);
+  b = *reinterpret_cast<const float4*>(ok ? bp : safe);
+  r = *reinterpret_cast<const R4*>(ok ? rp : safe);
   return ok;
 }
 
@@ -195,7 +198,7 @@ __device__ __forceinline__ bool fetch_group(const GemmEpi& e, bool has_b, bool h
 template <typename T, int MODE>
 __device__ __forceinline__ void finish_group(const GemmEpi& e, bool ok, int m, int n, int N, float4 v,
                                              const float4& b, const typename Raw4<T>::type& r, int t_slot) {
-  if (ok) {
+  if (__builtin_expect(ok, 1)) {
     if (e.bias) { v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w; }
     if constexpr (MODE == EPI_RESID) {
       const float4 rf = raw4_to_f32<T>(r);
