@@ -269,6 +269,17 @@ nt_status nt_quantize_fp8(const float* h_W, int32_t in, int32_t out, uint8_t* h_
 nt_status nt_op_select(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv, int32_t* d_topi,
                        float* d_lse, void* stream);
 
+/* The same selection as the beam search runs it from the output projection's per-tile
+ * records (the projection's epilogue leaves, per row and 128-column tile, the tile row's
+ * max and sum of exp(x - max)): with tau the k-th largest tile maximum of a row, every one
+ * of the row's k largest logits lies in a tile whose maximum is >= tau, so only those
+ * tiles are read back, and the log-sum-exp is merged from the records.  Here the records
+ * are formed from d_logits by a separate kernel, in a device buffer this call allocates
+ * and frees.  Same arguments, layout and results as nt_op_select (the log-sum-exp summed
+ * in another order); additionally V <= 65536.  For tests. */
+nt_status nt_op_select_tiled(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv,
+                             int32_t* d_topi, float* d_lse, void* stream);
+
 /* Process-wide switch for nt_translate's graph replay of the decoder step (default on;
  * with 0, every step is launched kernel by kernel). */
 nt_status nt_set_graphs(int32_t enable);

@@ -257,7 +257,9 @@ template <> struct LdsWait<4, 4> {
 // Fused selection epilogue: the rows of an LDS-staged fp32 tile (ER rows x BN columns,
 // row stride CS) are reduced to one partial record per row -- running max, sum of
 // exp(x - max), and the k2 largest (value, index) in (value desc, index asc) order.
-// TPR consecutive lanes share a row; each scans a contiguous run of columns.
+// TPR consecutive lanes share a row; each scans a contiguous run of columns.  K2 = 0
+// leaves only (max, sum), in two branch-free passes (the max, then one exponential per
+// logit), for beam search, which reads its candidates back from the stored logits.
 __device__ __forceinline__ bool topk_better(float v1, int i1, float v2, int i2) {
   return v1 > v2 || (v1 == v2 && i1 < i2);
 }
@@ -269,6 +271,33 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
   static_assert(TPR >= 1 && TPR <= kWave && (TPR & (TPR - 1)) == 0, "row group inside a wave");
   const int row = threadIdx.x / TPR, sub = threadIdx.x % TPR;
   const int m = mrow0 + row;
+  if constexpr (K2 == 0) {
+    float mx = -INFINITY;
+    for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
+      const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
+      const float xs[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, n0 + g4 * 4 + u < N ? xs[u] : -INFINITY);
+    }
+#pragma unroll
+    for (int o = TPR / 2; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    float sum = 0.f;
+    if (mx != -INFINITY) {
+      for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
+        const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
+        const float xs[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sum += __expf((n0 + g4 * 4 + u < N ? xs[u] : -INFINITY) - mx);
+      }
+    }
+#pragma unroll
+    for (int o = TPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, kWave);
+    if (sub == 0 && m < M) {
+      float* rec = e.part + ((size_t)m * e.n_tiles + tn) * topk_record(e.k2);
+      rec[0] = mx;
+      rec[1] = sum;
+    }
+  } else {
   float mx = -INFINITY, sum = 0.f;
   float v[K2];
   int ix[K2];
@@ -338,6 +367,7 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
       v[K2 - 1] = -INFINITY;
       ix[K2 - 1] = INT_MAX;
     }
+  }
   }
 }
 
@@ -570,8 +600,11 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     }
     __syncthreads();
     if (ROLE == 2 && epi.mode == EPI_TOPK) {
-      topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
-      continue;
+      if (!epi.out) {   // greedy: the records are all its selection needs
+        topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
+        continue;
+      }
+      topk_tile_rows<ER, BN_, 0>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);   // beam also stores the logits
     }
     // The mode is the same for every thread: one branch per pass, then that mode's groups.
     auto finish_pass = [&](auto mode_c) {

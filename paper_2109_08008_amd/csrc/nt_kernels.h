@@ -56,8 +56,9 @@ enum EpiMode : int {
   EPI_RESID = 2,      // out = resid + acc + bias  (resid may alias out)
   EPI_SELF_QKV = 3,   // decoder: cols [0,d) -> q out; [d,3d) -> K/V cache slot t of phys row
   EPI_CROSS_KV = 4,   // encoder: cols of [Ld][K|V][d] -> cross cache [Ld][2][B][H][S][dh]
-  EPI_TOPK = 5,       // output projection (greedy): per row and 128-column tile, the (max,
-                      // sum exp, largest (value, index)) partials instead of the logits
+  EPI_TOPK = 5,       // output projection: per row and 128-column tile, the (max, sum exp,
+                      // largest (value, index)) partials -- instead of the logits (greedy),
+                      // or with out set, as well as the fp32 logits (beam)
 };
 __host__ __device__ inline int topk_record(int k2) { return 2 + 2 * k2; }   // floats per partial record
 
@@ -244,6 +245,14 @@ hipError_t ens_combine(const float* logits, float* comb, const int* ctl, int bea
 hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, int V, int k2, float* topv, int* topi,
                        float* lse, hipStream_t s);
 hipError_t beam_update(const float* topv, const int* topi, const float* lse, const SearchState& st, hipStream_t s);
+// The same selection from an EPI_TOPK projection that also wrote the logits: part holds
+// each row's per-tile records (k2 = 1 layout, n_tiles = ceil(V / 128) <= 512), and only
+// the tiles that can hold one of the row's k2 largest logits are read back.  Same
+// results as beam_select (the log-sum-exp merged from the records).
+hipError_t beam_select_tiles(const float* part, int n_tiles, const float* logits, const int* ctl, int beam, int rows,
+                             int V, int k2, float* topv, int* topi, float* lse, hipStream_t s);
+// Per-tile records of a logits matrix in the projection epilogue's layout (for tests).
+hipError_t tile_records(const float* logits, int rows, int V, float* part, hipStream_t s);
 
 // Fused greedy selection after an EPI_TOPK projection (k2 = 1): merges the per-tile
 // partials of each live row into the argmax and the LSE, then the greedy update.

@@ -438,6 +438,7 @@ struct WsPlan {
   size_t hist, x, u, qkv, att, a, f, y, dlcl_part;
   // decoder buffers (comb: an ensemble's combined scores)
   size_t z, du, dq, datt, df, logits, comb, topv, topi, lse;
+  size_t tparts;   // beam: the projection's per-tile records, beside the logits
 };
 
 WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
@@ -513,6 +514,7 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.topv = take(R * 2 * K * 4);
   p.topi = take(R * 2 * K * 4);
   p.lse = take(R * 4);
+  p.tparts = take(K > 1 ? R * (size_t)((m.V + 127) / 128) * nt::topk_record(1) * 4 : 0);
   p.total = std::max(enc_end, off);
   return p;
 }
@@ -752,7 +754,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
     const float eps = m.cfg.ln_eps;
 
     auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
-      const double ob = e.mode == nt::EPI_TOPK ? 0.0 : e.out_f32 ? 4.0 : eb;
+      const double ob = (e.mode == nt::EPI_TOPK && !e.out) ? 0.0 : e.out_f32 ? 4.0 : eb;
       const double wb = e.wscale ? 1.0 : eb;   // bytes per weight (FP8: one)
       const double bytes = (double)R * Kd * eb + (double)N * Kd * wb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
       const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
@@ -884,12 +886,13 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
                    [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), Rp, d, eps, s, ctl, K); }));
     }
 
-    // Tied output projection.  Normally the projection's epilogue reduces each row to
-    // per-tile (max, sum exp, best) partials and the logits never reach HBM; teacher
-    // forcing and the logits copy-out use the plain path that writes fp32 logits.
-    // (measured: the fused epilogue pays for itself for greedy's argmax; a top-8 per tile
-    // row costs more than writing and re-reading the logits, so beam keeps the plain path)
-    // An ensemble member writes its logits and folds them into the combined scores.
+    // Tied output projection.  Its epilogue reduces each row to per-tile (max, sum exp,
+    // best) records: greedy needs nothing else, so its logits never reach HBM; beam also
+    // stores the logits and reads back only the tiles that can hold a row's 2K largest.
+    // Teacher forcing and the logits copy-out use the plain path that writes fp32 logits.
+    // (measured: a top-8 per tile row in the epilogue costs more than the (max, sum)
+    // records and the targeted re-read.)  An ensemble member writes its logits and folds
+    // them into the combined scores.
     if (M > 1) {
       nt::GemmEpi e{};
       e.mode = nt::EPI_STORE;
@@ -911,7 +914,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       const float* part = st->at<float>(p.logits);
       const double pbytes = (double)R * n_tiles * nt::topk_record(1) * 4;
       NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, s); }));
-    } else {
+    } else if (d_logits || d_forced) {   // teacher forcing, or the caller wants the logits
       nt::GemmEpi e{};
       e.mode = nt::EPI_STORE;
       e.out = at(p.logits);
@@ -931,6 +934,27 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
           return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, s);
         }));
       }
+    } else {
+      // Beam: the projection also leaves per-tile (max, sum exp) records, so the selection
+      // reads them and only the few tiles that can hold a row's 2K largest logits.
+      const int n_tiles = (m.V + 127) / 128;
+      nt::GemmEpi e{};
+      e.mode = nt::EPI_TOPK;
+      e.part = st->at<float>(p.tparts);
+      e.k2 = 1;
+      e.n_tiles = n_tiles;
+      e.out = at(p.logits);
+      e.ldc = m.V;
+      e.out_f32 = 1;
+      NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
+      const double sbytes = (double)R * (n_tiles * nt::topk_record(1) * 4.0 + 2.0 * K * 128 * 4);
+      NT_HIP(timed(NT_K_SELECT, s, sbytes, 0.0, [&] {
+        return nt::beam_select_tiles(st->at<float>(p.tparts), n_tiles, st->at<float>(p.logits), ctl, K, Rp, m.V,
+                                     2 * K, st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), s);
+      }));
+      NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
+        return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, s);
+      }));
     }
   }   // members
 
@@ -1728,6 +1752,27 @@ nt_status nt_op_select(const float* d_logits, int32_t rows, int32_t V, int32_t k
   if (rows < 0 || V <= 0) return fail(NT_E_INVALID, "rows must be >= 0 and V > 0");
   if (k < 1 || k > 32 || k > V) return fail(NT_E_UNSUPPORTED, "k must be in [1, min(32, V)]");
   NT_HIP(nt::beam_select(d_logits, nullptr, 1, rows, V, k, d_topv, d_topi, d_lse, static_cast<hipStream_t>(stream)));
+  return NT_OK;
+}
+
+nt_status nt_op_select_tiled(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv,
+                             int32_t* d_topi, float* d_lse, void* stream) {
+  g_err.clear();
+  if (!d_logits || !d_topv || !d_topi || !d_lse) return fail(NT_E_INVALID, "null argument to nt_op_select_tiled");
+  if (rows < 0 || V <= 0) return fail(NT_E_INVALID, "rows must be >= 0 and V > 0");
+  if (k < 1 || k > 32 || k > V) return fail(NT_E_UNSUPPORTED, "k must be in [1, min(32, V)]");
+  if (V > 65536) return fail(NT_E_UNSUPPORTED, "V > 65536");
+  if (rows == 0) return NT_OK;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int n_tiles = (V + 127) / 128;
+  float* part = nullptr;
+  NT_HIP(hipMalloc((void**)&part, (size_t)rows * n_tiles * nt::topk_record(1) * sizeof(float)));
+  hipError_t e = nt::tile_records(d_logits, rows, V, part, s);
+  if (e == hipSuccess) e = nt::beam_select_tiles(part, n_tiles, d_logits, nullptr, 1, rows, V, k, d_topv, d_topi, d_lse, s);
+  const hipError_t se = hipStreamSynchronize(s);   // the records buffer is freed below
+  (void)hipFree(part);
+  NT_HIP(e);
+  NT_HIP(se);
   return NT_OK;
 }
 

@@ -488,6 +488,172 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const floa
   }
 }
 
+// Beam selection from the output projection's per-tile records.  The projection's
+// epilogue leaves, for every row and 128-column tile, the tile row's (max, sum of
+// exp(x - max)); the logits are written as well.  Let tau be the k2-th largest of a row's
+// tile maxima.  Every logit among the row's k2 largest lies in a tile whose maximum is at
+// least tau: a logit x in a tile of maximum below tau is smaller than at least k2 logits
+// (one per tile of maximum >= tau).  Equal values are covered too: a tile whose maximum
+// is below tau holds nothing equal to the k2-th largest logit, which is >= tau.  So only
+// the candidate tiles are read back -- usually k2 of them -- and the log-sum-exp comes
+// from merging the records.  One wave per row; the result equals a scan of the whole row
+// in (value desc, index asc) order.
+constexpr int TILE_COLS = 128;
+constexpr int SEL_TPL = 8;          // tile records per lane: up to 512 tiles (V <= 65536)
+constexpr int SEL_CAND = 16;        // candidate tiles read in one batch
+
+template <int K2>
+__global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __restrict__ part, int n_tiles,
+                                                                const float* __restrict__ logits,
+                                                                const int* __restrict__ ctl, int beam, int rows,
+                                                                int V, int k2, float* __restrict__ topv,
+                                                                int* __restrict__ topi,
+                                                                float* __restrict__ lse_out) {
+  constexpr int REC = 4;            // record floats (max, sum, best value, best index)
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int r = blockIdx.x * 4 + wave;
+  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
+  if (r >= live) return;            // whole wave; no block barrier below
+  const float* rec = part + (size_t)r * n_tiles * REC;
+  // the lane's tile maxima, and the row's (max, sum) merged over every record
+  float tm[SEL_TPL];
+  MaxSum acc{-INFINITY, 0.f};
+#pragma unroll
+  for (int j = 0; j < SEL_TPL; ++j) {
+    const int t = lane + j * kWave;
+    const float* q = rec + (size_t)min(t, n_tiles - 1) * REC;
+    const float mx = q[0], sm = q[1];
+    tm[j] = t < n_tiles ? mx : -INFINITY;
+    if (t < n_tiles) acc = ms_merge(acc, MaxSum{mx, sm});
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  // tau: k2 rounds of a wave max over the tile maxima, each winner giving up that entry
+  float tau = -INFINITY;
+  {
+    float rest[SEL_TPL];
+#pragma unroll
+    for (int j = 0; j < SEL_TPL; ++j) rest[j] = tm[j];
+    for (int round = 0; round < k2; ++round) {
+      float mine = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < SEL_TPL; ++j) mine = fmaxf(mine, rest[j]);
+      float best = mine;
+      int bl = lane;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(best, o, kWave);
+        const int ol = __shfl_xor(bl, o, kWave);
+        if (ov > best || (ov == best && ol < bl)) { best = ov; bl = ol; }
+      }
+      tau = best;
+      if (lane == bl) {
+        bool gone = false;
+#pragma unroll
+        for (int j = 0; j < SEL_TPL; ++j)
+          if (!gone && rest[j] == best) { rest[j] = -INFINITY; gone = true; }
+      }
+    }
+  }
+  // candidate tiles in increasing order, read SEL_CAND at a time with every load issued
+  // before any use; each lane inserts its columns in increasing index order
+  float v[K2];
+  int ix[K2];
+#pragma unroll
+  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
+  const float* row = logits + (size_t)r * V;
+  int j = 0;
+  unsigned long long mask = __ballot(lane < n_tiles && tm[0] >= tau);
+  bool more = true;
+  while (more) {
+    int ct[SEL_CAND];
+#pragma unroll
+    for (int c = 0; c < SEL_CAND; ++c) {
+      ct[c] = -1;
+      while (more && mask == 0) {
+        if (++j >= SEL_TPL) {
+          more = false;
+        } else {
+          float tj = -INFINITY;
+#pragma unroll
+          for (int q = 0; q < SEL_TPL; ++q) tj = q == j ? tm[q] : tj;
+          mask = __ballot(lane + j * kWave < n_tiles && tj >= tau);
+        }
+      }
+      if (more) {
+        const int l = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        ct[c] = l + j * kWave;
+      }
+    }
+    float xs[SEL_CAND][2];
+#pragma unroll
+    for (int c = 0; c < SEL_CAND; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int n = ct[c] * TILE_COLS + h * kWave + lane;
+        const bool ok = ct[c] >= 0 && n < V;
+        const float x = row[ok ? n : 0];
+        xs[c][h] = ok ? x : -INFINITY;
+      }
+#pragma unroll
+    for (int c = 0; c < SEL_CAND; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float x = xs[c][h];
+        if (x >= tau) list_insert<K2>(v, ix, x, ct[c] * TILE_COLS + h * kWave + lane);
+      }
+  }
+  // k2 rounds of a (value desc, index asc) wave argmax
+  for (int round = 0; round < k2; ++round) {
+    float bv = v[0];
+    int bi = ix[0];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, kWave);
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (better(ov, oi, bv, bi) || (bi == INT_MAX && oi != INT_MAX)) { bv = ov; bi = oi; }
+    }
+    if (lane == 0) {
+      topv[(size_t)r * k2 + round] = bi == INT_MAX ? -INFINITY : bv;
+      topi[(size_t)r * k2 + round] = bi;
+    }
+    if (ix[0] == bi && bi != INT_MAX) {
+#pragma unroll
+      for (int q = 0; q < K2 - 1; ++q) { v[q] = v[q + 1]; ix[q] = ix[q + 1]; }
+      v[K2 - 1] = -INFINITY;
+      ix[K2 - 1] = INT_MAX;
+    }
+  }
+  if (lane == 0) lse_out[r] = acc.m + logf(acc.s);
+}
+
+// The per-tile records of a logits matrix, as the projection's epilogue forms them: one
+// wave per (row, tile), (max, sum of exp(x - max)) over the tile's columns.  For tests.
+__global__ __launch_bounds__(256) void tile_records_kernel(const float* __restrict__ logits, int rows, int V,
+                                                           int n_tiles, float* __restrict__ part) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const long long task = (long long)blockIdx.x * 4 + wave;
+  if (task >= (long long)rows * n_tiles) return;
+  const int r = (int)(task / n_tiles), t = (int)(task % n_tiles);
+  MaxSum acc{-INFINITY, 0.f};
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int n = t * TILE_COLS + h * kWave + lane;
+    const float x = n < V ? logits[(size_t)r * V + n] : -INFINITY;
+    if (x != -INFINITY) acc = ms_merge(acc, MaxSum{x, 1.f});
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  if (lane == 0) {
+    float* q = part + ((size_t)r * n_tiles + t) * 4;
+    q[0] = acc.m;
+    q[1] = acc.s;
+    q[2] = acc.m;
+    q[3] = 0.f;
+  }
+}
+
 // ---- beam: per-sentence update (one wave per live sentence) ----------------------------
 constexpr int MAXC = 8;       // candidates per lane: K * 2K <= 512 = 64 * 8
 
@@ -789,6 +955,30 @@ hipError_t beam_select(const float* logits, const int* ctl, int beam, int rows, 
   else if (k2 <= 32) NT_SEL(32);
   else return hipErrorInvalidValue;
 #undef NT_SEL
+  return hipGetLastError();
+}
+
+hipError_t beam_select_tiles(const float* part, int n_tiles, const float* logits, const int* ctl, int beam, int rows,
+                             int V, int k2, float* topv, int* topi, float* lse, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (n_tiles != (V + TILE_COLS - 1) / TILE_COLS || n_tiles > SEL_TPL * kWave || k2 < 1 || k2 > 32 || k2 > V)
+    return hipErrorInvalidValue;
+  const dim3 grid((rows + 3) / 4);
+#define NT_SEL(K2) \
+  NT_LAUNCH(beam_select_tiles_kernel<K2>, grid, dim3(256), 0, s, part, n_tiles, logits, ctl, beam, rows, V, k2, topv, topi, lse)
+  if (k2 <= 4) NT_SEL(4);
+  else if (k2 <= 8) NT_SEL(8);
+  else if (k2 <= 16) NT_SEL(16);
+  else NT_SEL(32);
+#undef NT_SEL
+  return hipGetLastError();
+}
+
+hipError_t tile_records(const float* logits, int rows, int V, float* part, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int n_tiles = (V + TILE_COLS - 1) / TILE_COLS;
+  const long long tasks = (long long)rows * n_tiles;
+  NT_LAUNCH(tile_records_kernel, dim3((unsigned)((tasks + 3) / 4)), dim3(256), 0, s, logits, rows, V, n_tiles, part);
   return hipGetLastError();
 }
 

@@ -1,9 +1,13 @@
 """GPU: the beam step's selection (top-k logits in (value desc, index asc) order plus the
-row's log-sum-exp) through nt_op_select, against NumPy.
+row's log-sum-exp) against NumPy, through nt_op_select (a scan of the whole row) and
+nt_op_select_tiled (from per-128-column-tile records, reading back only the tiles that
+can hold one of the k largest).
 
 Covers the register-resident kernel (V % 4 == 0, V <= 32768) and the streaming kernel
-(other V), heavy ties (values drawn from a few integers, equal rows), a row whose maximum
-is its last logit, -inf logits (never selected) and k up to 32.
+(other V), heavy ties (values drawn from a few integers, equal rows -- many tiles then
+share the k-th largest maximum), a row whose maximum is its last logit, -inf logits
+(never selected; whole tiles of -inf), V below one tile and not a multiple of it, and k
+up to 32.
 """
 import numpy as np
 import pytest
@@ -29,7 +33,7 @@ def _expected(x, k):
     return np.array(vals), np.array(idxs), lse
 
 
-def _run(x, k):
+def _run(x, k, entry="nt_op_select"):
     import torch
     from paper_2109_08008_amd import nt
     rows, V = x.shape
@@ -37,7 +41,7 @@ def _run(x, k):
     tv = torch.empty(rows, k, dtype=torch.float32, device="cuda")
     ti = torch.empty(rows, k, dtype=torch.int32, device="cuda")
     ls = torch.empty(rows, dtype=torch.float32, device="cuda")
-    nt.nt_op_select(dx.data_ptr(), rows, V, k, tv.data_ptr(), ti.data_ptr(), ls.data_ptr())
+    getattr(nt, entry)(dx.data_ptr(), rows, V, k, tv.data_ptr(), ti.data_ptr(), ls.data_ptr())
     torch.cuda.synchronize()
     return tv.cpu().numpy(), ti.cpu().numpy().astype(np.int64), ls.cpu().numpy()
 
@@ -58,15 +62,16 @@ def _logits(V, rows, kind, seed):
     return x
 
 
+@pytest.mark.parametrize("entry", ["nt_op_select", "nt_op_select_tiled"])
 @pytest.mark.parametrize("V", [7, 101, 1000, 4096, 32000, 40000])
 @pytest.mark.parametrize("kind", ["normal", "ties", "rows"])
-def test_select_matches_numpy(V, kind):
+def test_select_matches_numpy(V, kind, entry):
     rows = 12
     x = _logits(V, rows, kind, seed=V + len(kind))
     for k in (1, 4, 8) + ((16, 32) if V >= 32 else ()):
         if k > V:
             continue
-        tv, ti, ls = _run(x, k)
+        tv, ti, ls = _run(x, k, entry)
         ev, ei, el = _expected(x, k)
         np.testing.assert_array_equal(ti, ei, err_msg=f"k={k}")
         np.testing.assert_array_equal(tv, ev, err_msg=f"k={k}")
