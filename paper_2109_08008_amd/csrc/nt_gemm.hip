@@ -257,9 +257,10 @@ template <> struct LdsWait<4, 4> {
 // Fused selection epilogue: the rows of an LDS-staged fp32 tile (ER rows x BN columns,
 // row stride CS) are reduced to one partial record per row -- running max, sum of
 // exp(x - max), and the k2 largest (value, index) in (value desc, index asc) order.
-// TPR consecutive lanes share a row; each scans a contiguous run of columns.  K2 = 0
-// leaves only (max, sum), in two branch-free passes (the max, then one exponential per
-// logit), for beam search, which reads its candidates back from the stored logits.
+// TPR consecutive lanes share a row; each scans a contiguous run of columns.  K2 <= 1
+// takes two passes, the max (and, for K2 = 1, the lowest column holding it, which is the
+// k2 = 1 record's best entry) and then one exponential per logit: K2 = 0 for beam search,
+// which reads its candidates back from the stored logits, K2 = 1 for greedy.
 __device__ __forceinline__ bool topk_better(float v1, int i1, float v2, int i2) {
   return v1 > v2 || (v1 == v2 && i1 < i2);
 }
@@ -271,16 +272,33 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
   static_assert(TPR >= 1 && TPR <= kWave && (TPR & (TPR - 1)) == 0, "row group inside a wave");
   const int row = threadIdx.x / TPR, sub = threadIdx.x % TPR;
   const int m = mrow0 + row;
-  if constexpr (K2 == 0) {
+  if constexpr (K2 <= 1) {
     float mx = -INFINITY;
+    int bi = INT_MAX;   // lowest column holding mx (K2 = 1)
     for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
       const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
       const float xs[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, n0 + g4 * 4 + u < N ? xs[u] : -INFINITY);
+      for (int u = 0; u < 4; ++u) {
+        const int n = n0 + g4 * 4 + u;
+        const float x = n < N ? xs[u] : -INFINITY;
+        if constexpr (K2 == 1) {
+          if (x > mx) { mx = x; bi = n; }   // columns rise within a lane: ties keep the lowest
+        } else {
+          mx = fmaxf(mx, x);
+        }
+      }
     }
 #pragma unroll
-    for (int o = TPR / 2; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+    for (int o = TPR / 2; o > 0; o >>= 1) {
+      const float om = __shfl_xor(mx, o, kWave);
+      if constexpr (K2 == 1) {
+        const int oi = __shfl_xor(bi, o, kWave);
+        if (topk_better(om, oi, mx, bi)) { mx = om; bi = oi; }
+      } else {
+        mx = fmaxf(mx, om);
+      }
+    }
     float sum = 0.f;
     if (mx != -INFINITY) {
       for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
@@ -296,6 +314,10 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
       float* rec = e.part + ((size_t)m * e.n_tiles + tn) * topk_record(e.k2);
       rec[0] = mx;
       rec[1] = sum;
+      if constexpr (K2 == 1) {
+        rec[2] = mx;
+        rec[3] = __int_as_float(bi);
+      }
     }
   } else {
   float mx = -INFINITY, sum = 0.f;
