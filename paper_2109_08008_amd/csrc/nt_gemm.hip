@@ -255,12 +255,11 @@ template <> struct LdsWait<4, 4> {
 };
 
 // Fused selection epilogue: the rows of an LDS-staged fp32 tile (ER rows x BN columns,
-// row stride CS) are reduced to one partial record per row -- running max, sum of
-// exp(x - max), and the k2 largest (value, index) in (value desc, index asc) order.
-// TPR consecutive lanes share a row; each scans a contiguous run of columns.  K2 <= 1
-// takes two passes, the max (and, for K2 = 1, the lowest column holding it, which is the
-// k2 = 1 record's best entry) and then one exponential per logit: K2 = 0 for beam search,
-// which reads its candidates back from the stored logits, K2 = 1 for greedy.
+// row stride CS) are reduced to one record per row: the max, the sum of exp(x - max),
+// and for K2 = 1 the best (value, column) -- the max at its lowest column.  TPR
+// consecutive lanes share a row; each scans its columns in increasing order.  Two
+// passes: the max (and its column), then one exponential per logit.  K2 = 0 serves beam
+// search, which reads its candidates back from the stored logits; K2 = 1 serves greedy.
 __device__ __forceinline__ bool topk_better(float v1, int i1, float v2, int i2) {
   return v1 > v2 || (v1 == v2 && i1 < i2);
 }
@@ -268,11 +267,12 @@ __device__ __forceinline__ bool topk_better(float v1, int i1, float v2, int i2) 
 template <int ER, int BN_, int K2>
 __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow0, int n0, int M, int N, int tn,
                                                const GemmEpi& e) {
+  static_assert(K2 == 0 || K2 == 1, "records carry at most the best entry");
   constexpr int TPR = NTHR / ER;            // threads per row (2, 4 or 8)
   static_assert(TPR >= 1 && TPR <= kWave && (TPR & (TPR - 1)) == 0, "row group inside a wave");
   const int row = threadIdx.x / TPR, sub = threadIdx.x % TPR;
   const int m = mrow0 + row;
-  if constexpr (K2 <= 1) {
+  {
     float mx = -INFINITY;
     int bi = INT_MAX;   // lowest column holding mx (K2 = 1)
     for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
@@ -319,77 +319,6 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
         rec[3] = __int_as_float(bi);
       }
     }
-  } else {
-  float mx = -INFINITY, sum = 0.f;
-  float v[K2];
-  int ix[K2];
-#pragma unroll
-  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
-  // lanes of a row interleave by groups of 4 columns (16-byte LDS reads, spread banks);
-  // each lane still visits its columns in increasing order
-  for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
-    const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
-    const float xs[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int n = n0 + g4 * 4 + u;
-      const float x = n < N ? xs[u] : -INFINITY;
-      if (x > mx) {
-        sum = mx == -INFINITY ? 0.f : sum * __expf(mx - x);
-        mx = x;
-      }
-      if (n < N) sum += __expf(x - mx);
-      if (x > v[K2 - 1]) {                     // sorted insert; equal values keep the lower index
-        v[K2 - 1] = x;
-        ix[K2 - 1] = n;
-#pragma unroll
-        for (int j = K2 - 1; j > 0; --j)
-          if (v[j] > v[j - 1]) {
-            const float tv = v[j]; v[j] = v[j - 1]; v[j - 1] = tv;
-            const int ti = ix[j]; ix[j] = ix[j - 1]; ix[j - 1] = ti;
-          }
-      }
-    }
-  }
-  // (max, sum) over the TPR lanes of the row
-#pragma unroll
-  for (int o = TPR / 2; o > 0; o >>= 1) {
-    const float om = __shfl_xor(mx, o, kWave), os = __shfl_xor(sum, o, kWave);
-    if (om != -INFINITY) {
-      if (mx == -INFINITY) { mx = om; sum = os; }
-      else {
-        const float nm = fmaxf(mx, om);
-        sum = sum * __expf(mx - nm) + os * __expf(om - nm);
-        mx = nm;
-      }
-    }
-  }
-  float* rec = e.part + ((size_t)m * e.n_tiles + tn) * topk_record(e.k2);
-  if (sub == 0 && m < M) {
-    rec[0] = mx;
-    rec[1] = sum;
-  }
-  // k2 rounds of a group argmax; the winning lane drops its head
-  for (int r = 0; r < K2 && r < e.k2; ++r) {
-    float bv = v[0];
-    int bi = ix[0];
-#pragma unroll
-    for (int o = TPR / 2; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
-      if (topk_better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
-    if (sub == 0 && m < M) {
-      rec[2 + 2 * r] = bv;
-      rec[3 + 2 * r] = __int_as_float(bi);
-    }
-    if (ix[0] == bi && bi != INT_MAX) {
-#pragma unroll
-      for (int j = 0; j < K2 - 1; ++j) { v[j] = v[j + 1]; ix[j] = ix[j + 1]; }
-      v[K2 - 1] = -INFINITY;
-      ix[K2 - 1] = INT_MAX;
-    }
-  }
   }
 }
 

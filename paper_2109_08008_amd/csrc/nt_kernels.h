@@ -87,7 +87,8 @@ struct GemmEpi {
   const float* wscale = nullptr;
   // EPI_TOPK (the launch uses 128x128 tiles, so n_tiles = ceil(N / 128))
   float* part = nullptr;           // [M][n_tiles][topk_record(k2)]
-  int k2 = 1;
+  int k2 = 1;                      // record layout: 1 (max, sum, best value, best column); the
+                                   //   projection fills the best entry for greedy only
   int n_tiles = 0;
 };
 
