@@ -47,8 +47,8 @@ GEMM_CLASSES = (0, 1, 2)
 TRAFFIC = {
     ("gemm_dec", "base-6-6"): {
         "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
-        "sha256": "c8b52c9ce80222020192c3640342ad29464086578794c4c265df341d8715af2d",
-        "fetch_kib": 3913.77, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
+        "sha256": "892c50410868408773fd04b4ec18f090e0dfe2dfe811046840f65b57af130d3a",
+        "fetch_kib": 3913.94, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 
