@@ -500,7 +500,6 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const floa
 // in (value desc, index asc) order.
 constexpr int TILE_COLS = 128;
 constexpr int SEL_TPL = 8;          // tile records per lane: up to 512 tiles (V <= 65536)
-constexpr int SEL_CAND = 16;        // candidate tiles read in one batch
 
 template <int K2>
 __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __restrict__ part, int n_tiles,
@@ -510,6 +509,7 @@ __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __r
                                                                 int* __restrict__ topi,
                                                                 float* __restrict__ lse_out) {
   constexpr int REC = 4;            // record floats (max, sum, best value, best index)
+  constexpr int SEL_CAND = K2 < 8 ? 8 : K2 > 16 ? 16 : K2;   // candidate tiles per batch (usually all)
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int r = blockIdx.x * 4 + wave;
   const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
