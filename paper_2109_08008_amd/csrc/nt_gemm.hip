@@ -272,52 +272,50 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
   static_assert(TPR >= 1 && TPR <= kWave && (TPR & (TPR - 1)) == 0, "row group inside a wave");
   const int row = threadIdx.x / TPR, sub = threadIdx.x % TPR;
   const int m = mrow0 + row;
-  {
-    float mx = -INFINITY;
-    int bi = INT_MAX;   // lowest column holding mx (K2 = 1)
+  float mx = -INFINITY;
+  int bi = INT_MAX;   // lowest column holding mx (K2 = 1)
+  for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
+    const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
+    const float xs[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int n = n0 + g4 * 4 + u;
+      const float x = n < N ? xs[u] : -INFINITY;
+      if constexpr (K2 == 1) {
+        if (x > mx) { mx = x; bi = n; }   // columns rise within a lane: ties keep the lowest
+      } else {
+        mx = fmaxf(mx, x);
+      }
+    }
+  }
+#pragma unroll
+  for (int o = TPR / 2; o > 0; o >>= 1) {
+    const float om = __shfl_xor(mx, o, kWave);
+    if constexpr (K2 == 1) {
+      const int oi = __shfl_xor(bi, o, kWave);
+      if (topk_better(om, oi, mx, bi)) { mx = om; bi = oi; }
+    } else {
+      mx = fmaxf(mx, om);
+    }
+  }
+  float sum = 0.f;
+  if (mx != -INFINITY) {
     for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
       const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
       const float xs[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int n = n0 + g4 * 4 + u;
-        const float x = n < N ? xs[u] : -INFINITY;
-        if constexpr (K2 == 1) {
-          if (x > mx) { mx = x; bi = n; }   // columns rise within a lane: ties keep the lowest
-        } else {
-          mx = fmaxf(mx, x);
-        }
-      }
+      for (int u = 0; u < 4; ++u) sum += __expf((n0 + g4 * 4 + u < N ? xs[u] : -INFINITY) - mx);
     }
+  }
 #pragma unroll
-    for (int o = TPR / 2; o > 0; o >>= 1) {
-      const float om = __shfl_xor(mx, o, kWave);
-      if constexpr (K2 == 1) {
-        const int oi = __shfl_xor(bi, o, kWave);
-        if (topk_better(om, oi, mx, bi)) { mx = om; bi = oi; }
-      } else {
-        mx = fmaxf(mx, om);
-      }
-    }
-    float sum = 0.f;
-    if (mx != -INFINITY) {
-      for (int g4 = sub; g4 < BN_ / 4; g4 += TPR) {
-        const float4 q = *reinterpret_cast<const float4*>(&cs[row * CS + g4 * 4]);
-        const float xs[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) sum += __expf((n0 + g4 * 4 + u < N ? xs[u] : -INFINITY) - mx);
-      }
-    }
-#pragma unroll
-    for (int o = TPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, kWave);
-    if (sub == 0 && m < M) {
-      float* rec = e.part + ((size_t)m * e.n_tiles + tn) * topk_record(e.k2);
-      rec[0] = mx;
-      rec[1] = sum;
-      if constexpr (K2 == 1) {
-        rec[2] = mx;
-        rec[3] = __int_as_float(bi);
-      }
+  for (int o = TPR / 2; o > 0; o >>= 1) sum += __shfl_xor(sum, o, kWave);
+  if (sub == 0 && m < M) {
+    float* rec = e.part + ((size_t)m * e.n_tiles + tn) * topk_record(e.k2);
+    rec[0] = mx;
+    rec[1] = sum;
+    if constexpr (K2 == 1) {
+      rec[2] = mx;
+      rec[3] = __int_as_float(bi);
     }
   }
 }
