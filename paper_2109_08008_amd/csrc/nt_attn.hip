@@ -295,14 +295,16 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
 // With one query this is a stream over the cache, kept on the vector units and laid out
 // for coalescing: the CPR = 16-byte chunks of a key's row sit on CPR consecutive lanes,
 // so one load instruction of the wave reads whole rows (8 keys of 128 bytes at d_head
-// 64).  Each lane carries KPL = 8 keys of a chunk of GPW * KPL keys (lane group g holds
-// keys g*KPL .. g*KPL+7).  A key's score is its lanes' partial dot products summed by a
+// 64).  Each lane carries KPL = 4 keys of a chunk of GPW * KPL keys (lane group g holds
+// keys g*KPL .. g*KPL+3).  A key's score is its lanes' partial dot products summed by a
 // butterfly inside the group; P.V accumulates per lane over its keys for its 16-byte
 // slice of channels and is summed over the lane groups once, after the last chunk.  The
-// softmax is online across chunks, in fp32.  No LDS, so occupancy is set by registers.
+// softmax is online across chunks, in fp32.  No LDS, so occupancy is set by registers:
+// four keys a lane (80 VGPRs at fp16, six waves a SIMD) measured 4% faster on base-6-6
+// than eight (91 VGPRs, five waves), and two (66 VGPRs) no faster than four.
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
-  constexpr int VEC = Vec<T>::N, CPR = DH / VEC, GPW = kWave / CPR, KPL = 8, KCH = GPW * KPL;
+  constexpr int VEC = Vec<T>::N, CPR = DH / VEC, GPW = kWave / CPR, KPL = 4, KCH = GPW * KPL;
   static_assert(CPR >= 1 && CPR <= kWave && (CPR & (CPR - 1)) == 0, "a key's chunks fit in a wave");
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int pair = blockIdx.x * 4 + wave;
