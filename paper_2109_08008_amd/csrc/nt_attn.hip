@@ -354,8 +354,12 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
       float dot = 0.f;
 #pragma unroll
       for (int x = 0; x < VEC; ++x) dot += q[x] * to_f32(ke[x]);
-#pragma unroll
-      for (int ofs = 1; ofs < CPR; ofs <<= 1) dot += __shfl_xor(dot, ofs, kWave);
+      if constexpr (CPR <= 16) {
+        dot = group_sum<CPR>(dot);
+      } else {
+        dot = group_sum<16>(dot);
+        dot += __shfl_xor(dot, 16, kWave);
+      }
       sc[j] = c0 + g * KPL + j < n ? dot : -INFINITY;
       cmax = fmaxf(cmax, sc[j]);
     }
@@ -378,7 +382,7 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
 #pragma unroll
   for (int ofs = CPR; ofs < kWave; ofs <<= 1)
 #pragma unroll
-    for (int x = 0; x < VEC; ++x) o[x] += __shfl_xor(o[x], ofs, kWave);
+    for (int x = 0; x < VEC; ++x) o[x] += ofs == 8 ? dpp_mov<DPP_XOR8>(o[x]) : __shfl_xor(o[x], ofs, kWave);
   const float inv = 1.0f / wave_sum(lsum);
   if (g == 0) {
 #pragma unroll

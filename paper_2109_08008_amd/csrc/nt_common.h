@@ -92,24 +92,74 @@ __device__ __forceinline__ void store_row(T* p, const float* in) {
   }
 }
 
-// Butterfly reductions: every lane ends with the same bits (each step adds a pair that
-// its partner adds in the other order, and fp addition is commutative).
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+// Whole-wave reductions without an LDS round trip per step.  Inside each row of 16
+// lanes four DPP butterfly steps: lane^1 and lane^2 by quad permutes, then the mirrored
+// half of each 8 and of each 16 lanes, which after the earlier steps holds the partial of
+// lane^4 and lane^8.  The four row results are then read as scalars and combined as
+// (r0 op r1) op (r2 op r3).  Each step pairs partials symmetrically and fp addition is
+// commutative, so every lane ends with the same bits: the xor butterfly's result taken
+// over the offsets 1, 2, ..., 32 in that order.  All 64 lanes must be active (every
+// caller reduces across a whole wave).
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp_mov_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ float readlane_f(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+__device__ __forceinline__ int readlane_i(int v, int lane) { return __builtin_amdgcn_readlane(v, lane); }
+constexpr int DPP_XOR1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141;  // lane 7-j of each 8
+constexpr int DPP_MIRROR = 0x140;       // lane 15-j of each 16
+constexpr int DPP_XOR8 = 0x128;         // row_ror:8, lane j^8 of each 16
+// Sum over aligned groups of N consecutive lanes (N = 1, 2, 4, 8 or 16), by the same
+// steps: every lane of a group ends with the group's sum, the xor butterfly's bits.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16, "a power-of-two group inside a row");
+  if constexpr (N >= 2) v += dpp_mov<DPP_XOR1>(v);
+  if constexpr (N >= 4) v += dpp_mov<DPP_XOR2>(v);
+  if constexpr (N >= 8) v += dpp_mov<DPP_HALF_MIRROR>(v);
+  if constexpr (N >= 16) v += dpp_mov<DPP_MIRROR>(v);
   return v;
 }
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_mov<DPP_XOR1>(v);
+  v += dpp_mov<DPP_XOR2>(v);
+  v += dpp_mov<DPP_HALF_MIRROR>(v);
+  v += dpp_mov<DPP_MIRROR>(v);
+  return (readlane_f(v, 0) + readlane_f(v, 16)) + (readlane_f(v, 32) + readlane_f(v, 48));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+  v = fmaxf(v, dpp_mov<DPP_XOR1>(v));
+  v = fmaxf(v, dpp_mov<DPP_XOR2>(v));
+  v = fmaxf(v, dpp_mov<DPP_HALF_MIRROR>(v));
+  v = fmaxf(v, dpp_mov<DPP_MIRROR>(v));
+  return fmaxf(fmaxf(readlane_f(v, 0), readlane_f(v, 16)), fmaxf(readlane_f(v, 32), readlane_f(v, 48)));
 }
 
 // LayerNorm of one row held as EPL fp32 values per lane (row length 64*EPL):
 // biased variance, two passes over registers, fp32 throughout.
 template <int EPL>
-__device__ __forceinline__ void wave_layernorm(const float* x, float* y, const float* gamma,
-                                               const float* beta, int col0, float inv_d, float eps) {
+struct LnCols {   // the lane's gain and bias columns
+  float g[EPL], b[EPL];
+};
+template <int EPL>
+__device__ __forceinline__ void load_ln_cols(const float* gamma, const float* beta, int col0, LnCols<EPL>& c) {
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) {
+    c.g[i] = gamma[col0 + i];
+    c.b[i] = beta[col0 + i];
+  }
+}
+template <int EPL>
+__device__ __forceinline__ void wave_layernorm(const float* x, float* y, const LnCols<EPL>& c, float inv_d,
+                                               float eps) {
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) s += x[i];
@@ -123,7 +173,15 @@ __device__ __forceinline__ void wave_layernorm(const float* x, float* y, const f
   const float var = wave_sum(q) * inv_d;
   const float rstd = 1.0f / sqrtf(var + eps);
 #pragma unroll
-  for (int i = 0; i < EPL; ++i) y[i] = (x[i] - mean) * rstd * gamma[col0 + i] + beta[col0 + i];
+  for (int i = 0; i < EPL; ++i) y[i] = (x[i] - mean) * rstd * c.g[i] + c.b[i];
+}
+// The same with the gain and bias read at the call (their loads overlap the reductions).
+template <int EPL>
+__device__ __forceinline__ void wave_layernorm(const float* x, float* y, const float* gamma,
+                                               const float* beta, int col0, float inv_d, float eps) {
+  LnCols<EPL> c;
+  load_ln_cols<EPL>(gamma, beta, col0, c);
+  wave_layernorm<EPL>(x, y, c, inv_d, eps);
 }
 
 }  // namespace nt

@@ -136,12 +136,14 @@ __global__ __launch_bounds__(256) void ln_kernel(const T* __restrict__ x, const 
                                                  T* __restrict__ y, int rows, int d, float eps, const int* ctl,
                                                  int ctl_rows) {
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
+  const int c0 = (threadIdx.x % kWave) * EPL;
+  LnCols<EPL> lc;   // row-independent: in flight with the live-row count
+  load_ln_cols<EPL>(ln, ln + d, c0, lc);
   if (ctl) rows = min(rows, ctl[CTL_NLIVE] * ctl_rows);
   if (row >= rows) return;
-  const int c0 = (threadIdx.x % kWave) * EPL;
   float v[EPL], o[EPL];
   load_row<T, EPL>(x + (size_t)row * d + c0, v);
-  wave_layernorm<EPL>(v, o, ln, ln + d, c0, 1.0f / (float)d, eps);
+  wave_layernorm<EPL>(v, o, lc, 1.0f / (float)d, eps);
   store_row<T, EPL>(y + (size_t)row * d + c0, o);
 }
 
@@ -154,9 +156,11 @@ __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ 
                                                         const float* __restrict__ ln, T* __restrict__ z,
                                                         T* __restrict__ u, int rows, int d, float eps) {
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
+  const int c0 = (threadIdx.x % kWave) * EPL;
+  LnCols<EPL> lc;
+  load_ln_cols<EPL>(ln, ln + d, c0, lc);
   if (row >= min(rows, ctl[CTL_NLIVE] * beam)) return;
   const int t = ctl[CTL_T];
-  const int c0 = (threadIdx.x % kWave) * EPL;
   const int p = sent_list[row / beam] * beam + row % beam;
   float v[EPL], o[EPL];
   load_row<T, EPL>(E + (size_t)cur_tok[p] * d + c0, v);
@@ -164,7 +168,7 @@ __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ 
 #pragma unroll
   for (int i = 0; i < EPL; ++i) v[i] = to_f32(from_f32<T>(scale * v[i] + pr[i]));
   store_row<T, EPL>(z + (size_t)row * d + c0, v);
-  wave_layernorm<EPL>(v, o, ln, ln + d, c0, 1.0f / (float)d, eps);
+  wave_layernorm<EPL>(v, o, lc, 1.0f / (float)d, eps);
   store_row<T, EPL>(u + (size_t)row * d + c0, o);
 }
 

@@ -37,6 +37,55 @@ __device__ __forceinline__ bool better(float v1, int i1, float v2, int i2) {
   return v1 > v2 || (v1 == v2 && i1 < i2);
 }
 
+// Whole-wave reductions on the DPP network, by the steps of wave_sum.  wave_best keeps
+// the best entry under (value desc, index asc) with empty entries (index INT_MAX) last, a
+// strict total order, so its result does not depend on the order of the steps;
+// ms_merge is symmetric in its operands, so both lanes of a pair hold the same bits after
+// each step of wave_ms.  Every lane returns the wave's result; all 64 must be active.
+__device__ __forceinline__ bool takes(float ov, int oi, float v, int i) {
+  return oi != INT_MAX && (i == INT_MAX || better(ov, oi, v, i));
+}
+template <int CTRL>
+__device__ __forceinline__ void best_step(float& v, int& i, float& p) {
+  const float ov = dpp_mov<CTRL>(v), op = dpp_mov<CTRL>(p);
+  const int oi = dpp_mov_i<CTRL>(i);
+  if (takes(ov, oi, v, i)) { v = ov; i = oi; p = op; }
+}
+__device__ __forceinline__ void wave_best(float& v, int& i, float& p) {
+  best_step<DPP_XOR1>(v, i, p);
+  best_step<DPP_XOR2>(v, i, p);
+  best_step<DPP_HALF_MIRROR>(v, i, p);
+  best_step<DPP_MIRROR>(v, i, p);
+  float bv = readlane_f(v, 0), bp = readlane_f(p, 0);
+  int bi = readlane_i(i, 0);
+#pragma unroll
+  for (int r = 1; r < 4; ++r) {
+    const float rv = readlane_f(v, 16 * r), rp = readlane_f(p, 16 * r);
+    const int ri = readlane_i(i, 16 * r);
+    if (takes(rv, ri, bv, bi)) { bv = rv; bi = ri; bp = rp; }
+  }
+  v = bv;
+  i = bi;
+  p = bp;
+}
+__device__ __forceinline__ void wave_best(float& v, int& i) {
+  float p = 0.f;   // no payload: the compiler drops its moves
+  wave_best(v, i, p);
+}
+template <int CTRL>
+__device__ __forceinline__ MaxSum ms_step(MaxSum a) {
+  return ms_merge(a, MaxSum{dpp_mov<CTRL>(a.m), dpp_mov<CTRL>(a.s)});
+}
+__device__ __forceinline__ MaxSum wave_ms(MaxSum a) {
+  a = ms_step<DPP_XOR1>(a);
+  a = ms_step<DPP_XOR2>(a);
+  a = ms_step<DPP_HALF_MIRROR>(a);
+  a = ms_step<DPP_MIRROR>(a);
+  const MaxSum r0{readlane_f(a.m, 0), readlane_f(a.s, 0)}, r1{readlane_f(a.m, 16), readlane_f(a.s, 16)};
+  const MaxSum r2{readlane_f(a.m, 32), readlane_f(a.s, 32)}, r3{readlane_f(a.m, 48), readlane_f(a.s, 48)};
+  return ms_merge(ms_merge(r0, r1), ms_merge(r2, r3));
+}
+
 // Per-thread online max/sum and argmax over a row; returns block-wide results in
 // every thread.  Elements are visited in increasing index per thread.
 __device__ void row_lse_argmax(const float* __restrict__ x, int V, float& lse, float& best, int& bidx) {
@@ -74,14 +123,8 @@ __device__ void row_lse_argmax(const float* __restrict__ x, int V, float& lse, f
     }
   }
   // wave reduction
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    MaxSum other{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)};
-    acc = ms_merge(acc, other);
-    const float ov = __shfl_xor(bv, o, kWave);
-    const int oi = __shfl_xor(bi, o, kWave);
-    if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-  }
+  acc = wave_ms(acc);
+  wave_best(bv, bi);
   const int wave = tid / kWave, lane = tid % kWave;
   if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; sb[wave] = bv; si[wave] = bi; }
   __syncthreads();
@@ -197,13 +240,8 @@ __global__ __launch_bounds__(SEL_THREADS) void greedy_fused_kernel(const float* 
     const int qi = __float_as_int(q.w);
     if (qi != INT_MAX && better(q.z, qi, bv, bi)) { bv = q.z; bi = qi; }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
-    const float ov = __shfl_xor(bv, o, kWave);
-    const int oi = __shfl_xor(bi, o, kWave);
-    if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-  }
+  acc = wave_ms(acc);
+  wave_best(bv, bi);
   if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; sb[wave] = bv; si[wave] = bi; }
   __syncthreads();
   if (tid != 0 || st.done[b]) return;
@@ -298,8 +336,7 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
       list_insert<K2>(v, ix, q, i);
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  acc = wave_ms(acc);
   if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; }
 
   // each wave merges its 64 lists: K2 rounds of a wave-wide (value desc, index asc) argmax;
@@ -307,12 +344,7 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_kernel(const float* _
   for (int round = 0; round < K2; ++round) {
     float bv = v[0];
     int bi = ix[0];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
+    wave_best(bv, bi);
     if (lane == 0) { wv[wave][round] = bv; wi[wave][round] = bi; }
     if (ix[0] == bi && v[0] == bv && bi != INT_MAX) {
 #pragma unroll
@@ -384,8 +416,7 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const floa
     for (int u = 0; u < SEL_REG; ++u)
       acc.s += (__expf(q[u].x - tmax) + __expf(q[u].y - tmax)) + (__expf(q[u].z - tmax) + __expf(q[u].w - tmax));
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  acc = wave_ms(acc);
   if (lane == 0) { sm[wave] = acc.m; ss[wave] = acc.s; }
   // the K2 largest thread maxima of each wave (K2 rounds of a wave max; one lane drops out)
   {
@@ -393,12 +424,7 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const floa
     for (int j = 0; j < K2; ++j) {
       float best = mine;
       int bl = lane;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const float ov = __shfl_xor(best, o, kWave);
-        const int ol = __shfl_xor(bl, o, kWave);
-        if (ov > best || (ov == best && ol < bl)) { best = ov; bl = ol; }
-      }
+      wave_best(best, bl);
       if (lane == 0) wmax[wave][j] = best;
       if (lane == bl) mine = -INFINITY;
     }
@@ -450,12 +476,7 @@ __global__ __launch_bounds__(SEL_THREADS) void beam_select_reg_kernel(const floa
   for (int round = 0; round < K2; ++round) {
     float bv = v[0];
     int bi = ix[0];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
-      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-    }
+    wave_best(bv, bi);
     if (lane == 0) { wv[wave][round] = bv; wi[wave][round] = bi; }
     if (ix[0] == bi && v[0] == bv && bi != INT_MAX) {
 #pragma unroll
@@ -526,8 +547,7 @@ __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __r
     tm[j] = t < n_tiles ? mx : -INFINITY;
     if (t < n_tiles) acc = ms_merge(acc, MaxSum{mx, sm});
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  acc = wave_ms(acc);
   // tau: k2 rounds of a wave max over the tile maxima, each winner giving up that entry
   float tau = -INFINITY;
   {
@@ -540,12 +560,7 @@ __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __r
       for (int j = 0; j < SEL_TPL; ++j) mine = fmaxf(mine, rest[j]);
       float best = mine;
       int bl = lane;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const float ov = __shfl_xor(best, o, kWave);
-        const int ol = __shfl_xor(bl, o, kWave);
-        if (ov > best || (ov == best && ol < bl)) { best = ov; bl = ol; }
-      }
+      wave_best(best, bl);
       tau = best;
       if (lane == bl) {
         bool gone = false;
@@ -608,12 +623,7 @@ __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __r
   for (int round = 0; round < k2; ++round) {
     float bv = v[0];
     int bi = ix[0];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
-      if (better(ov, oi, bv, bi) || (bi == INT_MAX && oi != INT_MAX)) { bv = ov; bi = oi; }
-    }
+    wave_best(bv, bi);
     if (lane == 0) {
       topv[(size_t)r * k2 + round] = bi == INT_MAX ? -INFINITY : bv;
       topi[(size_t)r * k2 + round] = bi;
@@ -643,8 +653,7 @@ __global__ __launch_bounds__(256) void tile_records_kernel(const float* __restri
     const float x = n < V ? logits[(size_t)r * V + n] : -INFINITY;
     if (x != -INFINITY) acc = ms_merge(acc, MaxSum{x, 1.f});
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) acc = ms_merge(acc, MaxSum{__shfl_xor(acc.m, o, kWave), __shfl_xor(acc.s, o, kWave)});
+  acc = wave_ms(acc);
   if (lane == 0) {
     float* q = part + ((size_t)r * n_tiles + t) * 4;
     q[0] = acc.m;
@@ -701,13 +710,7 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
 #pragma unroll
     for (int c = 0; c < MAXC; ++c)
       if (ck[c] != INT_MAX && (better(cv[c], ck[c], bv, bk) || bk == INT_MAX)) { bv = cv[c]; bk = ck[c]; blp = clp[c]; }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int ok = __shfl_xor(bk, o, kWave);
-      const float olp = __shfl_xor(blp, o, kWave);
-      if (ok != INT_MAX && (bk == INT_MAX || better(ov, ok, bv, bk))) { bv = ov; bk = ok; blp = olp; }
-    }
+    wave_best(bv, bk, blp);
 #pragma unroll
     for (int c = 0; c < MAXC; ++c)
       if (ck[c] == bk) ck[c] = INT_MAX;     // keys are unique: exactly one lane consumes it
