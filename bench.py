@@ -47,7 +47,7 @@ GEMM_CLASSES = (0, 1, 2)
 TRAFFIC = {
     ("gemm_dec", "base-6-6"): {
         "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
-        "sha256": "bba333e38b8b485c9db3e4e4e52d0da7bfd4230e346dab66893fa8cd1d73c3e4",
+        "sha256": "cfb8cb2073d7e5f4edc40f75635ddf3b3dc55a0144372cefea607e7ac1321b55",
         "fetch_kib": 3913.94, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
