@@ -64,13 +64,20 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
 
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int grp = lane >> 4, ln = lane & 15;
+  // every argument of the common path named at entry: their scalar-cache misses overlap
+  asm volatile("" ::"s"(a.q), "s"(a.q_ld), "s"(a.k), "s"(a.v), "s"(a.kb), "s"(a.kh), "s"(a.ks), "s"(a.out),
+               "s"(a.out_ld), "s"(a.group_map), "s"(a.lens), "s"(a.q_per_group), "s"(a.self_queries),
+               "s"(a.n_groups), "s"(a.H), "s"(a.scale), "s"(a.ctl));
   const int qblocks = (a.q_per_group + 15) / 16;
-  const int n_groups = a.ctl ? min(a.n_groups, a.ctl[CTL_NLIVE]) : a.n_groups;
   const int task = blockIdx.x * 4 + wave;
-  if (task >= n_groups * a.H * qblocks) return;   // whole wave; wave-local sync only below
+  if (task >= a.n_groups * a.H * qblocks) return;   // grid tail
   const int qb = task % qblocks, gh = task / qblocks;
   const int h = gh % a.H, g = gh / a.H;
+  // the group's entry (valid for every group of the grid) and the live count together
   const int b = a.group_map ? a.group_map[g] : g;
+  const int nlive = a.ctl ? a.ctl[CTL_NLIVE] : a.n_groups;
+  asm volatile("" ::"v"(b), "s"(nlive));
+  if (g >= min(a.n_groups, nlive)) return;   // whole wave; wave-local sync only below
   const int len = a.lens[b];
   const int nq = a.self_queries ? min(len, a.q_per_group) : a.q_per_group;
   const int q0 = qb * 16;
@@ -311,18 +318,27 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   constexpr int VEC = Vec<T>::N, CPR = DH / VEC, GPW = kWave / CPR, KPL = 4, KCH = GPW * KPL;
   static_assert(CPR >= 1 && CPR <= kWave && (CPR & (CPR - 1)) == 0, "a key's chunks fit in a wave");
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  // every argument the wave uses, named at entry: their scalar-cache misses overlap
+  asm volatile("" ::"s"(a.q), "s"(a.kcache), "s"(a.vcache), "s"(a.sent_list), "s"(a.beam), "s"(a.anc),
+               "s"(a.anc_stride), "s"(a.out), "s"(a.rows), "s"(a.H), "s"(a.Tcap), "s"(a.scale), "s"(a.ctl));
   const int pair = blockIdx.x * 4 + wave;
-  const int rows = min(a.rows, a.ctl[CTL_NLIVE] * a.beam);
-  if (pair >= rows * a.H) return;              // whole wave exits; no block barrier below
+  if (pair >= a.rows * a.H) return;            // grid tail
   const int row = pair / a.H, h = pair % a.H;
-  const int p = a.sent_list[row / a.beam] * a.beam + row % a.beam;
   const int c = lane % CPR, g = lane / CPR;    // channel chunk and key group of this lane
+  // The list entry, the query and the step counters are read together (every row of the
+  // grid is allocated and its list entry names a valid sentence); only the cache stream
+  // waits for the live-row check.
+  const int sent = a.sent_list[row / a.beam];
   float q[VEC];
   load16(static_cast<const T*>(a.q) + (size_t)row * a.H * DH + h * DH + c * VEC, q);
+  const int nlive = a.ctl[CTL_NLIVE], t = a.ctl[CTL_T], asel = a.ctl[CTL_ANC];
+  asm volatile("" ::"v"(sent), "s"(nlive), "s"(t), "s"(asel));
+  if (row >= min(a.rows, nlive * a.beam)) return;   // whole wave exits; no block barrier below
+  const int p = sent * a.beam + row % a.beam;
 #pragma unroll
   for (int x = 0; x < VEC; ++x) q[x] *= a.scale;
-  const int t = a.ctl[CTL_T], n = t + 1;
-  const int* anc = a.anc ? a.anc + (size_t)a.ctl[CTL_ANC] * a.anc_stride + (size_t)p * a.Tcap : nullptr;
+  const int n = t + 1;
+  const int* anc = a.anc ? a.anc + (size_t)asel * a.anc_stride + (size_t)p * a.Tcap : nullptr;
   const size_t head = (size_t)h * a.Tcap * DH + c * VEC;
   const T* K = static_cast<const T*>(a.kcache) + head;
   const T* Vc = static_cast<const T*>(a.vcache) + head;

@@ -135,19 +135,26 @@ template <typename T, int EPL>
 __global__ __launch_bounds__(256) void ln_kernel(const T* __restrict__ x, const float* __restrict__ ln,
                                                  T* __restrict__ y, int rows, int d, float eps, const int* ctl,
                                                  int ctl_rows) {
+  asm volatile("" ::"s"(x), "s"(ln), "s"(y), "s"(ctl), "s"(rows), "s"(d), "s"(ctl_rows));   // one wait for all arguments
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
-  const int c0 = (threadIdx.x % kWave) * EPL;
-  LnCols<EPL> lc;   // row-independent: in flight with the live-row count
-  load_ln_cols<EPL>(ln, ln + d, c0, lc);
-  if (ctl) rows = min(rows, ctl[CTL_NLIVE] * ctl_rows);
   if (row >= rows) return;
+  // Every row of the grid is allocated, so the row and the gain/bias are read before the
+  // live-row count arrives: the count (just written, often by another XCD) gates only
+  // the store, and its latency overlaps the row's.
+  const int c0 = (threadIdx.x % kWave) * EPL;
+  LnCols<EPL> lc;
+  load_ln_cols<EPL>(ln, ln + d, c0, lc);
   float v[EPL], o[EPL];
   load_row<T, EPL>(x + (size_t)row * d + c0, v);
+  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * ctl_rows) : rows;
   wave_layernorm<EPL>(v, o, lc, 1.0f / (float)d, eps);
-  store_row<T, EPL>(y + (size_t)row * d + c0, o);
+  if (row < live) store_row<T, EPL>(y + (size_t)row * d + c0, o);
 }
 
 // Decoder input of step t for live row r: z = sqrt(d) E[tok] + PE(t), u = LN(z).
+// Every row of the grid computes (its list entry and token are valid IDs whether or not
+// the row is live), and the live-row count gates only the stores: so the count, the list
+// entry and the gain/bias are in flight together instead of one after another.
 template <typename T, int EPL>
 __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ cur_tok,
                                                         const int* __restrict__ sent_list, int beam,
@@ -155,21 +162,25 @@ __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ 
                                                         const int* __restrict__ ctl, float scale,
                                                         const float* __restrict__ ln, T* __restrict__ z,
                                                         T* __restrict__ u, int rows, int d, float eps) {
+  asm volatile("" ::"s"(cur_tok), "s"(sent_list), "s"(E), "s"(pe), "s"(ctl), "s"(ln), "s"(rows), "s"(beam),
+               "s"(d));
   const int row = blockIdx.x * ROWS_PER_BLOCK + threadIdx.x / kWave;
+  if (row >= rows) return;
   const int c0 = (threadIdx.x % kWave) * EPL;
   LnCols<EPL> lc;
   load_ln_cols<EPL>(ln, ln + d, c0, lc);
-  if (row >= min(rows, ctl[CTL_NLIVE] * beam)) return;
-  const int t = ctl[CTL_T];
-  const int p = sent_list[row / beam] * beam + row % beam;
+  const int sent = sent_list[row / beam], t = ctl[CTL_T], nlive = ctl[CTL_NLIVE];
+  asm volatile("" ::"v"(sent), "v"(t), "v"(nlive));   // both loads issued before either is waited on
+  const int p = sent * beam + row % beam;
+  const bool live = row < min(rows, nlive * beam);
   float v[EPL], o[EPL];
   load_row<T, EPL>(E + (size_t)cur_tok[p] * d + c0, v);
   const float* pr = pe + (size_t)t * d + c0;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) v[i] = to_f32(from_f32<T>(scale * v[i] + pr[i]));
-  store_row<T, EPL>(z + (size_t)row * d + c0, v);
+  if (live) store_row<T, EPL>(z + (size_t)row * d + c0, v);
   wave_layernorm<EPL>(v, o, lc, 1.0f / (float)d, eps);
-  store_row<T, EPL>(u + (size_t)row * d + c0, o);
+  if (live) store_row<T, EPL>(u + (size_t)row * d + c0, o);
 }
 
 // dst[n][k] = src[k][n] through a 32x33 LDS tile.

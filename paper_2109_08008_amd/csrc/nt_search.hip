@@ -225,17 +225,22 @@ __global__ __launch_bounds__(SEL_THREADS) void greedy_fused_kernel(const float* 
                                                                    SearchState st) {
   __shared__ float sm[SEL_THREADS / kWave], ss[SEL_THREADS / kWave], sb[SEL_THREADS / kWave];
   __shared__ int si[SEL_THREADS / kWave];
-  const int r = blockIdx.x;
-  if (r >= st.ctl[CTL_NLIVE]) return;
-  const int t = st.ctl[CTL_T];
-  const int b = st.sent_list[r];
-  const float* rec = part + (size_t)r * n_tiles * 4;
+  asm volatile("" ::"s"(part), "s"(n_tiles), "s"(st.sent_list), "s"(st.ctl));   // one wait for the arguments
+  const int r = blockIdx.x;   // every row of the grid has records and a list entry
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const float4* rec = reinterpret_cast<const float4*>(part + (size_t)r * n_tiles * 4);
+  // The thread's first record, the list entry and the step counters are read together;
+  // the live-row check waits for them all at once.
+  float4 q0 = rec[min(tid, n_tiles - 1)];
+  const int b = st.sent_list[r], nlive = st.ctl[CTL_NLIVE], t = st.ctl[CTL_T];
+  asm volatile("" ::"v"(q0.x), "v"(q0.y), "v"(q0.z), "v"(q0.w), "v"(b), "s"(nlive), "s"(t));
+  if (r >= nlive) return;
+  if (tid >= n_tiles) q0 = float4{-INFINITY, 0.f, -INFINITY, __int_as_float(INT_MAX)};   // merges as nothing
   MaxSum acc{-INFINITY, 0.f};
   float bv = -INFINITY;
   int bi = INT_MAX;
   for (int i = tid; i < n_tiles; i += SEL_THREADS) {
-    const float4 q = reinterpret_cast<const float4*>(rec)[i];
+    const float4 q = i == tid ? q0 : rec[i];
     acc = ms_merge(acc, MaxSum{q.x, q.y});
     const int qi = __float_as_int(q.w);
     if (qi != INT_MAX && better(q.z, qi, bv, bi)) { bv = q.z; bi = qi; }
@@ -532,20 +537,29 @@ __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __r
   constexpr int REC = 4;            // record floats (max, sum, best value, best index)
   constexpr int SEL_CAND = K2 < 8 ? 8 : K2 > 16 ? 16 : K2;   // candidate tiles per batch (usually all)
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  asm volatile("" ::"s"(part), "s"(n_tiles), "s"(logits), "s"(ctl), "s"(beam), "s"(rows), "s"(V), "s"(k2));
   const int r = blockIdx.x * 4 + wave;
-  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
-  if (r >= live) return;            // whole wave; no block barrier below
+  if (r >= rows) return;            // grid tail
   const float* rec = part + (size_t)r * n_tiles * REC;
+  // The row's records (every row of the grid has them) and the live count are read
+  // together; the live-row check waits for them all at once.
+  float2 rq[SEL_TPL];
+#pragma unroll
+  for (int j = 0; j < SEL_TPL; ++j)
+    rq[j] = *reinterpret_cast<const float2*>(rec + (size_t)min(lane + j * kWave, n_tiles - 1) * REC);
+  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
+#pragma unroll
+  for (int j = 0; j < SEL_TPL; ++j) asm volatile("" ::"v"(rq[j].x), "v"(rq[j].y));
+  asm volatile("" ::"s"(live));
+  if (r >= live) return;            // whole wave; no block barrier below
   // the lane's tile maxima, and the row's (max, sum) merged over every record
   float tm[SEL_TPL];
   MaxSum acc{-INFINITY, 0.f};
 #pragma unroll
   for (int j = 0; j < SEL_TPL; ++j) {
     const int t = lane + j * kWave;
-    const float* q = rec + (size_t)min(t, n_tiles - 1) * REC;
-    const float mx = q[0], sm = q[1];
-    tm[j] = t < n_tiles ? mx : -INFINITY;
-    if (t < n_tiles) acc = ms_merge(acc, MaxSum{mx, sm});
+    tm[j] = t < n_tiles ? rq[j].x : -INFINITY;
+    if (t < n_tiles) acc = ms_merge(acc, MaxSum{rq[j].x, rq[j].y});
   }
   acc = wave_ms(acc);
   // tau: k2 rounds of a wave max over the tile maxima, each winner giving up that entry
@@ -673,15 +687,45 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
   __shared__ int sel_key[4][32];
   __shared__ int nk_par[4][16], nk_cnt[4];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  asm volatile("" ::"s"(topv), "s"(topi), "s"(lse), "s"(st.B), "s"(st.beam), "s"(st.V), "s"(st.sent_list),
+               "s"(st.ctl), "s"(st.score), "s"(st.done));
   const int bl = blockIdx.x * 4 + wave;
-  if (bl >= st.ctl[CTL_NLIVE]) return;              // whole wave leaves; no block barrier below
-  const int t = st.ctl[CTL_T];
-  const int* anc_cur = st.anc + (size_t)st.ctl[CTL_ANC] * st.anc_stride;
-  int* anc_next = st.anc + (size_t)(st.ctl[CTL_ANC] ^ 1) * st.anc_stride;
-  const int b = st.sent_list[bl];
-  if (st.done[b]) return;
-  const int K = st.beam, K2 = 2 * K, V = st.V, n = t + 1;
+  if (bl >= st.B) return;                           // grid tail
+  const int K = st.beam, K2 = 2 * K, V = st.V;
   const int ncand = K * K2;
+  // The candidates of list entry bl (every entry of the grid has them), the entry and the
+  // live count are read together, then the sentence's flag and scores: two dependent
+  // round trips before the merge instead of four.
+  float rv[MAXC], rl[MAXC], rs[MAXC];
+  int rw[MAXC];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    rv[c] = -INFINITY;
+    rl[c] = 0.f;
+    rw[c] = INT_MAX;
+    if (c * kWave < ncand) {                // the same in every lane
+      const int q = min(lane + c * kWave, ncand - 1), k = q / K2, i = q - k * K2, r = bl * K + k;
+      rv[c] = topv[(size_t)r * K2 + i];
+      rw[c] = topi[(size_t)r * K2 + i];
+      rl[c] = lse[r];
+    }
+  }
+  const int b0 = st.sent_list[bl], nlive = st.ctl[CTL_NLIVE];
+  asm volatile("" ::"v"(b0), "s"(nlive));
+  if (bl >= nlive) return;                          // whole wave leaves; no block barrier below
+  const int b = b0;
+  const int t = st.ctl[CTL_T], asel = st.ctl[CTL_ANC];
+  const int* anc_cur = st.anc + (size_t)asel * st.anc_stride;
+  int* anc_next = st.anc + (size_t)(asel ^ 1) * st.anc_stride;
+  const int n = t + 1;
+  const int done = st.done[b];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    rs[c] = 0.f;
+    if (c * kWave < ncand) rs[c] = st.score[b * K + min(lane + c * kWave, ncand - 1) / K2];
+  }
+  asm volatile("" ::"v"(done));
+  if (done) return;
 
   float cv[MAXC], clp[MAXC];
   int ck[MAXC];
@@ -692,13 +736,12 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
     clp[c] = 0.f;
     ck[c] = INT_MAX;
     if (q < ncand) {
-      const int k = q / K2, i = q - k * K2;
-      const int r = bl * K + k, p = b * K + k;
-      const float v = topv[(size_t)r * K2 + i];
-      const int w = topi[(size_t)r * K2 + i];
+      const int k = q / K2;
+      const float v = rv[c];
+      const int w = rw[c];
       if (w == INT_MAX) continue;           // fewer than 2K words in the vocabulary
-      const float lp = st.logp_input ? v : v - lse[r];
-      cv[c] = st.score[p] + lp;
+      const float lp = st.logp_input ? v : v - rl[c];
+      cv[c] = rs[c] + lp;
       clp[c] = lp;
       ck[c] = k * V + w;
     }
