@@ -47,8 +47,8 @@ GEMM_CLASSES = (0, 1, 2)
 TRAFFIC = {
     ("gemm_dec", "base-6-6"): {
         "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
-        "sha256": "cfb8cb2073d7e5f4edc40f75635ddf3b3dc55a0144372cefea607e7ac1321b55",
-        "fetch_kib": 3913.94, "write_kib": 1304.31, "fetch_scale": 2.0, "write_scale": 1.0,
+        "sha256": "a723ea1969414fa97747cf7f8b31623a3cd7257e2bf25dcd010a9857ffce0779",
+        "fetch_kib": 3923.22, "write_kib": 1304.33, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 

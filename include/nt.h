@@ -252,6 +252,19 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
                      const float* d_bias, const void* d_resid, void* d_out, int32_t ldc, int32_t out_f32,
                      int32_t relu, int32_t tile, const float* d_bscale, void* stream);
 
+/* The same projection with its input's pre-norm LayerNorm folded in (Sec. 2.1: every
+ * sublayer normalises its input first), as the decoder step runs it for weights in the
+ * model dtype:  out[m][n] = act(rstd_m (A_m . Bt_n - mu_m colsum[n]) + bias[n]), with mu_m
+ * the mean of row m of A over its K values, rstd_m = 1/sqrt(var_m + ln_eps) (biased
+ * variance), and act = ReLU if relu != 0.  With Bt = (diag(gamma) W)^T, colsum[n] =
+ * sum_k Bt[n][k] and bias = b + beta W this is LN(A) W + b.  A, Bt and out (ldc) are
+ * device arrays in `dtype`; d_colsum [N] and d_bias [N] fp32 device arrays (bias may be
+ * NULL).  K % 64 == 0 and K is the whole row.  tile as for nt_op_gemm (2 runs as 4, which
+ * holds the row statistics at a higher occupancy).  Asynchronous. */
+nt_status nt_op_gemm_ln(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N,
+                        int32_t K, const float* d_colsum, float ln_eps, const float* d_bias, void* d_out,
+                        int32_t ldc, int32_t relu, int32_t tile, void* stream);
+
 /* The FP8 weight quantization nt_load_weights applies with fp8_weights, on the host: W
  * [in][out] fp32 (row-major, y = x W) -> q [out][in] E4M3 codes (OCP, bias 7, ties to
  * even, saturating at 448) and scale [out] fp32, with scale[n] = max_k |W[k][n]| / 448

@@ -52,6 +52,33 @@ __device__ __forceinline__ u32x4 f8_to_f16x8(unsigned w0, unsigned w1) {
   return u32x4{f8x2<false>(w0), f8x2<true>(w0), f8x2<false>(w1), f8x2<true>(w1)};
 }
 
+// Sum and sum of squares of the eight (fp16/bf16) or four (fp32) values of one 16-byte
+// operand fragment, added into s and q in fp32: the row statistics of a folded LayerNorm.
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+template <typename T>
+__device__ __forceinline__ void frag_stats(const u32x4& a, float& s, float& q) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if constexpr (std::is_same<T, f16>::value) {
+      // the word is copied out first: a bit_cast of the vector element itself read word 0
+      const unsigned u = a[w];
+      const half2v h = __builtin_bit_cast(half2v, u);
+      s = __builtin_amdgcn_fdot2(h, half2v{(_Float16)1.0f, (_Float16)1.0f}, s, false);
+      q = __builtin_amdgcn_fdot2(h, h, q, false);
+    } else if constexpr (std::is_same<T, bf16>::value) {
+      const float lo = __uint_as_float(a[w] << 16), hi = __uint_as_float(a[w] & 0xffff0000u);
+      s += lo;
+      s += hi;
+      q = fmaf(lo, lo, q);
+      q = fmaf(hi, hi, q);
+    } else {
+      const float x = __uint_as_float(a[w]);
+      s += x;
+      q = fmaf(x, x, q);
+    }
+  }
+}
+
 // Four consecutive elements of the model dtype as loaded (raw bits: converted only where
 // they are used, so the load does not have to complete where it is issued).
 template <typename T> struct Raw4 { using type = uint2; };
@@ -325,10 +352,11 @@ __device__ __forceinline__ void topk_tile_rows(const float* cs, int CS, int mrow
 // wave load moves 16 of them), each lane's 16-byte B fragment carries the 16 k-values
 // of both half-steps, and lane l supplies A k-values 16*(l/16) .. +7 and +8 .. +15 (the
 // two operands agree on the k each lane carries, which is all the MFMA needs).
-template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false>
+template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false, bool LNF = false>
 __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int lda, const void* __restrict__ Bt,
                                                     int M, int N, int K, GemmEpi epi, int tiles_m, int tiles_n) {
   static_assert(!F8 || std::is_same<T, f16>::value, "FP8 weights pair with fp16 activations");
+  static_assert(!(F8 && LNF), "a folded LayerNorm needs weights in the model dtype");
   constexpr int ROWB_B = F8 ? ROWB8 : ROWB;
   constexpr int STAGE_BYTES = BM_ * ROWB + BN_ * ROWB_B;
   constexpr int GROUPS_A = BM_ / 8;                 // 8 A rows = one 1 KB wave load
@@ -445,6 +473,18 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     }
   }
 
+  // folded LayerNorm: lane (fr, fc) sums the k-chunks fc and 4+fc of its fragment rows
+  // over every k-step; the four lanes of a row together see each of its K values once.
+  // The lane's column sums (its output column is fixed per 16x16 block) are fetched here,
+  // so their latency hides behind the k-loop instead of stalling the epilogue.
+  float lsum[LNF ? FM : 1], lsq[LNF ? FM : 1], lcs[LNF ? FN : 1];
+#pragma unroll
+  for (int i = 0; i < (LNF ? FM : 1); ++i) lsum[i] = lsq[i] = 0.f;
+  if constexpr (LNF) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) lcs[j] = epi.lnf_colsum[min(n0 + wn * WN + j * 16 + fr, N - 1)];
+  }
+
   const int nk = (int)((size_t)K * sizeof(T) / ROWB);
   for (int st = 0; st < STAGES - 1 && st < nk; ++st) NT_ISSUE(st, st)
   int slot = 0;   // slot of k-step kt
@@ -487,15 +527,48 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af0[i], bf0[j], acc[i][j]);
+    if constexpr (LNF) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) frag_stats<T>(af0[i], lsum[i], lsq[i]);
+    }
     __builtin_amdgcn_sched_barrier(0);   // keep the second wait behind the first half's MFMAs
     LdsWait<FM, FN>::template run<0>(af1, bf1);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af1[i], bf1[j], acc[i][j]);
+    if constexpr (LNF) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) frag_stats<T>(af1[i], lsum[i], lsq[i]);
+    }
     slot = slot == STAGES - 1 ? 0 : slot + 1;
   }
 #undef NT_ISSUE
+  // folded LayerNorm: each row's mean and 1/sqrt(biased variance + eps), one pass over
+  // the fragments (E[x^2] - mean^2 in fp32), kept per tile row for the epilogue
+  // (the accumulators become rstd * (acc - mean * colsum[n]) as they enter the epilogue)
+  float* ln_mu = nullptr;
+  float* ln_rs = nullptr;
+  if constexpr (LNF) {
+    __shared__ __attribute__((aligned(16))) float ln_stat[2 * BM_];
+    ln_mu = ln_stat;
+    ln_rs = ln_stat + BM_;
+    const float inv_k = 1.0f / (float)K;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      float s = lsum[i], q = lsq[i];
+      s += __shfl_xor(s, 16, kWave);
+      q += __shfl_xor(q, 16, kWave);
+      s += __shfl_xor(s, 32, kWave);
+      q += __shfl_xor(q, 32, kWave);
+      if (wn == 0 && fc == 0) {
+        const float mu = s * inv_k;
+        const float var = fmaxf(q * inv_k - mu * mu, 0.f);
+        ln_mu[wm * WM + i * 16 + fr] = mu;
+        ln_rs[wm * WM + i * 16 + fr] = 1.0f / sqrtf(var + epi.lnf_eps);
+      }
+    }
+  }
   __syncthreads();
 
   // --- epilogue through the LDS ring in passes of ER rows: fragments -> [ER][BN+4] fp32
@@ -540,11 +613,20 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     for (int i = 0; i < FM; ++i) {
       const int rb = wm * WM + i * 16;            // first tile row of this block
       if (rb >= pass * ER && rb < pass * ER + ER) {
+        float4 mu4{0.f, 0.f, 0.f, 0.f}, rs4{1.f, 1.f, 1.f, 1.f};   // lane rows rb + 4*fc + r
+        if constexpr (LNF) {
+          mu4 = *reinterpret_cast<const float4*>(ln_mu + rb + fc * 4);
+          rs4 = *reinterpret_cast<const float4*>(ln_rs + rb + fc * 4);
+        }
+        const float mur[4] = {mu4.x, mu4.y, mu4.z, mu4.w}, rsr[4] = {rs4.x, rs4.y, rs4.z, rs4.w};
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            cs[(rb - pass * ER + fc * 4 + r) * CS + wn * WN + j * 16 + fr] = F8 ? acc[i][j][r] * wsc[j] : acc[i][j][r];
+          for (int r = 0; r < 4; ++r) {
+            float v = F8 ? acc[i][j][r] * wsc[j] : acc[i][j][r];
+            if constexpr (LNF) v = (v - mur[r] * lcs[j]) * rsr[r];
+            cs[(rb - pass * ER + fc * 4 + r) * CS + wn * WN + j * 16 + fr] = v;
+          }
       }
     }
     __syncthreads();
@@ -597,11 +679,11 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   }
 }
 
-template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false>
+template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false, bool LNF = false>
 hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                        hipStream_t s) {
   const int tm = (M + BM_ - 1) / BM_, tn = (N + BN_ - 1) / BN_;
-  NT_LAUNCH((gemm_kernel<T, BM_, BN_, STAGES, ROLE, F8>), dim3(tm * tn), dim3(NTHR), 0, s,
+  NT_LAUNCH((gemm_kernel<T, BM_, BN_, STAGES, ROLE, F8, LNF>), dim3(tm * tn), dim3(NTHR), 0, s,
                      static_cast<const T*>(A), lda, Bt, M, N, K, epi, tm, tn);
   return hipGetLastError();
 }
@@ -629,6 +711,21 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
   // 32x64 (3 stages) is the best small tile (650x512x512: 5.1 us against 6.2 at 64x64;
   // 1300x512x2048: 13.0 against 15.9) and 64x64 the best middle one (1300x1536x512: 8.2
   // against 9.1 at 64x128).
+  // folded LayerNorm: decoder-step launches with weights in the model dtype
+  if (epi.lnf_colsum) {
+    if constexpr (ROLE != 1) {
+      return hipErrorInvalidValue;
+    } else {
+      // (128x128 would hold the row statistics at one wave per SIMD: 64x128 instead)
+      if (epi.wscale) return hipErrorInvalidValue;
+      switch (tile) {
+        case 2:
+        case 4: return launch_tile<T, 64, 128, 2, ROLE, false, true>(A, lda, Bt, M, N, K, epi, s);
+        case 3: return launch_tile<T, 128, 64, 2, ROLE, false, true>(A, lda, Bt, M, N, K, epi, s);
+        default: return launch_tile<T, 64, 32, 3, ROLE, false, true>(A, lda, Bt, M, N, K, epi, s);
+      }
+    }
+  }
   if (epi.wscale) {
     if constexpr (!std::is_same<T, f16>::value || ROLE == 2) {
       return hipErrorInvalidValue;

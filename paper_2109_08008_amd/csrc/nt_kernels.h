@@ -85,6 +85,14 @@ struct GemmEpi {
   // FP8 weights: Bt is [N][K] FP8 E4M3 bytes and column n of the product is scaled by
   // wscale[n] (fp32); null for weights in the model dtype.  fp16 activations only.
   const float* wscale = nullptr;
+  // Pre-norm LayerNorm folded into the product (decoder-step launches, weights in the
+  // model dtype, K = the row width): A holds the rows x before normalisation, Bt holds
+  // W' = diag(gamma) W, bias holds b + beta W, and lnf_colsum[n] = sum_k Bt[n][k].  The
+  // kernel sums each row's x and x^2 from its A fragments during the k-loop, and the
+  // epilogue forms rstd * (acc - mean * lnf_colsum[n]) before adding the bias, which is
+  // LN(x) W + b up to rounding.
+  const float* lnf_colsum = nullptr;
+  float lnf_eps = 0.f;
   // EPI_TOPK (the launch uses 128x128 tiles, so n_tiles = ceil(N / 128))
   float* part = nullptr;           // [M][n_tiles][topk_record(k2)]
   int k2 = 1;                      // record layout: 1 (max, sum, best value, best column); the
@@ -156,6 +164,9 @@ hipError_t dec_embed_ln(DT dt, const int* cur_tok, const int* sent_list, int bea
 hipError_t pack_transpose(DT dt, const float* src, void* dst, int K, int N, hipStream_t s);
 // dst[i] = (T) src[i].
 hipError_t pack_convert(DT dt, const float* src, void* dst, size_t n, hipStream_t s);
+// out[n] = sum_k Bt[n][k] in fp32, over a packed [N][K] weight matrix of the model dtype
+// (the column sums a folded LayerNorm subtracts, taken from the values the GEMM reads).
+hipError_t packed_row_sums(DT dt, const void* Bt, int N, int K, float* out, hipStream_t s);
 
 // ---------------------------------------------------------------------------------
 // Attention.

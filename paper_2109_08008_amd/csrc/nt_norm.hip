@@ -297,7 +297,29 @@ hipError_t convert_t(const float* src, void* dst, size_t n, hipStream_t s) {
   NT_LAUNCH(convert_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, s, src, static_cast<T*>(dst), n);
   return hipGetLastError();
 }
+// One wave per packed row: the row's K values summed in fp32 (lanes stride over k).
+template <typename T>
+__global__ __launch_bounds__(256) void row_sums_kernel(const T* __restrict__ Bt, int N, int K,
+                                                       float* __restrict__ out) {
+  const int n = blockIdx.x * 4 + threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  if (n >= N) return;
+  float s = 0.f;
+  for (int k = lane; k < K; k += kWave) s += to_f32(Bt[(size_t)n * K + k]);
+  s = wave_sum(s);
+  if (lane == 0) out[n] = s;
+}
+
+template <typename T>
+hipError_t row_sums_t(const void* Bt, int N, int K, float* out, hipStream_t s) {
+  NT_LAUNCH(row_sums_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, static_cast<const T*>(Bt), N, K, out);
+  return hipGetLastError();
+}
 }  // namespace
+
+hipError_t packed_row_sums(DT dt, const void* Bt, int N, int K, float* out, hipStream_t s) {
+  if (N <= 0) return hipSuccess;
+  NT_DT_SWITCH(dt, row_sums_t, Bt, N, K, out, s)
+}
 
 hipError_t pack_transpose(DT dt, const float* src, void* dst, int K, int N, hipStream_t s) {
   NT_DT_SWITCH(dt, transpose_t, src, dst, K, N, s)

@@ -21,6 +21,7 @@
 #include <mutex>
 #include <numeric>
 #include <string>
+#include <deque>
 #include <vector>
 
 #include "../../include/nt.h"
@@ -154,6 +155,10 @@ struct DecLayerW {
   const float *ln1, *bqkv, *bo, *ln2, *bq, *boc, *ln3, *b1, *b2;
   const void *Wqkv, *Wo, *Wq, *Woc, *W1, *W2;
   const float *sqkv = nullptr, *so = nullptr, *sq = nullptr, *soc = nullptr, *s1 = nullptr, *s2 = nullptr;
+  // Folded pre-norm LayerNorms (weights in the model dtype): Wqkv, Wq and W1 hold
+  // diag(gamma) W of ln1, ln2 and ln3, their biases b + beta W, and these the column sums of
+  // the packed matrices; null when the LayerNorms run as kernels of their own (FP8).
+  const float *cqkv = nullptr, *cq = nullptr, *c1 = nullptr;
 };
 
 struct nt_model {
@@ -213,7 +218,8 @@ struct ModelLayout {
   size_t total = 0;
   size_t E, pe, hist_ln, dlcl, enc_out_ln, Wkv_all, bkv_all, dec_out_ln;
   struct Enc { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, W1, b1, W2, b2, relk, relv, sqkv, so, s1, s2; };
-  struct Dec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Woc, boc, ln3, W1, b1, W2, b2, sqkv, so, sq, soc, s1, s2; };
+  struct Dec { size_t ln1, Wqkv, bqkv, Wo, bo, ln2, Wq, bq, Woc, boc, ln3, W1, b1, W2, b2, sqkv, so, sq, soc, s1, s2,
+               cqkv, cq, c1; };
   size_t skv_all = 0;
   std::vector<Enc> enc;
   std::vector<Dec> dec;
@@ -286,6 +292,9 @@ ModelLayout layout_of(const nt_model_cfg& c) {
     e.soc = f8 ? take(d * 4) : 0;
     e.s1 = f8 ? take(F * 4) : 0;
     e.s2 = f8 ? take(d * 4) : 0;
+    e.cqkv = f8 ? 0 : take(3 * d * 4);
+    e.cq = f8 ? 0 : take(d * 4);
+    e.c1 = f8 ? 0 : take(F * 4);
     Lo.dec.push_back(e);
   }
   Lo.Wkv_all = take(Ld * 2 * d * d * mb);
@@ -789,7 +798,12 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.d = d;
       e.H = m.H;
       e.dh = m.dh;
-      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wqkv, 3 * d, d, e));
+      // folded pre-norm LayerNorms: the projection normalises its input rows itself
+      const bool fold = w.cqkv != nullptr;
+      const void* ln_in = fold ? at(p.z) : at(p.du);
+      e.lnf_colsum = w.cqkv;
+      e.lnf_eps = eps;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, ln_in, d, w.Wqkv, 3 * d, d, e));
 
       nt::SelfAttnArgs sa{};
       sa.q = at(p.dq);
@@ -818,8 +832,9 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.ldc = d;
       NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Wo, d, d, e));
 
-      NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                   [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), Rp, d, eps, s, ctl, K); }));
+      if (!fold)
+        NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                     [&] { return nt::layernorm(m.dt, at(p.z), w.ln2, at(p.du), Rp, d, eps, s, ctl, K); }));
 
       e = nt::GemmEpi{};
       e.mode = nt::EPI_STORE;
@@ -827,7 +842,9 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.wscale = w.sq;
       e.out = at(p.dq);
       e.ldc = d;
-      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.Wq, d, d, e));
+      e.lnf_colsum = w.cq;
+      e.lnf_eps = eps;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, ln_in, d, w.Wq, d, d, e));
 
       const size_t cross_layer = (size_t)2 * st->B * st->S * d;   // elements per layer (K and V)
       nt::MhaArgs ma{};
@@ -861,8 +878,9 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.ldc = d;
       NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.datt), d, w.Woc, d, d, e));
 
-      NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                   [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), Rp, d, eps, s, ctl, K); }));
+      if (!fold)
+        NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                     [&] { return nt::layernorm(m.dt, at(p.z), w.ln3, at(p.du), Rp, d, eps, s, ctl, K); }));
 
       e = nt::GemmEpi{};
       e.mode = nt::EPI_RELU;
@@ -870,7 +888,9 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.wscale = w.s1;
       e.out = at(p.df);
       e.ldc = m.F;
-      NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.du), d, w.W1, m.F, d, e));
+      e.lnf_colsum = w.c1;
+      e.lnf_eps = eps;
+      NT_HIP(gemm_dec(NT_K_GEMM_DEC, ln_in, d, w.W1, m.F, d, e));
 
       e = nt::GemmEpi{};
       e.mode = nt::EPI_RESID;
@@ -881,9 +901,11 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.ldc = d;
       NT_HIP(gemm_dec(NT_K_GEMM_DEC, at(p.df), m.F, w.W2, d, m.F, e));
 
+      // the next layer's ln1 (unless folded into its QKV projection), or the output LN
       const float* next_ln = j + 1 < m.Ld ? m.dec[j + 1].ln1 : m.dec_out_ln;
-      NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
-                   [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), Rp, d, eps, s, ctl, K); }));
+      if (j + 1 == m.Ld || !fold)
+        NT_HIP(timed(NT_K_LN, s, 2.0 * R * d * eb, 8.0 * R * d,
+                     [&] { return nt::layernorm(m.dt, at(p.z), next_ln, at(p.du), Rp, d, eps, s, ctl, K); }));
     }
 
     // Tied output projection.  Its epilogue reduces each row to per-tile (max, sum exp,
@@ -1249,6 +1271,34 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     if (e != hipSuccess) return e;
     return hipMemcpyAsync(base + scale_off, keep_s.back().data(), keep_s.back().size() * 4, hipMemcpyHostToDevice, s);
   };
+  // A pre-norm LayerNorm folded into the projection it feeds (decoder layers, weights in
+  // the model dtype): LN(x) W + b = rstd (x W' - mean colsum(W')) + b' with
+  // W' = diag(gamma) W and b' = b + beta W.  W' (fp32 products) replaces W in the staging
+  // copy before packing, b' is summed in double, and the column sums come from the packed
+  // matrix, so they are those of the values the GEMM multiplies.
+  std::deque<std::vector<float>> keep_f;   // element references stay valid as it grows
+  auto folded = [&](size_t dev_w, size_t dev_b, size_t dev_c, size_t hw, size_t hb, size_t hln, int in,
+                    int outn) -> hipError_t {
+    const float* W = host_weights + hw;
+    const float* g = host_weights + hln;
+    const float* be = host_weights + hln + in;
+    keep_f.emplace_back((size_t)in * outn);
+    std::vector<float>& Wf = keep_f.back();
+    for (int k = 0; k < in; ++k)
+      for (int n = 0; n < outn; ++n) Wf[(size_t)k * outn + n] = g[k] * W[(size_t)k * outn + n];
+    keep_f.emplace_back(outn);
+    std::vector<float>& bf = keep_f.back();
+    for (int n = 0; n < outn; ++n) {
+      double acc = host_weights[hb + n];
+      for (int k = 0; k < in; ++k) acc += (double)be[k] * W[(size_t)k * outn + n];
+      bf[n] = (float)acc;
+    }
+    hipError_t e = hipMemcpyAsync(staging + hw, Wf.data(), Wf.size() * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = nt::pack_transpose(dt, staging + hw, base + dev_w, in, outn, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(base + dev_b, bf.data(), bf.size() * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = nt::packed_row_sums(dt, base + dev_w, outn, in, reinterpret_cast<float*>(base + dev_c), s);
+    return e;
+  };
   NT_HIP(nt::pack_convert(dt, staging + Lo.hE, base + Lo.E, (size_t)V * d, s));
   NT_HIP(vec(Lo.hist_ln, Lo.hhist, (size_t)(L + 1) * 2 * d));
   NT_HIP(vec(Lo.dlcl, Lo.hdlcl, (size_t)(L + 1) * (L + 2) / 2));
@@ -1277,18 +1327,24 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     const auto& D = Lo.dec[j];
     const auto& Hh = Lo.hdec[j];
     NT_HIP(vec(D.ln1, Hh.ln1, 2 * d));
-    NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d, D.sqkv));
-    NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
+    NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
+    NT_HIP(vec(D.ln3, Hh.ln3, 2 * d));
+    if (f8) {
+      NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d, D.sqkv));
+      NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
+      NT_HIP(mat(D.Wq, Hh.Wq, d, d, D.sq));
+      NT_HIP(vec(D.bq, Hh.bq, d));
+      NT_HIP(mat(D.W1, Hh.W1, d, F, D.s1));
+      NT_HIP(vec(D.b1, Hh.b1, F));
+    } else {
+      NT_HIP(folded(D.Wqkv, D.bqkv, D.cqkv, Hh.Wqkv, Hh.bqkv, Hh.ln1, d, 3 * d));
+      NT_HIP(folded(D.Wq, D.bq, D.cq, Hh.Wq, Hh.bq, Hh.ln2, d, d));
+      NT_HIP(folded(D.W1, D.b1, D.c1, Hh.W1, Hh.b1, Hh.ln3, d, F));
+    }
     NT_HIP(mat(D.Wo, Hh.Wo, d, d, D.so));
     NT_HIP(vec(D.bo, Hh.bo, d));
-    NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
-    NT_HIP(mat(D.Wq, Hh.Wq, d, d, D.sq));
-    NT_HIP(vec(D.bq, Hh.bq, d));
     NT_HIP(mat(D.Woc, Hh.Woc, d, d, D.soc));
     NT_HIP(vec(D.boc, Hh.boc, d));
-    NT_HIP(vec(D.ln3, Hh.ln3, 2 * d));
-    NT_HIP(mat(D.W1, Hh.W1, d, F, D.s1));
-    NT_HIP(vec(D.b1, Hh.b1, F));
     NT_HIP(mat(D.W2, Hh.W2, F, d, D.s2));
     NT_HIP(vec(D.b2, Hh.b2, d));
     // cross K/V projections of all layers stacked into one [Ld*2d][d] matrix
@@ -1343,6 +1399,12 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     const auto& D = Lo.dec[j];
     m->dec.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.bq), fp(D.boc), fp(D.ln3), fp(D.b1), fp(D.b2),
                       base + D.Wqkv, base + D.Wo, base + D.Wq, base + D.Woc, base + D.W1, base + D.W2});
+    if (!f8) {
+      DecLayerW& w = m->dec.back();
+      w.cqkv = fp(D.cqkv);
+      w.cq = fp(D.cq);
+      w.c1 = fp(D.c1);
+    }
     if (f8) {
       DecLayerW& w = m->dec.back();
       w.sqkv = fp(D.sqkv);
@@ -1730,6 +1792,29 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
   e.ldc = ldc;
   e.out_f32 = out_f32 ? 1 : 0;
   NT_HIP(nt::gemm(static_cast<DT>(dtype), d_A, lda, d_Bt, M, N, K, e, static_cast<hipStream_t>(stream), 0, tile));
+  return NT_OK;
+}
+
+nt_status nt_op_gemm_ln(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N,
+                        int32_t K, const float* d_colsum, float ln_eps, const float* d_bias, void* d_out,
+                        int32_t ldc, int32_t relu, int32_t tile, void* stream) {
+  g_err.clear();
+  if (!d_A || !d_Bt || !d_out || !d_colsum) return fail(NT_E_INVALID, "null argument to nt_op_gemm_ln");
+  if (dtype < NT_F32 || dtype > NT_BF16) return fail(NT_E_INVALID, "unknown dtype %d", dtype);
+  if (M < 0 || N <= 0 || K <= 0 || K % 64 != 0) return fail(NT_E_UNSUPPORTED, "need N > 0, K > 0, K %% 64 == 0");
+  const int eb = dtype == NT_F32 ? 4 : 2;
+  if (lda < K || (lda * eb) % 16 != 0 || ldc < N)
+    return fail(NT_E_INVALID, "lda must be >= K with 16-byte rows, ldc >= N");
+  if (tile < 0 || tile > 4) return fail(NT_E_INVALID, "tile must be 0..4");
+  if (!(ln_eps > 0.f)) return fail(NT_E_INVALID, "ln_eps must be positive");
+  nt::GemmEpi e{};
+  e.mode = relu ? nt::EPI_RELU : nt::EPI_STORE;
+  e.bias = d_bias;
+  e.out = d_out;
+  e.ldc = ldc;
+  e.lnf_colsum = d_colsum;
+  e.lnf_eps = ln_eps;
+  NT_HIP(nt::gemm(static_cast<DT>(dtype), d_A, lda, d_Bt, M, N, K, e, static_cast<hipStream_t>(stream), 1, tile));
   return NT_OK;
 }
 

@@ -29,7 +29,7 @@ EXPORTS = [
     "nt_weights_size", "nt_load_weights", "nt_free_model", "nt_workspace_size", "nt_translate_workspace_size",
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
-    "nt_op_gemm", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units", "nt_op_select",
+    "nt_op_gemm", "nt_op_gemm_ln", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units", "nt_op_select",
     "nt_op_select_tiled",
     "nt_ensemble", "nt_quantize_fp8",
 ]
@@ -103,6 +103,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_prof_get": (c_int32, [c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
         "nt_op_gemm": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, P, P, c_int32, c_int32, c_int32,
                                  c_int32, P, P]),
+        "nt_op_gemm_ln": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, c_float, P, P, c_int32,
+                                    c_int32, c_int32, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -253,6 +255,14 @@ def nt_op_gemm(dtype: str, d_A: int, lda: int, d_Bt: int, M: int, N: int, K: int
                                      c_void_p(d_bias) if d_bias else None, c_void_p(d_resid) if d_resid else None,
                                      c_void_p(d_out), ldc, int(out_f32), int(relu), tile,
                                      c_void_p(d_bscale) if d_bscale else None, _stream(stream)))
+
+
+def nt_op_gemm_ln(dtype: str, d_A: int, lda: int, d_Bt: int, M: int, N: int, K: int, d_colsum: int, ln_eps: float,
+                  d_bias, d_out: int, ldc: int, relu: bool = False, tile: int = 0, stream=None):
+    _check(load_library().nt_op_gemm_ln(DTYPES[dtype], c_void_p(d_A), lda, c_void_p(d_Bt), M, N, K,
+                                        c_void_p(d_colsum), float(ln_eps),
+                                        c_void_p(d_bias) if d_bias else None, c_void_p(d_out), ldc, int(relu),
+                                        tile, _stream(stream)))
 
 
 def nt_quantize_fp8(w: np.ndarray):

@@ -1,0 +1,115 @@
+"""GPU: the projection with its pre-norm LayerNorm folded in (nt_op_gemm_ln).
+
+The kernel sums each row of A and its squares during the k-loop and forms
+rstd * (A.Bt - mean * colsum) + bias.  The reference normalises A in fp64 first
+(biased variance, Sec. 2.1's pre-norm LayerNorm with unit gain and zero bias) and
+multiplies after, so an error in the row statistics, the column sums or the row/column
+bookkeeping of the epilogue shows up as an O(1) difference.  Rows carry a non-zero
+mean so that the mean term matters.  A second test checks the algebra the weight loader
+relies on: with Bt = (diag(gamma) W)^T and bias b + beta W the result is LN(A) W + b.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+TORCH_DT = {"f32": "float32", "f16": "float16", "bf16": "bfloat16"}
+ULP = {"f32": 2.0 ** -23, "f16": 2.0 ** -10, "bf16": 2.0 ** -7}
+EPS = 1e-5
+
+
+def _rows(M, K, seed, tdt):
+    import torch
+    g = torch.Generator().manual_seed(seed)
+    mean = torch.randn(M, 1, generator=g) * 0.5
+    scale = torch.rand(M, 1, generator=g) * 1.5 + 0.25
+    return (torch.randn(M, K, generator=g) * scale + mean).to(tdt)
+
+
+def _run(dtype, A, Bt, colsum, bias=None, relu=False, tile=0):
+    import torch
+    from paper_2109_08008_amd import nt
+    M, K = A.shape
+    N = Bt.shape[0]
+    dA, dB, dc = A.cuda(), Bt.cuda(), colsum.float().cuda()
+    db = bias.float().cuda() if bias is not None else None
+    out = torch.full((M, N), float("nan"), dtype=A.dtype, device="cuda")
+    nt.nt_op_gemm_ln(dtype, dA.data_ptr(), K, dB.data_ptr(), M, N, K, dc.data_ptr(), EPS,
+                     db.data_ptr() if db is not None else 0, out.data_ptr(), N, relu, tile)
+    torch.cuda.synchronize()
+    return out.cpu()
+
+
+def _ln64(A):
+    a = A.double()
+    mu = a.mean(dim=1, keepdim=True)
+    var = ((a - mu) ** 2).mean(dim=1, keepdim=True)
+    return (a - mu) / (var + EPS).sqrt()
+
+
+@pytest.mark.parametrize("tile", [0, 1, 3, 4])
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (37, 100, 512), (200, 520, 128), (300, 1000, 1024), (129, 136, 576)])
+def test_folded_ln_gemm_matches_fp64(dtype, tile, M, N, K):
+    import torch
+    tdt = getattr(torch, TORCH_DT[dtype])
+    g = torch.Generator().manual_seed(M * 3 + N + K)
+    A = _rows(M, K, M + 7 * N + K, tdt)
+    Bt = (torch.randn(N, K, generator=g) * 0.05).to(tdt)
+    bias = torch.randn(N, generator=g)
+    colsum = Bt.double().sum(dim=1)
+    ref = _ln64(A) @ Bt.double().T
+    for mode in ("plain", "bias", "relu"):
+        want = ref.clone()
+        kw = {}
+        if mode != "plain":
+            kw["bias"] = bias
+            want = want + bias.double()
+        if mode == "relu":
+            kw["relu"] = True
+            want = want.clamp_min(0)
+        got = _run(dtype, A, Bt, colsum, tile=tile, **kw)
+        assert not torch.isnan(got).any(), mode
+        # output rounding, plus fp32 accumulation and the one-pass variance, scaled by
+        # rstd (at most 4 here) and the row mean's share of the product
+        mu = A.double().mean(dim=1).abs().max().item()
+        tol = want.abs().max().item() * ULP[dtype] + 64 * 2.0 ** -24 * K * np.sqrt(K) * (1 + mu)
+        err = (got.double() - want).abs().max().item()
+        assert err <= tol, (mode, err, tol)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_folded_weights_give_layernorm_then_projection(dtype):
+    """Bt = (diag(gamma) W)^T rounded to the dtype, colsum from those values and bias
+    b + beta W: the result is LN(A; gamma, beta) W + b."""
+    import torch
+    tdt = getattr(torch, TORCH_DT[dtype])
+    M, K, N = 150, 512, 384
+    g = torch.Generator().manual_seed(11)
+    A = _rows(M, K, 12, tdt)
+    W = torch.randn(K, N, generator=g, dtype=torch.float64) * 0.05
+    gamma = 1.0 + 0.3 * torch.randn(K, generator=g, dtype=torch.float64)
+    beta = 0.3 * torch.randn(K, generator=g, dtype=torch.float64)
+    b = torch.randn(N, generator=g, dtype=torch.float64)
+    Bt = (gamma[:, None] * W).T.contiguous().to(tdt)
+    colsum = Bt.double().sum(dim=1)
+    bias = b + beta @ W
+    got = _run(dtype, A, Bt, colsum, bias=bias)
+    want = (_ln64(A) * gamma + beta) @ W + b
+    # the folded weights are rounded once to the dtype (relative ULP of each product)
+    tol = want.abs().max().item() * ULP[dtype] + 4 * ULP[dtype] * np.sqrt(K) * 0.05 * 4 + 1e-4
+    err = (got.double() - want).abs().max().item()
+    assert err <= tol, (err, tol)
+
+
+def test_folded_ln_rows_do_not_depend_on_tile_or_batch():
+    import torch
+    A = _rows(700, 512, 3, torch.float16)
+    g = torch.Generator().manual_seed(4)
+    Bt = (torch.randn(384, 512, generator=g) * 0.05).half()
+    colsum = Bt.double().sum(dim=1)
+    bias = torch.randn(384, generator=g)
+    full = _run("f16", A, Bt, colsum, bias=bias, tile=4)
+    for tile in (1, 3):
+        assert torch.equal(_run("f16", A, Bt, colsum, bias=bias, tile=tile), full)
+    assert torch.equal(_run("f16", A[100:133].contiguous(), Bt, colsum, bias=bias, tile=1), full[100:133])
