@@ -154,7 +154,8 @@ hipError_t dlcl_combine(DT dt, const DlclArgs& a, hipStream_t s);
 hipError_t layernorm(DT dt, const void* x, const float* ln, void* y, int rows, int d, float eps, hipStream_t s,
                      const int* ctl = nullptr, int ctl_rows = 1);
 
-// Decoder step input: z[r] = emb_scale*E[tok[phys(r)]] + pe[t]; u[r] = LN(z[r]); rows and t
+// Decoder step input: z[r] = emb_scale*E[tok[phys(r)]] + pe[t]; u[r] = LN(z[r]) unless u is
+// null (then ln is not read); rows and t
 // from ctl (rows = ctl[CTL_NLIVE] * beam, t = ctl[CTL_T]), `rows` being the launch maximum.
 hipError_t dec_embed_ln(DT dt, const int* cur_tok, const int* sent_list, int beam, const void* E,
                         const float* pe, const int* ctl, float emb_scale, const float* ln, void* z, void* u,

@@ -151,7 +151,8 @@ __global__ __launch_bounds__(256) void ln_kernel(const T* __restrict__ x, const 
   if (row < live) store_row<T, EPL>(y + (size_t)row * d + c0, o);
 }
 
-// Decoder input of step t for live row r: z = sqrt(d) E[tok] + PE(t), u = LN(z).
+// Decoder input of step t for live row r: z = sqrt(d) E[tok] + PE(t), u = LN(z) (u and ln
+// null when the first layer's projection normalises its input itself).
 // Every row of the grid computes (its list entry and token are valid IDs whether or not
 // the row is live), and the live-row count gates only the stores: so the count, the list
 // entry and the gain/bias are in flight together instead of one after another.
@@ -168,7 +169,7 @@ __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ 
   if (row >= rows) return;
   const int c0 = (threadIdx.x % kWave) * EPL;
   LnCols<EPL> lc;
-  load_ln_cols<EPL>(ln, ln + d, c0, lc);
+  if (u) load_ln_cols<EPL>(ln, ln + d, c0, lc);
   const int sent = sent_list[row / beam], t = ctl[CTL_T], nlive = ctl[CTL_NLIVE];
   asm volatile("" ::"v"(sent), "v"(t), "v"(nlive));   // both loads issued before either is waited on
   const int p = sent * beam + row % beam;
@@ -179,6 +180,7 @@ __global__ __launch_bounds__(256) void dec_embed_kernel(const int* __restrict__ 
 #pragma unroll
   for (int i = 0; i < EPL; ++i) v[i] = to_f32(from_f32<T>(scale * v[i] + pr[i]));
   if (live) store_row<T, EPL>(z + (size_t)row * d + c0, v);
+  if (!u) return;
   wave_layernorm<EPL>(v, o, lc, 1.0f / (float)d, eps);
   if (live) store_row<T, EPL>(u + (size_t)row * d + c0, o);
 }

@@ -774,9 +774,11 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       return timed(cls, s, bytes, 2.0 * R * N * Kd, [&] { return nt::gemm(m.dt, A, lda, W, Rp, N, Kd, ec, s, role, tile); });
     };
 
-    NT_HIP(timed(NT_K_LN, s, 3.0 * R * d * eb, 8.0 * R * d, [&] {
-      return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, ctl, std::sqrt((float)d), m.dec[0].ln1,
-                              at(p.z), at(p.du), Rp, d, eps, s);
+    // the first layer's ln1 output only when its QKV projection does not normalise itself
+    const bool fold0 = m.dec[0].cqkv != nullptr;
+    NT_HIP(timed(NT_K_LN, s, (fold0 ? 2.0 : 3.0) * R * d * eb, 8.0 * R * d, [&] {
+      return nt::dec_embed_ln(m.dt, st->at<int>(p.cur_tok), list, K, m.E, m.pe, ctl, std::sqrt((float)d),
+                              fold0 ? nullptr : m.dec[0].ln1, at(p.z), fold0 ? nullptr : at(p.du), Rp, d, eps, s);
     }));
 
     for (int j = 0; j < m.Ld; ++j) {

@@ -724,6 +724,11 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
     rs[c] = 0.f;
     if (c * kWave < ncand) rs[c] = st.score[b * K + min(lane + c * kWave, ncand - 1) / K2];
   }
+  // the sentence's best finished hypothesis and length limit arrive with the flag and
+  // the scores; the serial update below keeps them in registers and stores them once
+  int bf_nout = st.best_nout[b], bf_step = st.best_step[b], bf_row = st.best_row[b];
+  float bf_score = st.best_score[b], bf_raw = st.best_raw[b];
+  const int maxlen_b = st.maxlen[b];
   asm volatile("" ::"v"(done));
   if (done) return;
 
@@ -777,12 +782,12 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
       const int ppar = b * K + k;
       if (w == st.eos) {
         const float s = c / lpn;
-        if (st.best_nout[b] < 0 || s > st.best_score[b]) {
-          st.best_score[b] = s;
-          st.best_raw[b] = c;
-          st.best_step[b] = t - 1;
-          st.best_row[b] = ppar;
-          st.best_nout[b] = t;
+        if (bf_nout < 0 || s > bf_score) {
+          bf_score = s;
+          bf_raw = c;
+          bf_step = t - 1;
+          bf_row = ppar;
+          bf_nout = t;
         }
       } else if (nk < K) {
         nk_score[nk] = c;
@@ -807,23 +812,28 @@ __global__ __launch_bounds__(256) void beam_update_kernel(const float* __restric
       }
     }
     int done = 0;
-    if (n >= st.maxlen[b]) {
+    if (n >= maxlen_b) {
       for (int k = 0; k < nk; ++k) {
         const float s = nk_score[k] / lpn;
-        if (st.best_nout[b] < 0 || s > st.best_score[b]) {
-          st.best_score[b] = s;
-          st.best_raw[b] = nk_score[k];
-          st.best_step[b] = t;
-          st.best_row[b] = b * K + k;
-          st.best_nout[b] = t + 1;
+        if (bf_nout < 0 || s > bf_score) {
+          bf_score = s;
+          bf_raw = nk_score[k];
+          bf_step = t;
+          bf_row = b * K + k;
+          bf_nout = t + 1;
         }
       }
       done = 1;
-    } else if (st.early_stop && st.best_nout[b] >= 0 && st.best_score[b] >= mx / lpn) {
+    } else if (st.early_stop && bf_nout >= 0 && bf_score >= mx / lpn) {
       done = 1;
     } else if (nk == 0) {
       done = 1;
     }
+    st.best_score[b] = bf_score;
+    st.best_raw[b] = bf_raw;
+    st.best_step[b] = bf_step;
+    st.best_row[b] = bf_row;
+    st.best_nout[b] = bf_nout;
     st.done[b] = done;
     nk_cnt[wave] = done ? 0 : nk;
   }
