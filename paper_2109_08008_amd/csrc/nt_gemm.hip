@@ -53,26 +53,32 @@ __device__ __forceinline__ u32x4 f8_to_f16x8(unsigned w0, unsigned w1) {
 }
 
 // Sum and sum of squares of the eight (fp16/bf16) or four (fp32) values of one 16-byte
-// operand fragment, added into s and q in fp32: the row statistics of a folded LayerNorm.
+// operand fragment, each taken relative to the row's shift c (one of the row's own
+// values), added into s and q in fp32: the row statistics of a folded LayerNorm.  With
+// the shift, the variance (q/K - (s/K)^2) no longer cancels when the row's mean is large
+// against its spread: the deviations from c are of the size of the spread.  For fp16 the
+// deviation is formed in fp16 (exact whenever x and c are within a factor of two, which is
+// where cancellation would matter), then squared and summed by fdot2 in fp32.
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 template <typename T>
-__device__ __forceinline__ void frag_stats(const u32x4& a, float& s, float& q) {
+__device__ __forceinline__ void frag_stats(const u32x4& a, T c, float& s, float& q) {
 #pragma unroll
   for (int w = 0; w < 4; ++w) {
     if constexpr (std::is_same<T, f16>::value) {
       // the word is copied out first: a bit_cast of the vector element itself read word 0
       const unsigned u = a[w];
-      const half2v h = __builtin_bit_cast(half2v, u);
+      const half2v h = __builtin_bit_cast(half2v, u) - half2v{c, c};
       s = __builtin_amdgcn_fdot2(h, half2v{(_Float16)1.0f, (_Float16)1.0f}, s, false);
       q = __builtin_amdgcn_fdot2(h, h, q, false);
     } else if constexpr (std::is_same<T, bf16>::value) {
-      const float lo = __uint_as_float(a[w] << 16), hi = __uint_as_float(a[w] & 0xffff0000u);
+      const float cf = to_f32(c);
+      const float lo = __uint_as_float(a[w] << 16) - cf, hi = __uint_as_float(a[w] & 0xffff0000u) - cf;
       s += lo;
       s += hi;
       q = fmaf(lo, lo, q);
       q = fmaf(hi, hi, q);
     } else {
-      const float x = __uint_as_float(a[w]);
+      const float x = __uint_as_float(a[w]) - to_f32(c);
       s += x;
       q = fmaf(x, x, q);
     }
@@ -475,14 +481,18 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
 
   // folded LayerNorm: lane (fr, fc) sums the k-chunks fc and 4+fc of its fragment rows
   // over every k-step; the four lanes of a row together see each of its K values once.
-  // The lane's column sums (its output column is fixed per 16x16 block) are fetched here,
-  // so their latency hides behind the k-loop instead of stalling the epilogue.
+  // The lane's column sums (its output column is fixed per 16x16 block) and its rows'
+  // shifts (each row's first value, the same for the four lanes of a row) are fetched
+  // here, so their latency hides behind the k-loop instead of stalling it.
   float lsum[LNF ? FM : 1], lsq[LNF ? FM : 1], lcs[LNF ? FN : 1];
+  T lsh[LNF ? FM : 1];
 #pragma unroll
   for (int i = 0; i < (LNF ? FM : 1); ++i) lsum[i] = lsq[i] = 0.f;
   if constexpr (LNF) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) lcs[j] = epi.lnf_colsum[min(n0 + wn * WN + j * 16 + fr, N - 1)];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) lsh[i] = A[(size_t)min(m0 + wm * WM + i * 16 + fr, M - 1) * lda];
   }
 
   const int nk = (int)((size_t)K * sizeof(T) / ROWB);
@@ -529,7 +539,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af0[i], bf0[j], acc[i][j]);
     if constexpr (LNF) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i) frag_stats<T>(af0[i], lsum[i], lsq[i]);
+      for (int i = 0; i < FM; ++i) frag_stats<T>(af0[i], lsh[i], lsum[i], lsq[i]);
     }
     __builtin_amdgcn_sched_barrier(0);   // keep the second wait behind the first half's MFMAs
     LdsWait<FM, FN>::template run<0>(af1, bf1);
@@ -539,14 +549,15 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       for (int j = 0; j < FN; ++j) acc[i][j] = Mfma<T>::step(af1[i], bf1[j], acc[i][j]);
     if constexpr (LNF) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i) frag_stats<T>(af1[i], lsum[i], lsq[i]);
+      for (int i = 0; i < FM; ++i) frag_stats<T>(af1[i], lsh[i], lsum[i], lsq[i]);
     }
     slot = slot == STAGES - 1 ? 0 : slot + 1;
   }
 #undef NT_ISSUE
-  // folded LayerNorm: each row's mean and 1/sqrt(biased variance + eps), one pass over
-  // the fragments (E[x^2] - mean^2 in fp32), kept per tile row for the epilogue
-  // (the accumulators become rstd * (acc - mean * colsum[n]) as they enter the epilogue)
+  // folded LayerNorm: each row's mean and 1/sqrt(biased variance + eps) from the sums of
+  // its deviations from the shift c (mean = c + s/K, variance = q/K - (s/K)^2, fp32),
+  // kept per tile row for the epilogue (the accumulators become
+  // rstd * (acc - mean * colsum[n]) as they enter the epilogue)
   float* ln_mu = nullptr;
   float* ln_rs = nullptr;
   if constexpr (LNF) {
@@ -562,9 +573,9 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       s += __shfl_xor(s, 32, kWave);
       q += __shfl_xor(q, 32, kWave);
       if (wn == 0 && fc == 0) {
-        const float mu = s * inv_k;
-        const float var = fmaxf(q * inv_k - mu * mu, 0.f);
-        ln_mu[wm * WM + i * 16 + fr] = mu;
+        const float ms = s * inv_k;
+        const float var = fmaxf(q * inv_k - ms * ms, 0.f);
+        ln_mu[wm * WM + i * 16 + fr] = to_f32(lsh[i]) + ms;
         ln_rs[wm * WM + i * 16 + fr] = 1.0f / sqrtf(var + epi.lnf_eps);
       }
     }

@@ -1,7 +1,7 @@
 """GPU: the projection with its pre-norm LayerNorm folded in (nt_op_gemm_ln).
 
-The kernel sums each row of A and its squares during the k-loop and forms
-rstd * (A.Bt - mean * colsum) + bias.  The reference normalises A in fp64 first
+The kernel sums each row's deviations from one of its own values, and their squares,
+during the k-loop and forms rstd * (A.Bt - mean * colsum) + bias.  The reference normalises A in fp64 first
 (biased variance, Sec. 2.1's pre-norm LayerNorm with unit gain and zero bias) and
 multiplies after, so an error in the row statistics, the column sums or the row/column
 bookkeeping of the epilogue shows up as an O(1) difference.  Rows carry a non-zero
@@ -70,8 +70,8 @@ def test_folded_ln_gemm_matches_fp64(dtype, tile, M, N, K):
             want = want.clamp_min(0)
         got = _run(dtype, A, Bt, colsum, tile=tile, **kw)
         assert not torch.isnan(got).any(), mode
-        # output rounding, plus fp32 accumulation and the one-pass variance, scaled by
-        # rstd (at most 4 here) and the row mean's share of the product
+        # output rounding, plus fp32 accumulation scaled by rstd (at most 4 here) and the
+        # row mean's share of the product (A.Bt - mean * colsum cancels that share)
         mu = A.double().mean(dim=1).abs().max().item()
         tol = want.abs().max().item() * ULP[dtype] + 64 * 2.0 ** -24 * K * np.sqrt(K) * (1 + mu)
         err = (got.double() - want).abs().max().item()
@@ -113,3 +113,32 @@ def test_folded_ln_rows_do_not_depend_on_tile_or_batch():
     for tile in (1, 3):
         assert torch.equal(_run("f16", A, Bt, colsum, bias=bias, tile=tile), full)
     assert torch.equal(_run("f16", A[100:133].contiguous(), Bt, colsum, bias=bias, tile=1), full[100:133])
+
+
+@pytest.mark.parametrize("tile", [1, 3, 4])
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("M,N,K", [(37, 100, 64), (200, 520, 512), (129, 136, 1024)])
+def test_folded_ln_large_mean_rows(dtype, tile, M, N, K):
+    """Rows whose mean is more than 100 times their spread (|mu| in [45, 55], sigma in
+    [0.2, 0.4]): the row statistics must not cancel, so the result is held to the plain
+    projection's bound (output rounding plus 8 * 2^-24 * K^1.5), with no term growing with
+    the mean."""
+    import torch
+    tdt = getattr(torch, TORCH_DT[dtype])
+    g = torch.Generator().manual_seed(M + 5 * N + K)
+    sign = torch.where(torch.rand(M, 1, generator=g) < 0.5, -1.0, 1.0)
+    mean = sign * (45.0 + 10.0 * torch.rand(M, 1, generator=g))
+    sd = 0.2 + 0.2 * torch.rand(M, 1, generator=g)
+    A = (torch.randn(M, K, generator=g) * sd + mean).to(tdt)
+    a64 = A.double()
+    spread = a64.std(dim=1, unbiased=False)
+    assert (a64.mean(dim=1).abs() / spread).min().item() >= 100.0
+    Bt = (torch.randn(N, K, generator=g) * 0.05).to(tdt)
+    colsum = Bt.double().sum(dim=1)
+    bias = torch.randn(N, generator=g)
+    want = _ln64(A) @ Bt.double().T + bias.double()
+    got = _run(dtype, A, Bt, colsum, bias=bias, tile=tile)
+    assert not torch.isnan(got).any()
+    tol = want.abs().max().item() * ULP[dtype] + 8 * 2.0 ** -24 * K * np.sqrt(K)
+    err = (got.double() - want).abs().max().item()
+    assert err <= tol, (err, tol)
