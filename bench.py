@@ -5,15 +5,19 @@ One step = one nt_translate call over the whole synthetic workload (sorting, dyn
 batching, DLCL encoder, cached decoder steps, search, pruning, results back in host
 memory), with inputs and weights generated beforehand.  Prints one JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload base-6-6]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload wide-30-6]
 
-Batches are decoded four at a time on their own streams (the library default), each
-decoder step replayed from a captured HIP graph.  The line carries a roofline entry for
-the dominant kernel class, timed with HIP events on the launch stream inside the timed
-region: about 12 units (decoder steps or batch encodes) are sampled, and each sample
-runs alone on the GPU so that its kernel durations are the kernel's own, as a
-kernel-trace profiler reports them.  It also carries the CPU oracle's throughput on a
-bounded sample of the same workload (the oracle as written, one process per core).
+The default workload is the largest configuration, the wide teacher-size model (d = 1024,
+30-layer DLCL encoder, 6-layer decoder, beam 4, 4096 sentences).  Batches are decoded four
+at a time on their own streams (the library default), each decoder step replayed from a
+captured HIP graph.  The line carries a roofline entry for the dominant kernel class,
+timed with HIP events on the launch stream inside the timed region: about 48 units
+(decoder steps or batch encodes) are sampled, and each sample runs alone on the GPU so
+that its kernel durations are the kernel's own.  Next to that per-launch rate the entry
+gives the class's algorithmic work per translation over the timed step's wall time
+(`in_pipeline`), and how much kernel time the concurrent batches overlap (`overlap`).
+It also carries the CPU oracle's throughput on a bounded sample of the same workload
+(the oracle as written, one process per core).
 """
 from __future__ import annotations
 
@@ -73,18 +77,22 @@ def parse_args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="base-6-6", choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--workload", default="wide-30-6", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graphs", action="store_true", help="launch decoder steps kernel by kernel")
     ap.add_argument("--streams", type=int, default=0, help="batches decoded concurrently (0: library default)")
-    ap.add_argument("--samples", type=int, default=12, help="timing samples (isolated units) in the timed region")
+    ap.add_argument("--samples", type=int, default=48, help="timing samples (isolated units) in the timed region")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work for the oracle sample")
     ap.add_argument("--cpu-procs", type=int, default=0, help="oracle processes (0: min(16, cores))")
+    ap.add_argument("--cpu-full", action="store_true",
+                    help="time the oracle on the whole sentence set instead of a bounded sample (slow)")
     return ap.parse_args()
 
 
 def roofline_entry(cls: int, prof: dict, dtype: str, workload: str) -> dict:
-    """Roofline of one kernel class from its event timings and algorithmic work."""
+    """Roofline of one kernel class from its event timings and algorithmic work.  The
+    bound follows the class's algorithmic intensity (flops over the bytes the method must
+    move: weights, keys/values, logits) against the ridge of the peaks."""
     from paper_2109_08008_amd import nt
     n = max(prof["launches"], 1)
     sec = prof["ms"] / 1e3
@@ -125,7 +133,8 @@ def phase_rooflines(breakdown: dict, dtype: str) -> dict:
                               "frac": round(enc_tf / PEAK["mfma_TFLOPs"][dtype], 4)},
         "decode_step_hbm": {"achieved": round(dec_gbs, 2), "peak": PEAK["hbm_GBps"], "unit": "GB/s",
                             "frac": round(dec_gbs / PEAK["hbm_GBps"], 4),
-                            "note": "algorithmic bytes of the decoder-step kernel classes / their kernel time"},
+                            "note": "algorithmic bytes of the decoder-step kernel classes (weights, keys/values, "
+                                    "logits) / their kernel time"},
     }
 
 
@@ -177,9 +186,9 @@ def _oracle_worker(idx):
         return len(_oracle_translate(_ORACLE["srcs"][idx]).tokens)
 
 
-def cpu_baseline(w: synth.Workload, blobs, ids, offs, seconds: float, procs: int) -> dict:
-    """The fp32 oracle on a length-stratified sample, split over processes (one BLAS
-    thread each) the way the paper splits CPU decoding by lines."""
+def cpu_baseline(w: synth.Workload, blobs, ids, offs, seconds: float, procs: int, full: bool = False) -> dict:
+    """The fp32 oracle on a length-stratified sample (or, with full, every sentence), split
+    over processes (one BLAS thread each) the way the paper splits CPU decoding by lines."""
     import multiprocessing as mp
     import oracle
     from threadpoolctl import threadpool_limits
@@ -198,7 +207,7 @@ def cpu_baseline(w: synth.Workload, blobs, ids, offs, seconds: float, procs: int
         t0 = time.perf_counter()
         _oracle_translate(srcs[probe])
         t_one = time.perf_counter() - t0
-    n = int(min(len(srcs), max(P, P * max(1, math.floor(seconds / max(t_one, 1e-3))))))
+    n = len(srcs) if full else int(min(len(srcs), max(P, P * max(1, math.floor(seconds / max(t_one, 1e-3))))))
     sample = synth.stratified_subset(offs, n)
     ctx = mp.get_context("fork")
     with ctx.Pool(P) as pool:
@@ -209,6 +218,7 @@ def cpu_baseline(w: synth.Workload, blobs, ids, offs, seconds: float, procs: int
         "value": round(sum(toks) / dt, 2), "unit": "tokens/s", "cores": P, "kind": "oracle",
         "sample": f"{n} of {len(srcs)} sentences, every ({len(srcs)}/{n})-th of the length-sorted order; "
                   f"fp32 NumPy oracle, {P} processes x 1 BLAS thread; {sum(toks)} target tokens in {dt:.1f} s",
+        "host_cpu_count": os.cpu_count(),
     }
 
 
@@ -276,8 +286,25 @@ def main():
     elapsed = t1 - t0
     value = n_tokens * args.steps / elapsed
 
+    # the dominant class inside the timed run: its algorithmic work per translation (every
+    # launch, from the all-unit profile) over the timed step's wall time; and how much of
+    # the kernels' own time the concurrent batches hide
+    dom = breakdown[nt.KERNEL_CLASSES[dominant]]
+    rl = roofline_entry(dominant, prof, w.dtype, w.name)
+    step_s = elapsed / args.steps
+    work = dom["flops"] if rl["bound"] == "mfma" else dom["bytes"]
+    pipe = work / step_s / (1e12 if rl["bound"] == "mfma" else 1e9)
+    rl["in_pipeline"] = {
+        "achieved": round(pipe, 2), "frac": round(pipe / rl["peak"], 4),
+        "note": "the class's algorithmic work per translation (all its launches) / the timed step's wall time",
+    }
+    rl["overlap"] = round(sum(v["ms"] for v in breakdown.values()) / (step_s * 1e3), 3)
+    rl["sampled_units_stride"] = stride
+    rl["timing"] = ("HIP events around every launch of the class in the sampled units of the timed region, "
+                    "each unit run alone on the GPU")
+
     line = {
-        "metric": "target tokens/sec translated (1 GPU)",
+        "metric": "target tokens/sec translated (fp16, 1 GPU); encoder MFMA util; decode HBM GB/s",
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -297,7 +324,7 @@ def main():
             "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 4,
             "workspace_GB": round(ws_bytes / 1e9, 2),
         },
-        "roofline": dict(roofline_entry(dominant, prof, w.dtype, w.name), sampled_units_stride=stride),
+        "roofline": rl,
         "phase_rooflines": phase_rooflines(breakdown, w.dtype),
         "achievable_peaks": peaks,
         "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},
@@ -307,7 +334,7 @@ def main():
                                      f"{f'+RPR{mb.model.rel_k}' if mb.model.rel_k else ''}" for mb in w.members]
         line["config"]["ensemble_rule"] = ["mean log-prob", "log mean prob"][w.ensemble_rule]
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w, blobs, ids, offs, args.cpu_seconds, args.cpu_procs)
+        line["cpu_baseline"] = cpu_baseline(w, blobs, ids, offs, args.cpu_seconds, args.cpu_procs, args.cpu_full)
     else:
         line["cpu_baseline"] = None
     model.close()

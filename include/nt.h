@@ -86,7 +86,9 @@ typedef struct {
 /* Search and batching options.
  *  beam: 1 = greedy (Sec. 4.4), 2..16 = beam search (Sec. 4.1).
  *  len_penalty: alpha of lp(n) = ((5+n)/6)^alpha applied to finished/final scores; 0 = raw.
- *  max target tokens of sentence i (EOS counted) = floor(max_len_a * len_i) + max_len_b.
+ *  max target tokens of sentence i (EOS counted) = floor(max_len_a * len_i) + max_len_b,
+ *    lowered to max_len_cap when max_len_cap > 0 (Sec. 4.4 caps targets at 200 tokens;
+ *    0 = no cap).
  *  token_budget: dynamic batching (Sec. 4.2) packs sentences, longest first, while
  *    n_sentences * longest_length <= token_budget (padded source tokens).
  *  max_batch_sents: 0 = no cap; otherwise at most this many sentences per batch.
@@ -99,6 +101,7 @@ typedef struct {
   float len_penalty;
   float max_len_a;
   int32_t max_len_b;
+  int32_t max_len_cap;
   int32_t token_budget;
   int32_t max_batch_sents;
   int32_t early_stop;
@@ -121,7 +124,10 @@ typedef struct {
 
 /* Sizes for a model: host_floats = length of the fp32 blob; device_bytes = size of the
  * device buffer nt_load_weights needs.  Returns NT_E_INVALID / NT_E_UNSUPPORTED for a
- * shape the library cannot run. */
+ * shape the library cannot run.
+ * Defined by: the model of Sec. 2.1 (pre-norm Transformer whose encoder layers are
+ * combined by Eq. 1-2) with tied embeddings (Sec. 2.2); the blob's matrix parameters add
+ * up to the counts of Tables 1 and 2 (152M for 35-6, 131M for 35-1, 49M for 9-1). */
 nt_status nt_weights_size(const nt_model_cfg* cfg, size_t* host_floats, size_t* device_bytes);
 
 /* Converts the host blob into the device layout: matrices rounded (nearest even) to the
@@ -129,9 +135,15 @@ nt_status nt_weights_size(const nt_model_cfg* cfg, size_t* host_floats, size_t* 
  * column scales) and stored transposed ([out][in]) for the GEMMs, vectors kept in fp32, a
  * sinusoidal position table computed once.  device_buf (>= device_bytes, 256-byte
  * aligned) is borrowed for the model's lifetime.  The host blob may be freed on return.
- * Synchronises `stream` before returning. */
+ * Synchronises `stream` before returning.  Allocates (and frees) one device staging
+ * buffer of the blob's size.  NT_E_INVALID for a null pointer, a blob of the wrong length
+ * or a misaligned buffer; NT_E_WORKSPACE if device_bytes is too small (the message
+ * states the bytes required); NT_E_DEVICE for a HIP error.
+ * Defined by: Sec. 4.2 "FP16 Inference" (every model parameter stored in FP16; with
+ * NT_F32 they stay fp32), the model of Sec. 2.1-2.2 as for nt_weights_size. */
 nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, size_t host_floats,
                           void* device_buf, size_t device_bytes, void* stream, nt_model** out);
+/* Frees the handle (not device_buf, which the caller owns).  NULL is ignored. */
 void nt_free_model(nt_model* m);
 
 /* ---- ensembles -------------------------------------------------------------------------
@@ -158,14 +170,21 @@ nt_status nt_ensemble(nt_model* const* members, int32_t n_members, int32_t rule,
 
 /* ---- workspace (the memory pool)-------------------------------------------------------
  * Bytes of workspace needed to encode and decode one batch of up to max_sents sentences
- * padded to max_src tokens under `search` (beam width and length limits). */
+ * padded to max_src tokens under `search` (beam width and length limits).
+ * NT_E_INVALID for a null pointer or a non-positive size; NT_E_UNSUPPORTED for beam > 16.
+ * Defined by: the memory pool of Sec. 4.4 ("Profile-guided optimization": blocks are
+ * taken from a pool during decoding and given back when the translation is done); here
+ * the pool is one caller-owned buffer carved by the library, and nothing is allocated
+ * while a batch decodes. */
 nt_status nt_workspace_size(const nt_model* m, const nt_search_cfg* search, int32_t max_sents,
                             int32_t max_src, size_t* bytes);
 
 /* Bytes of workspace nt_translate needs for this exact input at the current stream
  * setting (nt_set_streams): one slice per concurrently decoded batch, each the maximum
  * over the batches that dynamic batching forms from it.  A smaller workspace (at least
- * one slice) makes nt_translate decode fewer batches at once. */
+ * one slice) makes nt_translate decode fewer batches at once.
+ * Defined by: the memory pool of Sec. 4.4 and the dynamic batching of Sec. 4.2 (batches
+ * hold as many sentences as the token budget allows). */
 nt_status nt_translate_workspace_size(const nt_model* m, const nt_search_cfg* search,
                                       const int64_t* h_src_off, int32_t n_sent, size_t* bytes);
 
@@ -174,9 +193,17 @@ nt_status nt_translate_workspace_size(const nt_model* m, const nt_search_cfg* se
  * encoder-decoder keys/values of every decoder layer once (Sec. 4.1), then sets up the
  * decoder state.  d_src: [B,S] int32 device IDs, row-major, PAD-padded; d_len: [B] int32
  * device lengths (1..S).  IDs must lie in [0, vocab): nt_translate checks them on the
- * host; here an ID outside the range is read as the nearest valid ID.  d_ws / ws_bytes: workspace,
- * borrowed until nt_free_state.  Asynchronous except for a small host->device copy of
- * per-sentence length limits, which reads h_len if given (else copies d_len back). */
+ * host; here an ID outside the range is read as the nearest valid ID.  h_len: NULL, or
+ * the same B lengths in host memory (the per-sentence length limits are computed on the
+ * host; without h_len the lengths are copied back from d_len, which synchronises the
+ * stream).  d_ws / ws_bytes: workspace (256-byte aligned), borrowed until nt_free_state.
+ * Asynchronous except for a small host->device copy of the length limits.
+ * NT_E_INVALID for a null pointer, an empty batch, a length outside 1..S, S or a target
+ * limit beyond max_positions; NT_E_UNSUPPORTED for beam > 16; NT_E_WORKSPACE if ws_bytes
+ * is below nt_workspace_size (the message states the bytes required); NT_E_DEVICE.
+ * Defined by: Sec. 2.1 Eq. 1-2 (x_{l+1} = sum_{k<=l} W_k^(l+1) LN(y_k)), Sec. 3.2 (the
+ * deep encoder), Sec. 4.1 "Caching" (the encoder-decoder keys and values are projected
+ * once and kept). */
 nt_status nt_encode(nt_model* m, const int32_t* d_src, const int32_t* d_len, const int32_t* h_len,
                     int32_t B, int32_t S, const nt_search_cfg* search, void* d_ws, size_t ws_bytes,
                     void* stream, nt_dec_state** st);
@@ -186,6 +213,12 @@ nt_status nt_encode(nt_model* m, const int32_t* d_src, const int32_t* d_len, con
  * cached encoder-decoder keys/values, the tied output projection, then selection (greedy
  * argmax with log-sum-exp, or beam top-2K) and the search update; with pruning on, the
  * finished sentences leave the batch.
+ * Defined by: Sec. 4.1 "Caching" (keys and values of every earlier step are kept),
+ * "Faster Beam Search" (a sentence stops once a candidate has ended with EOS and no
+ * live candidate scores higher) and "Batch Pruning" (finished hypotheses leave the
+ * batch); Sec. 4.4 "Greedy Search" and the removal of log_softmax for greedy search
+ * (the argmax needs no normalisation; the chosen token's log-prob comes from the same
+ * pass's log-sum-exp).
  *  d_forced: NULL, or [B*beam] int32 device tokens (greedy only): teacher forcing --
  *    row r emits d_forced[r] instead of its argmax (its log-prob is still recorded);
  *    an ID outside [0, V) is replaced by EOS.
@@ -202,19 +235,25 @@ nt_status nt_decode_step(nt_dec_state* st, const int32_t* d_forced, float* d_log
  *  h_scores [B] (normalised score; with alpha = 0 the sum of log-probs including EOS),
  *  h_token_logp [B, max_tgt] fp32 log-prob of each output token.  Any pointer may be
  *  NULL.  max_tgt is reported by nt_dec_state_info.  NT_E_STATE if a sentence is still
- *  decoding.  Synchronises the stream. */
+ *  decoding.  Synchronises the stream.
+ * Defined by: the result of the search of Sec. 4.1 ("Faster Beam Search": the best
+ * finished hypothesis) or of greedy search (Sec. 4.4). */
 nt_status nt_dec_state_read(nt_dec_state* st, int32_t* h_tokens, int32_t* h_lens, float* h_scores,
                             float* h_token_logp, void* stream);
 
 /* Shape of a state: batch size, padded source length, beam, max target tokens, steps
- * taken, sentences still decoding (as of the last step that reported it). */
+ * taken, sentences still decoding (as of the last step that reported it).  Any output
+ * pointer may be NULL; NT_E_INVALID for a null state.  Diagnostics (no passage of the
+ * paper defines them). */
 nt_status nt_dec_state_info(const nt_dec_state* st, int32_t* B, int32_t* S, int32_t* beam,
                             int32_t* max_tgt, int32_t* steps, int32_t* alive);
 
 /* Copies the encoder output LN_out(x_{L+1}) [B,S,d] to host fp32 (rows of padding
- * included).  Synchronises the stream.  For tests. */
+ * included).  Synchronises the stream.  For tests.  Defined by: Eq. 2 applied to the
+ * last layer's history, then the encoder's output LayerNorm (Sec. 2.1, pre-norm). */
 nt_status nt_dec_state_encoder_out(nt_dec_state* st, float* h_enc, void* stream);
 
+/* Frees a state (not its workspace, which the caller owns).  NULL is ignored. */
 void nt_free_state(nt_dec_state* st);
 
 /* ---- whole-job entry point -------------------------------------------------------------
@@ -232,7 +271,15 @@ void nt_free_state(nt_dec_state* st);
  * Every per-step quantity lives in a device-side control block, so the decoder step is
  * one fixed kernel sequence: each batch's step is captured once into a HIP graph and
  * replayed (or, after nt_set_graphs(0), launched kernel by kernel).  Both ways run the
- * same kernels and give bitwise identical results. */
+ * same kernels and give bitwise identical results.
+ * NT_E_INVALID for a null pointer, n_sent <= 0, an empty sentence, an ID outside
+ * [0, V), a source or target limit beyond max_positions, or out_cap below the output
+ * size (the message states it); NT_E_UNSUPPORTED for beam > 16; NT_E_WORKSPACE if
+ * ws_bytes is below one slice (the message states the bytes required); NT_E_DEVICE.
+ * Defined by: Sec. 4.2 "Dynamic Batching" (as many sentences per batch as the token
+ * budget allows), Sec. 5 (input sentences sorted by descending length; one memory pool)
+ * and Sec. 4.3 "Decoding in Parallel" (parts translated apart, merged back in the
+ * original order). */
 nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* h_src,
                        const int64_t* h_src_off, int32_t n_sent, int32_t* h_out, int64_t out_cap,
                        int64_t* h_out_off, float* h_score, float* h_tok_logp, void* d_ws,
@@ -302,7 +349,8 @@ nt_status nt_set_graphs(int32_t enable);
  * graph replay; 3 without it). */
 nt_status nt_set_streams(int32_t n);
 
-/* Thread-local message of the last failing call on this thread ("" if none). */
+/* Thread-local message of the last failing call on this thread ("" if none); valid until
+ * the next nt_* call on this thread.  A convention of this library, not of the paper. */
 const char* nt_last_error(void);
 
 /* ---- kernel timing ---------------------------------------------------------------------

@@ -64,7 +64,11 @@ def greedy_search(scorer, max_tgt, eos=synth.EOS_ID) -> Hypothesis:
     return Hypothesis(prefix, total, lps, None, total)
 
 
-def beam_search(scorer, K, max_tgt, alpha=0.0, early_stop=True, eos=synth.EOS_ID) -> Hypothesis:
+def beam_search(scorer, K, max_tgt, alpha=0.0, early_stop=True, eos=synth.EOS_ID, on_step=None) -> Hypothesis:
+    """``on_step`` (optional, for diagnostics) is called at every step, before the
+    candidates are walked, as on_step(t, live_tokens, logits, cand, order): the live
+    prefixes, their logits [n, V], the candidate scores c (flattened h*V + w) and the
+    candidate order; it changes nothing."""
     live = [([], 0.0, [])]                      # (tokens, raw score, per-token logp)
     best: Hypothesis | None = None
 
@@ -80,6 +84,8 @@ def beam_search(scorer, K, max_tgt, alpha=0.0, early_stop=True, eos=synth.EOS_ID
         V = logp.shape[1]
         cand = (np.array([h[1] for h in live], dtype=logp.dtype)[:, None] + logp).reshape(-1)
         order = np.lexsort((np.arange(cand.size), -cand))
+        if on_step is not None:
+            on_step(t, [h[0] for h in live], logits, cand, order)
         new_live = []
         for idx in order[:min(2 * K, cand.size)]:
             h, w = divmod(int(idx), V)
@@ -103,14 +109,15 @@ def beam_search(scorer, K, max_tgt, alpha=0.0, early_stop=True, eos=synth.EOS_ID
     return best
 
 
-def translate(model, src, search: synth.SearchSetup) -> Hypothesis:
-    """Translate one sentence with the workload's search setup."""
+def translate(model, src, search: synth.SearchSetup, on_step=None) -> Hypothesis:
+    """Translate one sentence with the workload's search setup (``on_step``: see
+    beam_search; beam only)."""
     from .model import IncrementalScorer
     max_tgt = synth.max_target_len(search, len(src))
     sc = IncrementalScorer(model, src)
     if search.beam <= 1:
         return greedy_search(sc, max_tgt)
-    return beam_search(sc, search.beam, max_tgt, search.len_penalty, bool(search.early_stop))
+    return beam_search(sc, search.beam, max_tgt, search.len_penalty, bool(search.early_stop), on_step=on_step)
 
 
 def brute_force_best(scorer, V, max_tgt, alpha=0.0, eos=synth.EOS_ID) -> Hypothesis:

@@ -529,7 +529,8 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
 }
 
 int max_tgt_of(const nt_search_cfg& s, int len) {
-  return (int)std::floor((double)s.max_len_a * (double)len) + s.max_len_b;
+  const int n = (int)std::floor((double)s.max_len_a * (double)len) + s.max_len_b;
+  return s.max_len_cap > 0 ? std::min(n, s.max_len_cap) : n;
 }
 
 nt_status validate_search(const nt_model& m, const nt_search_cfg* s) {
@@ -538,6 +539,7 @@ nt_status validate_search(const nt_model& m, const nt_search_cfg* s) {
   if (s->beam > 16) return fail(NT_E_UNSUPPORTED, "beam %d > 16", s->beam);
   if (s->max_len_a < 0.f || !std::isfinite(s->max_len_a)) return fail(NT_E_INVALID, "max_len_a must be >= 0");
   if (s->token_budget < 0 || s->max_batch_sents < 0) return fail(NT_E_INVALID, "negative budget / sentence cap");
+  if (s->max_len_cap < 0) return fail(NT_E_INVALID, "max_len_cap must be >= 0");
   if (!std::isfinite(s->len_penalty)) return fail(NT_E_INVALID, "len_penalty must be finite");
   (void)m;
   return NT_OK;
@@ -762,10 +764,17 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
     const double eb = (double)m.eb;
     const float eps = m.cfg.ln_eps;
 
+    // Algorithmic bytes of a decode-step launch count what the step must move: the
+    // weights (read once per step, shared by every row) and, for the vocabulary
+    // projection, the logits it stores (fp32, when they are materialised) or its per-tile
+    // records; the rows' activations stay out of the count.
     auto gemm_dec = [&](int cls, const void* A, int lda, const void* W, int N, int Kd, const nt::GemmEpi& e) -> hipError_t {
-      const double ob = (e.mode == nt::EPI_TOPK && !e.out) ? 0.0 : e.out_f32 ? 4.0 : eb;
       const double wb = e.wscale ? 1.0 : eb;   // bytes per weight (FP8: one)
-      const double bytes = (double)R * Kd * eb + (double)N * Kd * wb + (double)R * N * ob * (e.mode == nt::EPI_RESID ? 2 : 1);
+      double bytes = (double)N * Kd * wb;
+      if (cls == NT_K_GEMM_VOCAB) {
+        if (e.out) bytes += (double)R * N * (e.out_f32 ? 4.0 : eb);
+        if (e.mode == nt::EPI_TOPK) bytes += (double)R * e.n_tiles * nt::topk_record(e.k2) * 4.0;
+      }
       const int role = cls == NT_K_GEMM_VOCAB ? 2 : 1;
       const int tile = e.mode == nt::EPI_TOPK ? 2 : 0;   // the partial records assume 128-column tiles
       nt::GemmEpi ec = e;
@@ -822,7 +831,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       sa.Tcap = st->Tcap;
       sa.scale = 1.0f / std::sqrt((float)m.dh);
       sa.ctl = ctl;
-      NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * (2.0 + 2.0 * (t + 1)), 4.0 * R * (t + 1) * (double)d,
+      NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * 2.0 * (t + 1), 4.0 * R * (t + 1) * (double)d,
                    [&] { return nt::self_attn(m.dt, sa, s); }));
 
       e = nt::GemmEpi{};
@@ -868,7 +877,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       ma.dh = m.dh;
       ma.scale = 1.0f / std::sqrt((float)m.dh);
       ma.ctl = ctl;
-      NT_HIP(timed(NT_K_ATTN_CROSS, s, ((double)st->n_live * 2 * st->S * d + 2.0 * R * d) * eb,
+      NT_HIP(timed(NT_K_ATTN_CROSS, s, (double)st->n_live * 2 * st->S * d * eb,
                    4.0 * R * (double)st->S * d, [&] { return nt::mha(m.dt, ma, s, 1); }));
 
       e = nt::GemmEpi{};
@@ -1585,16 +1594,17 @@ nt_status nt_translate(nt_model* m, const nt_search_cfg* search, const int32_t* 
     int* mirror = nullptr;
     hipEvent_t start = nullptr;
     ~Res() {
+      // Every slot's queued work (a replayed step may still be running on an error path)
+      // completes before anything it uses is released.
+      for (Slot& sl : slots)
+        if (sl.s) (void)hipStreamSynchronize(sl.s);
       for (Slot& sl : slots) {
         if (sl.st) free_state(sl.st);
         if (sl.exec) (void)hipGraphExecDestroy(sl.exec);
         for (auto e : sl.ev)
           if (e) (void)hipEventDestroy(e);
         if (sl.cs) (void)hipStreamDestroy(sl.cs);
-        if (sl.s) {
-          (void)hipStreamSynchronize(sl.s);
-          (void)hipStreamDestroy(sl.s);
-        }
+        if (sl.s) (void)hipStreamDestroy(sl.s);
       }
       if (start) (void)hipEventDestroy(start);
       if (pin) (void)hipHostFree(pin);

@@ -45,8 +45,8 @@ class nt_model_cfg(ctypes.Structure):
 
 class nt_search_cfg(ctypes.Structure):
     _fields_ = [("beam", c_int32), ("len_penalty", c_float), ("max_len_a", c_float), ("max_len_b", c_int32),
-                ("token_budget", c_int32), ("max_batch_sents", c_int32), ("early_stop", c_int32),
-                ("prune", c_int32)]
+                ("max_len_cap", c_int32), ("token_budget", c_int32), ("max_batch_sents", c_int32),
+                ("early_stop", c_int32), ("prune", c_int32)]
 
 
 class NTError(RuntimeError):
@@ -143,7 +143,14 @@ def model_cfg(shape, dtype: str = "f16", hist_norm: bool = True, ln_eps: float =
 def search_cfg(s) -> nt_search_cfg:
     """nt_search_cfg from any object with the nt_search_cfg field names."""
     return nt_search_cfg(int(s.beam), float(s.len_penalty), float(s.max_len_a), int(s.max_len_b),
-                         int(s.token_budget), int(s.max_batch_sents), int(s.early_stop), int(s.prune))
+                         int(getattr(s, "max_len_cap", 0)), int(s.token_budget), int(s.max_batch_sents),
+                         int(s.early_stop), int(s.prune))
+
+
+def max_target_tokens(sc: nt_search_cfg, src_len: int) -> int:
+    """A sentence's target length limit under sc, as the library computes it."""
+    n = int(np.floor(np.float32(sc.max_len_a) * np.float64(src_len))) + int(sc.max_len_b)
+    return min(n, int(sc.max_len_cap)) if sc.max_len_cap > 0 else n
 
 
 # ---- the C entry points ----------------------------------------------------------------
@@ -343,7 +350,7 @@ class _Translator:
         need = nt_translate_workspace_size(self.handle, sc, offs)
         ws = self.workspace(need)
         lens = np.diff(offs)
-        cap = int(sum(int(np.floor(np.float32(sc.max_len_a) * np.float64(L))) + sc.max_len_b for L in lens))
+        cap = int(sum(max_target_tokens(sc, int(L)) for L in lens))
         out, out_off, score, logp = nt_translate(self.handle, sc, ids, offs, cap, ws.data_ptr(), ws.numel())
         n = len(lens)
         return ([out[out_off[i]:out_off[i + 1]] for i in range(n)], score,

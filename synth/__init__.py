@@ -48,6 +48,7 @@ class SearchSetup:
     len_penalty: float = 0.0
     max_len_a: float = 1.5
     max_len_b: int = 10
+    max_len_cap: int = 0      # > 0: no target longer than this (0: no cap)
     token_budget: int = 8192
     max_batch_sents: int = 0
     early_stop: int = 1
@@ -366,8 +367,11 @@ def sentence_list(ids: np.ndarray, offs: np.ndarray) -> list:
 
 
 def max_target_len(search: SearchSetup, src_len: int) -> int:
-    """Per-sentence target cap: floor(a * S_i) + b tokens, EOS included."""
-    return int(math.floor(search.max_len_a * src_len)) + int(search.max_len_b)
+    """Per-sentence target cap: floor(a * S_i) + b tokens, EOS included, lowered to
+    max_len_cap when that is positive."""
+    n = int(math.floor(search.max_len_a * src_len)) + int(search.max_len_b)
+    cap = int(getattr(search, "max_len_cap", 0))
+    return min(n, cap) if cap > 0 else n
 
 
 def stratified_subset(offs: np.ndarray, k: int) -> np.ndarray:

@@ -106,3 +106,113 @@ def compare_greedy_ids(om, src, gpu_tokens, max_tgt, tau=1e-4):
         prefix = prefix + [g]
     assert len(gpu) == max_tgt
     return ties
+
+
+# ---- the oracle over host processes -----------------------------------------------------
+# The parity tests at full model shape run the fp64 oracle on tens of sentences.  Each
+# sentence is independent (the oracle decodes one sentence at a time), so they are
+# spread over forked host processes, one BLAS thread each, the way the paper splits CPU
+# decoding by lines (Sec. 4.3).  The children inherit POOL (the oracle model, the
+# sentences and the GPU's results, gathered before the fork) and use only NumPy.
+POOL: dict = {}
+
+
+def _pool_call(arg):
+    from threadpoolctl import threadpool_limits
+    fn, item = arg
+    with threadpool_limits(limits=1):
+        return fn(item)
+
+
+def oracle_map(fn, items, procs=None):
+    """[fn(x) for x in items] over min(16, cores) forked processes (fn at module level,
+    reading its inputs from POOL).  Items are handed out one at a time in the given
+    order, so the longest sentences should come first."""
+    import multiprocessing as mp
+    import os
+    items = list(items)
+    if not items:
+        return []
+    import time
+    P = min(procs or 16, os.cpu_count() or 1, len(items))
+    out = []
+    t0 = last = time.time()
+    with mp.get_context("fork").Pool(P) as pool:
+        for r in pool.imap(_pool_call, [(fn, x) for x in items], chunksize=1):
+            out.append(r)
+            if time.time() - last > 20:
+                last = time.time()
+                print(f"  oracle: {len(out)}/{len(items)} sentences after {last - t0:.0f} s", flush=True)
+    return out
+
+
+def greedy_follow(om, src, gpu_tokens, max_tgt, tau=1e-4):
+    """compare_greedy_ids that also returns the oracle's fp64 logits along the GPU's
+    tokens: (near-ties, [len+1 or max_tgt, V] rows; row t predicts token t)."""
+    sc = IncrementalScorer(om, src)
+    prefix: list = []
+    ties = 0
+    rows = []
+    gpu = list(int(x) for x in gpu_tokens)
+    for t in range(max_tgt):
+        logits, _ = sc([prefix])
+        row = logits[0]
+        rows.append(row)
+        w = int(np.argmax(row))
+        g = gpu[t] if t < len(gpu) else EOS
+        if w != g:
+            gap = float(row[w] - row[g])
+            assert gap <= tau, f"step {t}: oracle {w} vs GPU {g}, fp64 logit gap {gap:.3g}"
+            ties += 1
+        if g == EOS:
+            assert t == len(gpu)
+            return ties, np.stack(rows)
+        prefix = prefix + [g]
+    assert len(gpu) == max_tgt
+    return ties, np.stack(rows)
+
+
+class BeamFollower:
+    """on_step observer for oracle.beam_search that follows one hypothesis (the GPU's
+    output tokens).  It keeps the oracle's logits of every prefix of that hypothesis
+    while the prefix is live in the oracle's beam, and notes the first step at which the
+    hypothesis leaves the beam, with the oracle's fp64 gap there: between the candidate
+    kept at the boundary (the K-th live one, or the 2K-th walked one for an EOS
+    candidate) and the hypothesis's own candidate."""
+
+    def __init__(self, tokens, K, eos=EOS):
+        self.g = [int(x) for x in tokens]
+        self.K = K
+        self.eos = eos
+        self.rows: dict = {}
+        self.left = None
+        self.gap = None
+
+    def __call__(self, t, live, logits, cand, order):
+        if self.left is not None or t > len(self.g):
+            return
+        pre = self.g[:t]
+        h = next((i for i, toks in enumerate(live) if list(toks) == pre), None)
+        if h is None:
+            self.left, self.gap = t, float("inf")
+            return
+        self.rows[t] = np.array(logits[h])
+        V = logits.shape[1]
+        w = self.g[t] if t < len(self.g) else self.eos
+        idx = h * V + w
+        walked = [int(i) for i in order[:min(2 * self.K, cand.size)]]
+        if w == self.eos:
+            if idx not in walked:
+                self.left, self.gap = t, float(cand[walked[-1]] - cand[idx])
+        else:
+            kept = [i for i in walked if i % V != self.eos][:self.K]
+            if idx not in kept:
+                self.left, self.gap = t, float(cand[kept[-1]] - cand[idx])
+
+
+def hypothesis_score(rows, tokens, n_steps, alpha, eos_emitted):
+    """Normalised score of a hypothesis from the logits rows along it (row t predicts
+    token t): the sum of its log-probs (EOS included when emitted) over lp(n)."""
+    lp = [float(rows[t][w] - oracle.logsumexp(rows[t])) for t, w in enumerate(tokens)]
+    raw = sum(lp) + (float(rows[len(tokens)][EOS] - oracle.logsumexp(rows[len(tokens)])) if eos_emitted else 0.0)
+    return raw / oracle.length_penalty(n_steps, alpha), lp

@@ -36,10 +36,29 @@ def test_every_declared_function_is_exported(nt):
     assert sorted(nt.EXPORTS) == declared
 
 
-def test_struct_layouts_match_header(nt):
+def header_struct_fields(name):
+    """(field, C type) of `typedef struct { ... } name;` in nt.h, in declaration order."""
+    src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "nt.h")).read(), flags=re.S)
+    body = re.search(r"typedef struct \{([^}]*)\}\s*" + name + r"\s*;", src).group(1)
+    out = []
+    for decl in body.split(";"):
+        decl = decl.strip()
+        if not decl:
+            continue
+        ctype, names = decl.split(None, 1)
+        out += [(n.strip(), ctype) for n in names.split(",")]
+    return out
+
+
+@pytest.mark.parametrize("name", ["nt_model_cfg", "nt_search_cfg"])
+def test_struct_layouts_match_header(nt, name):
     import ctypes
-    assert ctypes.sizeof(nt.nt_model_cfg) == 15 * 4
-    assert ctypes.sizeof(nt.nt_search_cfg) == 8 * 4
+    cmap = {"int32_t": ctypes.c_int32, "float": ctypes.c_float}
+    fields = header_struct_fields(name)
+    binding = getattr(nt, name)._fields_
+    assert [f for f, _ in fields] == [f for f, _ in binding]
+    assert [cmap[t] for _, t in fields] == [t for _, t in binding]
+    assert ctypes.sizeof(getattr(nt, name)) == 4 * len(fields)
 
 
 @pytest.mark.parametrize("name", list(synth.WORKLOADS))

@@ -87,3 +87,112 @@ def test_one_step_target_limit(beam):
         else:
             assert G.compare_greedy_ids(om, s, tk, 1) <= 1
     model.close()
+
+
+def test_undersized_workspace_is_reported():
+    """NT_E_WORKSPACE from nt_encode and nt_translate when the workspace is one 256-byte
+    granule short, with the required size in the message; at the stated size both run."""
+    from paper_2109_08008_amd import nt
+    torch = G.torch_cuda()
+    blob = synth.make_weights(SHAPE, seed=75, lively=True)
+    model = G.new_model(SHAPE, blob, "f32")
+    srcs = [[5, 6, 7], [8], [9, 10]]
+    search = synth.SearchSetup(beam=2, max_len_a=1.0, max_len_b=3)
+    sc = nt.search_cfg(search)
+    arr, lens = G.pad_batch(srcs)
+    B, S = arr.shape
+    need = nt.nt_workspace_size(model.handle, sc, B, S)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    d_src, d_len = torch.from_numpy(arr).cuda(), torch.from_numpy(lens).cuda()
+    with pytest.raises(nt.NTError) as err:
+        nt.nt_encode(model.handle, d_src.data_ptr(), d_len.data_ptr(), lens, B, S, sc, ws.data_ptr(), need - 256)
+    assert err.value.status == nt.NT_E_WORKSPACE and str(need) in err.value.message, err.value
+    st = nt.nt_encode(model.handle, d_src.data_ptr(), d_len.data_ptr(), lens, B, S, sc, ws.data_ptr(), need)
+    nt.nt_free_state(st)
+    ids, offs = _csr(srcs)
+    need_t = nt.nt_translate_workspace_size(model.handle, sc, offs)
+    wst = torch.empty(need_t, dtype=torch.uint8, device="cuda")
+    cap = sum(synth.max_target_len(search, len(s)) for s in srcs)
+    with pytest.raises(nt.NTError) as err:
+        nt.nt_translate(model.handle, sc, ids, offs, cap, wst.data_ptr(), need_t - 256)
+    assert err.value.status == nt.NT_E_WORKSPACE and str(need_t) in err.value.message, err.value
+    out, out_off, _, _ = nt.nt_translate(model.handle, sc, ids, offs, cap, wst.data_ptr(), need_t)
+    assert out_off[-1] <= cap
+    model.close()
+
+
+def test_steps_after_the_end_and_early_reads_are_state_errors():
+    """nt_dec_state_read before every sentence has finished and nt_decode_step after it
+    give NT_E_STATE; the step-level results equal the oracle's beam search."""
+    from paper_2109_08008_amd import nt
+    blob = synth.make_weights(SHAPE, seed=76, lively=True)
+    model = G.new_model(SHAPE, blob, "f32")
+    srcs = [[5, 6, 7, 8], [9], [10, 11]]
+    search = synth.SearchSetup(beam=2, len_penalty=0.6, max_len_a=1.0, max_len_b=3)
+    st, keep = G.gpu_encode(model, srcs, search)
+    try:
+        with pytest.raises(nt.NTError) as err:
+            nt.nt_dec_state_read(st)
+        assert err.value.status == nt.NT_E_STATE, err.value
+        limit = max(synth.max_target_len(search, len(s)) for s in srcs)
+        steps = 0
+        while nt.nt_decode_step(st) > 0:
+            steps += 1
+            assert steps <= limit
+        for _ in range(2):
+            with pytest.raises(nt.NTError) as err:
+                nt.nt_decode_step(st)
+            assert err.value.status == nt.NT_E_STATE, err.value
+        toks, scores, _ = nt.nt_dec_state_read(st)
+    finally:
+        nt.nt_free_state(st)
+    om = G.oracle_model(SHAPE, blob, "f32")
+    for s, tk, sc in zip(srcs, toks, scores):
+        ref = oracle.translate(om, s, search)
+        assert list(tk) == list(ref.tokens)
+        assert abs(sc - ref.score) <= 1e-3
+    model.close()
+
+
+def test_beam_wider_than_16_is_unsupported():
+    from paper_2109_08008_amd import nt
+    blob = synth.make_weights(SHAPE, seed=77)
+    model = G.new_model(SHAPE, blob, "f32")
+    wide = synth.SearchSetup(beam=17, max_len_a=1.0, max_len_b=3)
+    ids, offs = _csr([[5, 6], [7]])
+    with pytest.raises(nt.NTError) as err:
+        nt.nt_workspace_size(model.handle, nt.search_cfg(wide), 2, 2)
+    assert err.value.status == nt.NT_E_UNSUPPORTED, err.value
+    with pytest.raises(nt.NTError) as err:
+        model.translate(ids, offs, wide)
+    assert err.value.status == nt.NT_E_UNSUPPORTED, err.value
+    toks, _, _ = model.translate(ids, offs, synth.replace(wide, beam=16))   # the widest accepted
+    assert all(len(t) <= 3 for t in toks)
+    model.close()
+
+
+@pytest.mark.parametrize("beam", [1, 4])
+def test_target_length_cap(beam):
+    """max_len_cap lowers every sentence's limit floor(a * len) + b to the cap (the
+    paper caps targets at 200 tokens, Sec. 4.4); a negative cap is rejected."""
+    from paper_2109_08008_amd import nt
+    blob = synth.make_weights(SHAPE, seed=78, lively=True, eos_boost=1.0)
+    rng = np.random.default_rng(79)
+    srcs = [list(rng.integers(4, SHAPE.vocab, size=n)) for n in (12, 3, 7, 20)]
+    ids, offs = _csr(srcs)
+    search = synth.SearchSetup(beam=beam, len_penalty=0.6, max_len_a=1.5, max_len_b=10, max_len_cap=5)
+    model = G.new_model(SHAPE, blob, "f32")
+    toks, scores, _ = model.translate(ids, offs, search)
+    om = G.oracle_model(SHAPE, blob, "f32")
+    for s, tk, sc in zip(srcs, toks, scores):
+        assert synth.max_target_len(search, len(s)) == 5 and len(tk) <= 5
+        if beam > 1:
+            ref = oracle.translate(om, s, search)
+            assert list(tk) == list(ref.tokens)
+            assert abs(sc - ref.score) <= 1e-3
+        else:
+            assert G.compare_greedy_ids(om, s, tk, 5) <= 1
+    with pytest.raises(nt.NTError) as err:
+        model.translate(ids, offs, synth.replace(search, max_len_cap=-1))
+    assert err.value.status == nt.NT_E_INVALID, err.value
+    model.close()

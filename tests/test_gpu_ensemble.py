@@ -22,6 +22,7 @@ MEMBERS = [  # (shape, seed, dlcl)
     (synth.ModelShape(64, 2, 256, 2, 2, V, rel_k=4), 43, True),
 ]
 SCORE_TOL = {"f32": 1e-3, "f16": 5e-2}
+LOGP_TOL = {"f32": 1e-3, "f16": 1e-2}   # per-token combined score of the returned hypothesis
 
 
 def _blobs():
@@ -65,8 +66,8 @@ def test_teacher_forced_combined_scores(dtype, rule):
         err = max(err, float(np.abs(got[b] - ref).max()))
         # the recorded per-token values and the score are sums of combined scores
         want = [ref[t, tg[t]] for t in range(len(tg))]
-        assert np.abs(np.asarray(logp[b]) - want).max(initial=0) <= 10 * SCORE_TOL[dtype]
-        assert abs(scores[b] - (sum(want) + ref[len(tg), synth.EOS_ID])) <= 10 * SCORE_TOL[dtype] * (len(tg) + 1)
+        assert np.abs(np.asarray(logp[b]) - want).max(initial=0) <= LOGP_TOL[dtype]
+        assert abs(scores[b] - (sum(want) + ref[len(tg), synth.EOS_ID])) <= LOGP_TOL[dtype] * (len(tg) + 1)
     print(f"rule {rule} {dtype}: combined scores max abs err {err:.3g}")
     assert err <= SCORE_TOL[dtype]
 

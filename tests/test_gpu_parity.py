@@ -1,10 +1,11 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
-Tolerances: fp32 logits <= 1e-3 max abs and identical token IDs (near-tie protocol);
-fp16 teacher-forced logits <= 5e-2 max abs and per-token log-probs of the returned
-hypothesis <= 1e-2; bf16 (8 mantissa bits against fp16's 11, so 8x the rounding
-error) logits <= 0.4.  The oracle always runs in fp64 on the weights as the GPU stores
-them (matrices rounded to the 16-bit type).
+Tolerances: fp32 logits <= 1e-3 max abs, per-token log-probs <= 1e-3 and identical token
+IDs (near-tie protocol); fp16 teacher-forced logits <= 5e-2 max abs and per-token
+log-probs <= 1e-2; bf16 (8 mantissa bits against fp16's 11, so 8x the rounding error)
+logits <= 0.4 and per-token log-probs <= 8e-2.  A score (a sum of per-token log-probs)
+is held to the per-token bound times the number of its terms.  The oracle always runs in
+fp64 on the weights as the GPU stores them (matrices rounded to the 16-bit type).
 """
 import numpy as np
 import pytest
@@ -15,6 +16,7 @@ from tests import gpu_util as G
 pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = {"f32": 1e-3, "f16": 5e-2, "bf16": 0.4}
+LOGP_TOL = {"f32": 1e-3, "f16": 1e-2, "bf16": 8e-2}
 ENC_TOL = {"f32": 1e-4, "f16": 3e-2, "bf16": 0.25}
 
 SHAPES = {
@@ -104,9 +106,9 @@ def test_teacher_forced_logits(name, dtype):
         # the recorded per-token log-probs are the forced tokens' log_softmax values
         ref_lp = ref - np.log(np.exp(ref - ref.max(1, keepdims=True)).sum(1, keepdims=True)) - ref.max(1, keepdims=True)
         want = [ref_lp[t, tg[t]] for t in range(len(tg))]
-        assert np.abs(np.asarray(logp[b]) - want).max(initial=0) <= 10 * LOGIT_TOL[dtype]
+        assert np.abs(np.asarray(logp[b]) - want).max(initial=0) <= LOGP_TOL[dtype]
         full = sum(want) + ref_lp[len(tg), synth.EOS_ID]
-        assert abs(scores[b] - full) <= 10 * LOGIT_TOL[dtype] * (len(tg) + 1)
+        assert abs(scores[b] - full) <= LOGP_TOL[dtype] * (len(tg) + 1)
     print(f"{name} {dtype}: teacher-forced logits max abs err {err:.3g}")
     assert err <= LOGIT_TOL[dtype]
 
@@ -130,13 +132,18 @@ def test_tiny_greedy_fp32_token_ids():
     assert ties <= 1
 
 
-@pytest.mark.parametrize("alpha,early", [(0.0, 1), (0.6, 1), (0.6, 0)])
-def test_beam_fp32_token_ids(alpha, early):
+@pytest.mark.parametrize("beam,alpha,early", [(4, 0.0, 1), (4, 0.6, 1), (4, 0.6, 0), (2, 0.0, 1), (2, 0.6, 1),
+                                              (8, 0.0, 1), (8, 0.6, 1), (16, 0.0, 1), (16, 0.6, 1), (16, 0.6, 0)])
+def test_beam_fp32_token_ids(beam, alpha, early):
+    """Beam widths 2 to 16 (the widest the library accepts; 2K = 32 candidates a row).  The
+    EOS row's boost is set so that hypotheses end at varied steps: some at once, some in
+    between, some at the length limit (a wider beam keeps an early EOS more easily, so
+    K = 16 gets a smaller boost)."""
     import oracle
     shape = SHAPES["d128"]
-    blob = synth.make_weights(shape, seed=21, lively=True, eos_boost=4.0)
+    blob = synth.make_weights(shape, seed=21, lively=True, eos_boost=1.0 if beam > 8 else 1.2)
     srcs, ids, offs = _sentences(10, 2, 20, shape.vocab, seed=6)
-    search = synth.SearchSetup(beam=4, len_penalty=alpha, max_len_a=1.0, max_len_b=6, early_stop=early)
+    search = synth.SearchSetup(beam=beam, len_penalty=alpha, max_len_a=1.0, max_len_b=6, early_stop=early)
     model = G.new_model(shape, blob, "f32")
     toks, scores, logp = model.translate(ids, offs, search)
     om = G.oracle_model(shape, blob, "f32")
@@ -145,7 +152,10 @@ def test_beam_fp32_token_ids(alpha, early):
         assert list(tk) == list(ref.tokens)
         assert abs(sc - ref.score) <= 1e-3
         np.testing.assert_allclose(lp, ref.tok_logp, atol=1e-3)
-    print("lengths:", [len(t) for t in toks])
+    lens = [len(t) for t in toks]
+    limits = [synth.max_target_len(search, len(s)) for s in srcs]
+    print("lengths:", lens, "limits:", limits)
+    assert sum(n > 0 for n in lens) >= 3 and any(0 < n < m for n, m in zip(lens, limits)), "degenerate search"
 
 
 @pytest.mark.parametrize("dtype", ["f32", "f16"])
