@@ -340,6 +340,21 @@ nt_status nt_op_select(const float* d_logits, int32_t rows, int32_t V, int32_t k
 nt_status nt_op_select_tiled(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv,
                              int32_t* d_topi, float* d_lse, void* stream);
 
+/* nt_op_select_tiled for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): the same kernels, arguments
+ * and results, with the per-tile records in a static array that the library holds on
+ * each GPU until the process ends (16 MiB: rows * ceil(V / 128) <= 1048576 records, i.e.
+ * 4194 rows at V = 32000; larger inputs return NT_E_UNSUPPORTED with the limit in the
+ * message).  Nothing is allocated and the stream is not synchronised: the call only
+ * enqueues work.  Every call on one GPU shares that GPU's array, which keeps the last
+ * call's records (each call writes every record it reads before reading it, so nothing
+ * needs clearing); calls that overlap on one GPU -- on different streams, or from
+ * different threads -- race on it and must be ordered by the caller.  Runs on the
+ * current device. */
+#define NT_SELECT_NOALLOC_MAX_RECORDS (1 << 20)
+nt_status nt_op_select_tiled_noalloc(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv,
+                                     int32_t* d_topi, float* d_lse, void* stream);
+
 /* Process-wide switch for nt_translate's graph replay of the decoder step (default on;
  * with 0, every step is launched kernel by kernel). */
 nt_status nt_set_graphs(int32_t enable);

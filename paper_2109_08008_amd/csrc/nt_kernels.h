@@ -266,6 +266,11 @@ hipError_t beam_select_tiles(const float* part, int n_tiles, const float* logits
                              int V, int k2, float* topv, int* topi, float* lse, hipStream_t s);
 // Per-tile records of a logits matrix in the projection epilogue's layout (for tests).
 hipError_t tile_records(const float* logits, int rows, int V, float* part, hipStream_t s);
+// The current device's copy of the library's static records array (room for
+// SELECT_NOALLOC_MAX_RECORDS records of the k2 = 1 layout), located on the first call on
+// each device and reused after that.
+constexpr int SELECT_NOALLOC_MAX_RECORDS = 1 << 20;   // 16 MiB
+hipError_t select_scratch(float** out, size_t* records);
 
 // Fused greedy selection after an EPI_TOPK projection (k2 = 1): merges the per-tile
 // partials of each live row into the argmax and the LSE, then the greedy update.

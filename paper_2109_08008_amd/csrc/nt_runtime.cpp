@@ -1873,6 +1873,29 @@ nt_status nt_op_select_tiled(const float* d_logits, int32_t rows, int32_t V, int
   return NT_OK;
 }
 
+nt_status nt_op_select_tiled_noalloc(const float* d_logits, int32_t rows, int32_t V, int32_t k, float* d_topv,
+                                     int32_t* d_topi, float* d_lse, void* stream) {
+  g_err.clear();
+  if (!d_logits || !d_topv || !d_topi || !d_lse) return fail(NT_E_INVALID, "null argument to nt_op_select_tiled_noalloc");
+  if (rows < 0 || V <= 0) return fail(NT_E_INVALID, "rows must be >= 0 and V > 0");
+  if (k < 1 || k > 32 || k > V) return fail(NT_E_UNSUPPORTED, "k must be in [1, min(32, V)]");
+  if (V > 65536) return fail(NT_E_UNSUPPORTED, "V > 65536");
+  const int n_tiles = (V + 127) / 128;
+  if ((long long)rows * n_tiles > NT_SELECT_NOALLOC_MAX_RECORDS)
+    return fail(NT_E_UNSUPPORTED, "rows * ceil(V / 128) = %lld records > %d (at most %d rows at V = %d)",
+                (long long)rows * n_tiles, NT_SELECT_NOALLOC_MAX_RECORDS, NT_SELECT_NOALLOC_MAX_RECORDS / n_tiles, V);
+  if (rows == 0) return NT_OK;
+  static_assert(NT_SELECT_NOALLOC_MAX_RECORDS == nt::SELECT_NOALLOC_MAX_RECORDS, "header and kernels agree");
+  float* part = nullptr;
+  size_t cap = 0;
+  NT_HIP(nt::select_scratch(&part, &cap));
+  if ((size_t)rows * n_tiles > cap) return fail(NT_E_UNSUPPORTED, "records exceed the static buffer");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  NT_HIP(nt::tile_records(d_logits, rows, V, part, s));
+  NT_HIP(nt::beam_select_tiles(part, n_tiles, d_logits, nullptr, 1, rows, V, k, d_topv, d_topi, d_lse, s));
+  return NT_OK;
+}
+
 nt_status nt_prof_config(uint32_t class_mask, int32_t stride) {
   g_err.clear();
   if (stride < 1) return fail(NT_E_INVALID, "stride must be >= 1");

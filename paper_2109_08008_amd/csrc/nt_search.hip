@@ -14,6 +14,9 @@
 // no cache row is ever copied.
 #include <limits.h>
 
+#include <mutex>
+#include <vector>
+
 #include "nt_common.h"
 #include "nt_kernels.h"
 
@@ -1028,6 +1031,34 @@ hipError_t beam_select_tiles(const float* part, int n_tiles, const float* logits
   else NT_SEL(32);
 #undef NT_SEL
   return hipGetLastError();
+}
+
+// ---- records of the allocation-free tiled selection ----------------------------------------
+// A file-scope device array stands in for the per-call records buffer of the tiled
+// selection, for callers that cannot allocate device memory.  Every GPU holds its own
+// copy until the process ends.  In host code the array's name is not a device address:
+// each device's copy is located once, with that device current, by hipGetSymbolAddress,
+// and only that address is handed to kernels.
+constexpr size_t SCRATCH_FLOATS = (size_t)SELECT_NOALLOC_MAX_RECORDS * 4;   // 4 floats a record
+static __device__ __align__(256) float scratch[SCRATCH_FLOATS];
+
+hipError_t select_scratch(float** out, size_t* records) {
+  static std::mutex mu;
+  static std::vector<float*> per_device;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((size_t)dev >= per_device.size()) per_device.resize(dev + 1, nullptr);
+  if (!per_device[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    per_device[dev] = static_cast<float*>(p);
+  }
+  *out = per_device[dev];
+  if (records) *records = SCRATCH_FLOATS / 4;
+  return hipSuccess;
 }
 
 hipError_t tile_records(const float* logits, int rows, int V, float* part, hipStream_t s) {

@@ -30,10 +30,11 @@ EXPORTS = [
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
     "nt_op_gemm", "nt_op_gemm_ln", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units", "nt_op_select",
-    "nt_op_select_tiled",
+    "nt_op_select_tiled", "nt_op_select_tiled_noalloc",
     "nt_ensemble", "nt_quantize_fp8",
 ]
 NT_ENS_MEAN_LOGP, NT_ENS_LOG_MEAN_P = 0, 1
+NT_SELECT_NOALLOC_MAX_RECORDS = 1 << 20   # include/nt.h: records of nt_op_select_tiled_noalloc
 
 
 class nt_model_cfg(ctypes.Structure):
@@ -98,6 +99,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_set_streams": (c_int32, [c_int32]),
         "nt_op_select": (c_int32, [P, c_int32, c_int32, c_int32, P, P, P, P]),
         "nt_op_select_tiled": (c_int32, [P, c_int32, c_int32, c_int32, P, P, P, P]),
+        "nt_op_select_tiled_noalloc": (c_int32, [P, c_int32, c_int32, c_int32, P, P, P, P]),
         "nt_prof_units": (c_int32, [POINTER(c_int64), POINTER(c_int64)]),
         "nt_prof_reset": (c_int32, []),
         "nt_prof_get": (c_int32, [c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double), POINTER(c_double)]),
@@ -292,6 +294,12 @@ def nt_op_select_tiled(d_logits: int, rows: int, V: int, k: int, d_topv: int, d_
                        stream=None):
     _check(load_library().nt_op_select_tiled(c_void_p(d_logits), rows, V, k, c_void_p(d_topv), c_void_p(d_topi),
                                              c_void_p(d_lse), _stream(stream)))
+
+
+def nt_op_select_tiled_noalloc(d_logits: int, rows: int, V: int, k: int, d_topv: int, d_topi: int, d_lse: int,
+                               stream=None):
+    _check(load_library().nt_op_select_tiled_noalloc(c_void_p(d_logits), rows, V, k, c_void_p(d_topv),
+                                                     c_void_p(d_topi), c_void_p(d_lse), _stream(stream)))
 
 
 def nt_prof_enable(mask: int):
