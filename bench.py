@@ -11,9 +11,9 @@ The default workload is the largest configuration, the wide teacher-size model (
 30-layer DLCL encoder, 6-layer decoder, beam 4, 4096 sentences).  Batches are decoded four
 at a time on their own streams (the library default), each decoder step replayed from a
 captured HIP graph.  The line carries a roofline entry for the dominant kernel class,
-timed with HIP events on the launch stream inside the timed region: about 48 units
-(decoder steps or batch encodes) are sampled, and each sample runs alone on the GPU so
-that its kernel durations are the kernel's own.  Next to that per-launch rate the entry
+timed with HIP events on the launch stream inside the timed region: up to 40 units
+(decoder steps or batch encodes; at most 2 per timed step) are sampled, and each sample
+runs alone on the GPU so that its kernel durations are the kernel's own.  Next to that per-launch rate the entry
 gives the class's algorithmic work per translation over the timed step's wall time
 (`in_pipeline`), and how much kernel time the concurrent batches overlap (`overlap`).
 It also carries the CPU oracle's throughput on a bounded sample of the same workload
@@ -48,11 +48,23 @@ GEMM_CLASSES = (0, 1, 2)
 # class) scaled by what the same counters read for a plain 512 MiB device copy (FETCH_SIZE
 # reads half the bytes moved, WRITE_SIZE all of them).  Valid only for the kernel source
 # the counters were taken on (sha256 over `files`); otherwise the bench reports null.
+GEMM_FILES = ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"]
 TRAFFIC = {
+    ("gemm_dec", "wide-30-6"): {
+        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
+        "fetch_kib": 12672.25, "write_kib": 4063.63, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
     ("gemm_dec", "base-6-6"): {
-        "files": ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"],
-        "sha256": "714ca558097181235fea097f6bfba846a9751e02f1dc300f4ed482d0cfb632bb",
-        "fetch_kib": 3927.24, "write_kib": 1304.32, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
+        "fetch_kib": 3920.85, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_enc", "deep-shallow-greedy"): {
+        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
+        "fetch_kib": 15269.18, "write_kib": 17941.88, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_vocab", "deep-shallow-beam"): {
+        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
+        "fetch_kib": 52133.48, "write_kib": 204231.26, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 
@@ -75,18 +87,36 @@ ENCODE_ONLY_CLASSES = (0, 3, 5)   # launched only by batch encodes (GEMM_ENC, DL
 def parse_args():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="wide-30-6", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graphs", action="store_true", help="launch decoder steps kernel by kernel")
     ap.add_argument("--streams", type=int, default=0, help="batches decoded concurrently (0: library default)")
-    ap.add_argument("--samples", type=int, default=48, help="timing samples (isolated units) in the timed region")
+    ap.add_argument("--samples", type=int, default=40,
+                    help="timing samples (isolated units) in the timed region, at most 2 per timed step")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work for the oracle sample")
     ap.add_argument("--cpu-procs", type=int, default=0, help="oracle processes (0: min(16, cores))")
     ap.add_argument("--cpu-full", action="store_true",
                     help="time the oracle on the whole sentence set instead of a bounded sample (slow)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run three 512 MiB device copies (the reference kernel that HBM counters are "
+                         "scaled by) and exit")
     return ap.parse_args()
+
+
+def calibrate_copy() -> dict:
+    """Three plain device copies of 512 MiB (fp32 tensors of 128 Mi elements): the kernel of
+    known traffic (512 MiB read and 512 MiB written each) that the FETCH_SIZE / WRITE_SIZE
+    readings of the library's kernels are scaled by."""
+    import torch
+    n = 1 << 27
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return {"copies": 3, "bytes_read_each": 4 * n, "bytes_written_each": 4 * n}
 
 
 def roofline_entry(cls: int, prof: dict, dtype: str, workload: str) -> dict:
@@ -224,6 +254,9 @@ def cpu_baseline(w: synth.Workload, blobs, ids, offs, seconds: float, procs: int
 
 def main():
     args = parse_args()
+    if args.calibrate_copy:
+        print(json.dumps(calibrate_copy()), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported by this build "
               "(sentences are independent: a multi-GPU run would shard batches across replicas)", file=sys.stderr)
@@ -270,8 +303,11 @@ def main():
 
     # timed region: events on the dominant class in about `samples` units, each run alone
     # (the other batches' streams drained first) so that they time the kernel by itself
+    # A sample drains the other batches' streams and runs alone, which stalls the pipeline
+    # for about one unit: at most 2 per timed step keeps that near 1% of the timed run.
     units = enc_units if dominant in ENCODE_ONLY_CLASSES else step_units
-    stride = max(1, (units * args.steps) // max(args.samples, 1))
+    samples = max(1, min(args.samples, 2 * args.steps))
+    stride = max(1, (units * args.steps) // samples)
     nt.nt_prof_reset()
     nt.nt_prof_config(1 << dominant, stride)
     torch.cuda.synchronize()
@@ -328,6 +364,9 @@ def main():
         "phase_rooflines": phase_rooflines(breakdown, w.dtype),
         "achievable_peaks": peaks,
         "kernel_ms_per_step_alone": {k: round(v["ms"], 3) for k, v in breakdown.items()},
+        "kernel_classes_per_step": {k: {"launches": v["launches"], "ms_alone": round(v["ms"], 3),
+                                        "alg_MB": round(v["bytes"] / 1e6, 2), "alg_GFLOP": round(v["flops"] / 1e9, 2)}
+                                    for k, v in breakdown.items()},
     }
     if w.members:
         line["config"]["members"] = [f"{mb.model.n_enc}-{mb.model.n_dec}{'+DLCL' if mb.dlcl else ''}"
