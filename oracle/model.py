@@ -137,7 +137,9 @@ def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> 
     the GPU stores them and widened back.  "f16" / "bf16": round to nearest even.
     "f8": the projection matrices W_* become q * scale of :func:`quantize_fp8_columns`
     (exact in float64, which is then the returned dtype) and E is rounded to fp16, as
-    an FP8-weight model with fp16 activations stores them.  Biases, LayerNorm and DLCL
+    an FP8-weight model with fp16 activations stores them; the decoder projections fed by
+    a pre-norm LayerNorm quantize the gain-scaled weights instead (see
+    :func:`_fp8_fold_layernorm`; their biases change accordingly).  Biases, LayerNorm and DLCL
     scalars keep fp32: that is what a reduced-precision model stores at full precision.
     """
     if precision == "f32":
@@ -145,7 +147,9 @@ def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> 
     if precision == "f8":
         out = blob.astype(np.float64)
         off = 0
+        where = {}
         for e in synth.weight_layout(shape):
+            where[e.name] = (off, e)
             seg = blob[off:off + e.size]
             if e.name == "E":
                 out[off:off + e.size] = seg.astype(np.float16)
@@ -153,6 +157,9 @@ def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> 
                 q, sc = quantize_fp8_columns(seg.reshape(e.shape))
                 out[off:off + e.size] = (q * sc.astype(np.float64)[None, :]).reshape(-1)
             off += e.size
+        for j in range(shape.n_dec):
+            for ln, w, b in (("ln1", "W_qkv", "b_qkv"), ("ln2", "W_q", "b_q"), ("ln3", "W_1", "b_1")):
+                _fp8_fold_layernorm(blob, out, where, f"dec.{j}.", ln, w, b)
         return out
     out = blob.copy()
     off = 0
@@ -169,6 +176,29 @@ def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> 
                 raise ValueError(precision)
         off += e.size
     return out
+
+
+def _fp8_fold_layernorm(blob, out, where, p, ln, w, b):
+    """FP8 weights of a decoder projection that takes a pre-norm LayerNorm's output.
+
+    Reading (the paper leaves lower precision to future work, Sec. 6): such a projection
+    stores its weights with the LayerNorm's gain folded in, Q = fp8(diag(gamma) W) with
+    diag(gamma) W formed in float32 and quantized per output column, and computes
+    LN0(u) Q + b + beta W, LN0 being the LayerNorm without gain and bias.  The same
+    function is written here as weights for the plain form LN(u; gamma, beta) W' + b':
+    W' = diag(gamma)^-1 Q and b' = b + beta (W - W'), since
+    (LN0(u) * gamma + beta) W' + b' = LN0(u) Q + b + beta W.  A row with gamma = 0 gets
+    W' = 0: its LayerNorm output is the constant beta, whose product b' already holds."""
+    (og, eg), (ow, ew), (ob, eb) = where[p + ln + ".gamma"], where[p + w], where[p + b]
+    gamma = blob[og:og + eg.size]
+    beta = blob[og + eg.size:og + 2 * eg.size]
+    W = blob[ow:ow + ew.size].reshape(ew.shape)
+    q, sc = quantize_fp8_columns((gamma[:, None] * W).astype(np.float32))
+    Q = q * sc.astype(np.float64)[None, :]
+    g = gamma.astype(np.float64)[:, None]
+    W_eff = np.divide(Q, g, out=np.zeros_like(Q), where=g != 0)
+    out[ow:ow + ew.size] = W_eff.reshape(-1)
+    out[ob:ob + eb.size] = blob[ob:ob + eb.size].astype(np.float64) + beta.astype(np.float64) @ (W.astype(np.float64) - W_eff)
 
 
 def param_count_formula(V, d, F, L, Ld):

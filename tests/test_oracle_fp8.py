@@ -7,7 +7,13 @@
   binade, saturation at 448, signed zero.
 * Per-column scaling: each column's largest magnitude maps to exactly 448, the error of
   a normal-range element is at most 1/16 of it, a zero column stays zero.
-* round_weights("f8") changes exactly the projection matrices (and E to fp16).
+* round_weights("f8") changes exactly the projection matrices (and E to fp16), and the
+  biases of the decoder projections that take a pre-norm LayerNorm's output.
+* Those folded projections (reading: their FP8 weights quantize diag(gamma) W): the
+  weights round_weights returns give LN(u; gamma, beta) W' + b' equal to
+  LN0(u) Q + b + beta W, with Q the per-column E4M3 quantization of diag(gamma) W formed by
+  torch's float8_e4m3fn cast and LN0 torch's layer_norm without gain or bias; a row with
+  zero gain included.
 """
 import math
 
@@ -82,11 +88,52 @@ def test_round_weights_f8_changes_exactly_the_matrices():
     off = 0
     for e in synth.weight_layout(shape):
         a, b = blob[off:off + e.size].astype(np.float64), r[off:off + e.size]
+        folded_bias = e.name.startswith("dec.") and e.name.endswith((".b_qkv", ".b_q", ".b_1"))
         if e.name == "E":
             np.testing.assert_array_equal(b, blob[off:off + e.size].astype(np.float16))
         elif ".W_" in e.name:
             assert not np.array_equal(a, b)
-            assert np.abs(a - b).max() <= np.abs(a).max() / 16
+            assert np.abs(a - b).max() <= np.abs(a).max() / 8   # gain-scaled ones: 1/16 of max|gamma W| / min gamma
+        elif folded_bias:
+            assert not np.array_equal(a, b)
         else:
             np.testing.assert_array_equal(a, b)
         off += e.size
+
+
+def _torch_fp8_columns(w32):
+    """Per-column E4M3 quantization by torch: scale = max |column| / 448 (fp32), codes by
+    the float8_e4m3fn cast of w / scale (fp32); returns the dequantized fp64 matrix."""
+    import torch
+    w = torch.from_numpy(w32)
+    amax = w.abs().amax(dim=0)
+    scale = torch.where(amax > 0, amax / torch.tensor(448.0, dtype=torch.float32), torch.tensor(1.0))
+    q = (w / scale[None, :]).to(torch.float8_e4m3fn).to(torch.float64)
+    return (q * scale.to(torch.float64)[None, :]).numpy()
+
+
+@pytest.mark.parametrize("ln,w,b", [("ln1", "W_qkv", "b_qkv"), ("ln2", "W_q", "b_q"), ("ln3", "W_1", "b_1")])
+def test_fp8_decoder_projection_folds_the_layernorm_gain(torch_cpu64, ln, w, b):
+    torch = torch_cpu64
+    shape = synth.ModelShape(64, 2, 256, 1, 2, 50)
+    blob = synth.make_weights(shape, seed=5)
+    named = synth.unpack(shape, blob.copy())
+    p = "dec.1."
+    named[p + ln + ".gamma"][:] = 1.0 + 0.5 * np.random.default_rng(6).standard_normal(shape.d_model)
+    named[p + ln + ".gamma"][7] = 0.0                       # a row whose LayerNorm output is the constant beta
+    named[p + ln + ".beta"][:] = 0.3 * np.random.default_rng(7).standard_normal(shape.d_model)
+    blob = synth.pack(shape, named)
+    named = synth.unpack(shape, blob)
+    r = synth.unpack(shape, oracle.round_weights(blob, shape, "f8"))
+    gamma, beta = named[p + ln + ".gamma"], named[p + ln + ".beta"]
+    W, bias = named[p + w], named[p + b]
+    Q = _torch_fp8_columns((gamma[:, None] * W).astype(np.float32))
+    u = torch.from_numpy(np.random.default_rng(8).normal(0.4, 1.3, size=(9, shape.d_model)))
+    ln0 = torch.nn.functional.layer_norm(u, (shape.d_model,), eps=1e-5).numpy()
+    want = ln0 @ Q + bias.astype(np.float64) + beta.astype(np.float64) @ W.astype(np.float64)
+    got = oracle.layer_norm(u.numpy(), gamma.astype(np.float64), beta.astype(np.float64)) @ r[p + w] + r[p + b]
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    assert not r[p + w][7].any()
+    # and it is not the unfolded quantization: Q / gamma differs from fp8(W)
+    plain = _torch_fp8_columns(W.astype(np.float32))
+    assert np.abs(r[p + w] - plain).max() > 1e-4
