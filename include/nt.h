@@ -307,10 +307,14 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
  * sum_k Bt[n][k] and bias = b + beta W this is LN(A) W + b.  A, Bt and out (ldc) are
  * device arrays in `dtype`; d_colsum [N] and d_bias [N] fp32 device arrays (bias may be
  * NULL).  K % 64 == 0 and K is the whole row.  tile as for nt_op_gemm (2 runs as 4, which
- * holds the row statistics at a higher occupancy).  Asynchronous. */
+ * holds the row statistics at a higher occupancy).  d_bscale: NULL, or (dtype NT_F16
+ * only) Bt holds FP8 E4M3 bytes and column n of A . Bt is multiplied by d_bscale[n] before
+ * the normalisation, as for the decoder projections of an fp8_weights model (colsum then
+ * holds the sums of the dequantized columns); tiles 1 and 4 are then 32x64 and 64x64.
+ * Asynchronous. */
 nt_status nt_op_gemm_ln(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N,
                         int32_t K, const float* d_colsum, float ln_eps, const float* d_bias, void* d_out,
-                        int32_t ldc, int32_t relu, int32_t tile, void* stream);
+                        int32_t ldc, int32_t relu, int32_t tile, const float* d_bscale, void* stream);
 
 /* The FP8 weight quantization nt_load_weights applies with fp8_weights, on the host: W
  * [in][out] fp32 (row-major, y = x W) -> q [out][in] E4M3 codes (OCP, bias 7, ties to

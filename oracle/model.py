@@ -23,6 +23,10 @@ Readings of what the paper leaves open (each is also listed in the design notes)
 * Embedding: y_0 = sqrt(d) E[id] + PE(pos), PE interleaved sin/cos from position 0.
 * Attention scale 1/sqrt(d_head); ReLU FFN; biases on every projection except the
   tied output projection; LayerNorm with biased variance and eps = 1e-5.
+* FP8 key/value cache (with FP8 weights; lower precision is future work in Sec. 6): the
+  decoder's self-attention keys and values are kept as the E4M3 values nearest to them
+  (ties to even, saturating at 448), quantized as they enter the cache, and attention
+  reads them from there, the current step's own key and value included.
 * Relative positions (the teachers are "Transformer-DLCL-RPR" with a maximum relative
   length of 8, Sec. 3.1; the method is Shaw et al., 2018), optional and in encoder
   self-attention only: per layer, key and value tables of 2k+1 rows of d_head shared by
@@ -214,15 +218,18 @@ class OracleModel:
     """The full model on one sentence at a time.
 
     ``blob`` is the canonical fp32 weight vector; ``precision`` rounds its matrices as
-    the GPU stores them ("f32", "f16", "bf16"); arithmetic is done in ``dtype``.
+    the GPU stores them ("f32", "f16", "bf16", "f8"); arithmetic is done in ``dtype``.
+    ``kv_fp8`` keeps the decoder's self-attention keys and values as E4M3 values (by
+    default with precision "f8", the FP8 mode).
     """
 
     def __init__(self, shape: synth.ModelShape, blob: np.ndarray, dtype=np.float64,
-                 precision: str = "f32", hist_norm: bool = True, eps: float = 1e-5):
+                 precision: str = "f32", hist_norm: bool = True, eps: float = 1e-5, kv_fp8=None):
         self.shape = shape
         self.dtype = np.dtype(dtype)
         self.hist_norm = hist_norm
         self.eps = eps
+        self.kv_fp8 = precision == "f8" if kv_fp8 is None else bool(kv_fp8)
         named = synth.unpack(shape, round_weights(blob, shape, precision))
         self.p = {k: v.astype(self.dtype) for k, v in named.items()}
         self.d = shape.d_model
@@ -285,6 +292,12 @@ class OracleModel:
         return out
 
     # -- decoder ----------------------------------------------------------------
+    def self_kv(self, k, v):
+        """A self-attention key/value as the cache keeps it (E4M3 values with kv_fp8)."""
+        if self.kv_fp8:
+            return e4m3_round(k).astype(self.dtype), e4m3_round(v).astype(self.dtype)
+        return k, v
+
     def dec_layer_step(self, z, j, cache_k, cache_v, cross):
         """Incremental decoder layer for one row z [d] at the newest position.
 
@@ -294,8 +307,9 @@ class OracleModel:
         d = self.d
         u = self.ln(z[None, :], p + "ln1")
         qkv = u @ self.p[p + "W_qkv"] + self.p[p + "b_qkv"]
-        k_all = np.concatenate([cache_k, qkv[:, d:2 * d]], axis=0)
-        v_all = np.concatenate([cache_v, qkv[:, 2 * d:]], axis=0)
+        k_new, v_new = self.self_kv(qkv[:, d:2 * d], qkv[:, 2 * d:])
+        k_all = np.concatenate([cache_k, k_new], axis=0)
+        v_all = np.concatenate([cache_v, v_new], axis=0)
         att = attention(qkv[:, :d], k_all, v_all, self.H)
         z = z + (att @ self.p[p + "W_o"] + self.p[p + "b_o"])[0]
         u = self.ln(z[None, :], p + "ln2")
@@ -305,7 +319,7 @@ class OracleModel:
         u = self.ln(z[None, :], p + "ln3")
         f = np.maximum(u @ self.p[p + "W_1"] + self.p[p + "b_1"], 0)
         z = z + (f @ self.p[p + "W_2"] + self.p[p + "b_2"])[0]
-        return z, qkv[0, d:2 * d], qkv[0, 2 * d:]
+        return z, k_new[0], v_new[0]
 
     def output_logits(self, z):
         """logits = LN_dec(z) E^T (tied projection, no bias)."""
@@ -323,7 +337,8 @@ class OracleModel:
             p = f"dec.{j}."
             u = self.ln(z, p + "ln1")
             qkv = u @ self.p[p + "W_qkv"] + self.p[p + "b_qkv"]
-            att = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], self.H, causal)
+            k, v = self.self_kv(qkv[:, d:2 * d], qkv[:, 2 * d:])
+            att = attention(qkv[:, :d], k, v, self.H, causal)
             z = z + att @ self.p[p + "W_o"] + self.p[p + "b_o"]
             u = self.ln(z, p + "ln2")
             q = u @ self.p[p + "W_q"] + self.p[p + "b_q"]

@@ -50,6 +50,28 @@ template <> struct Mfma<float> {
   }
 };
 
+// Code of the OCP FP8 E4M3 value (exponent bias 7, 3 mantissa bits, subnormals in steps
+// of 2^-9, largest finite 448) nearest to x, ties to even; magnitudes beyond 448
+// saturate to 448 and NaN gives 0x7F.  On the fp32 bits: below 2^-6 the value is a
+// multiple of 2^-9 (code 8 is 2^-6 itself), found by an exact scaling and a rounding to
+// the nearest even integer; above, the 23-bit mantissa is rounded to 3 bits (a carry
+// moves into the exponent) and the exponent is rebiased from 127 to 7.  The host
+// quantizer of FP8 weights and the projection that writes an FP8 key/value cache both
+// use it.
+__host__ __device__ inline uint8_t e4m3_rne(float x) {
+  const uint32_t bits = __builtin_bit_cast(uint32_t, x);
+  const uint32_t sign = (bits >> 24) & 0x80u, u = bits & 0x7FFFFFFFu;
+  if (u > 0x7F800000u) return 0x7F;
+  uint32_t code;
+  if (u < 0x3C800000u) {
+    code = (uint32_t)__builtin_rintf(__builtin_bit_cast(float, u) * 512.0f);
+  } else {
+    code = ((u + 0x7FFFFu + ((u >> 20) & 1u)) >> 20) - (120u << 3);
+    if (code > 0x7Eu) code = 0x7Eu;
+  }
+  return (uint8_t)(sign | code);
+}
+
 // Elements of T in one 16-byte vector.
 template <typename T> struct Vec { static constexpr int N = 16 / sizeof(T); };
 

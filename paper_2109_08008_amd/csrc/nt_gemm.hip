@@ -362,7 +362,6 @@ template <typename T, int BM_, int BN_, int STAGES, int ROLE, bool F8 = false, b
 __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int lda, const void* __restrict__ Bt,
                                                     int M, int N, int K, GemmEpi epi, int tiles_m, int tiles_n) {
   static_assert(!F8 || std::is_same<T, f16>::value, "FP8 weights pair with fp16 activations");
-  static_assert(!(F8 && LNF), "a folded LayerNorm needs weights in the model dtype");
   constexpr int ROWB_B = F8 ? ROWB8 : ROWB;
   constexpr int STAGE_BYTES = BM_ * ROWB + BN_ * ROWB_B;
   constexpr int GROUPS_A = BM_ / 8;                 // 8 A rows = one 1 KB wave load
@@ -729,7 +728,19 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
       return hipErrorInvalidValue;
     } else {
       // (128x128 would hold the row statistics at one wave per SIMD: 64x128 instead)
-      if (epi.wscale) return hipErrorInvalidValue;
+      if (epi.wscale) {   // FP8 weights with the gain folded in: the FP8 tile map
+        if constexpr (!std::is_same<T, f16>::value) {
+          return hipErrorInvalidValue;
+        } else {
+          // (the unfolded map's 128x128 becomes 128x64: 164 VGPRs with the row statistics)
+          switch (tile) {
+            case 2:
+            case 3: return launch_tile<T, 128, 64, 2, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
+            case 4: return launch_tile<T, 64, 64, 3, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
+            default: return launch_tile<T, 32, 64, 3, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
+          }
+        }
+      }
       switch (tile) {
         case 2:
         case 4: return launch_tile<T, 64, 128, 2, ROLE, false, true>(A, lda, Bt, M, N, K, epi, s);

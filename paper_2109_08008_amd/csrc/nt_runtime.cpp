@@ -25,6 +25,7 @@
 #include <vector>
 
 #include "../../include/nt.h"
+#include "nt_common.h"
 #include "nt_kernels.h"
 
 using nt::DT;
@@ -292,9 +293,9 @@ ModelLayout layout_of(const nt_model_cfg& c) {
     e.soc = f8 ? take(d * 4) : 0;
     e.s1 = f8 ? take(F * 4) : 0;
     e.s2 = f8 ? take(d * 4) : 0;
-    e.cqkv = f8 ? 0 : take(3 * d * 4);
-    e.cq = f8 ? 0 : take(d * 4);
-    e.c1 = f8 ? 0 : take(F * 4);
+    e.cqkv = take(3 * d * 4);
+    e.cq = take(d * 4);
+    e.c1 = take(F * 4);
     Lo.dec.push_back(e);
   }
   Lo.Wkv_all = take(Ld * 2 * d * d * mb);
@@ -355,27 +356,13 @@ ModelLayout layout_of(const nt_model_cfg& c) {
 // FP8 weights: OCP E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa bits; subnormals
 // of 2^-9; no infinities; 0x7F / 0xFF are NaN, so the largest finite value is 448).
 
-// Code of the E4M3 value nearest to x, ties to even; magnitudes beyond 448 saturate.
-uint8_t e4m3_code(float x) {
-  const uint8_t sign = std::signbit(x) ? 0x80 : 0;
-  const float a = std::fabs(x);
-  if (std::isnan(a)) return 0x7F;
-  if (a == 0.f) return sign;
-  int E;
-  (void)std::frexp(a, &E);          // a = f * 2^E, f in [0.5, 1): binade 2^(E-1)
-  int e = std::max(E - 1, -6);      // below 2^-6 the step stays 2^-9 (subnormals)
-  // a in units of the binade's step 2^(e-3) (exact scaling), rounded half to even
-  int m = (int)std::nearbyint(std::ldexp(a, 3 - e));
-  if (e == -6 && m < 8) return sign | (uint8_t)m;   // subnormal: exponent field 0
-  if (m == 16) {                    // rounded up into the next binade
-    m = 8;
-    ++e;
-  }
-  if (e > 8 || (e == 8 && m > 14)) {   // beyond 448 = 1.75 * 2^8
-    e = 8;
-    m = 14;
-  }
-  return sign | (uint8_t)(((e + 7) << 3) | (m - 8));
+uint8_t e4m3_code(float x) { return nt::e4m3_rne(x); }
+
+// Value of an E4M3 code (finite codes only; the quantizer never produces NaN).
+double e4m3_value(uint8_t c) {
+  const int e = (c >> 3) & 15, m = c & 7;
+  const double v = e == 0 ? std::ldexp((double)m, -9) : std::ldexp(8.0 + m, e - 10);
+  return (c & 0x80) ? -v : v;
 }
 
 // Weight matrix W [in][out] (row-major, y = x W) as FP8 codes q [out][in] (the GEMM's
@@ -1282,14 +1269,15 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     if (e != hipSuccess) return e;
     return hipMemcpyAsync(base + scale_off, keep_s.back().data(), keep_s.back().size() * 4, hipMemcpyHostToDevice, s);
   };
-  // A pre-norm LayerNorm folded into the projection it feeds (decoder layers, weights in
-  // the model dtype): LN(x) W + b = rstd (x W' - mean colsum(W')) + b' with
-  // W' = diag(gamma) W and b' = b + beta W.  W' (fp32 products) replaces W in the staging
-  // copy before packing, b' is summed in double, and the column sums come from the packed
-  // matrix, so they are those of the values the GEMM multiplies.
+  // A pre-norm LayerNorm folded into the projection it feeds (decoder layers):
+  // LN(x) W + b = rstd (x W' - mean colsum(W')) + b' with W' = diag(gamma) W and
+  // b' = b + beta W.  W' (fp32 products) replaces W in the staging copy before packing, b'
+  // is summed in double, and the column sums come from the packed matrix, so they are
+  // those of the values the GEMM multiplies.  With FP8 weights W' is what is quantized
+  // (per output column), and the column sums are those of the dequantized codes.
   std::deque<std::vector<float>> keep_f;   // element references stay valid as it grows
   auto folded = [&](size_t dev_w, size_t dev_b, size_t dev_c, size_t hw, size_t hb, size_t hln, int in,
-                    int outn) -> hipError_t {
+                    int outn, size_t scale_off) -> hipError_t {
     const float* W = host_weights + hw;
     const float* g = host_weights + hln;
     const float* be = host_weights + hln + in;
@@ -1304,9 +1292,28 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
       for (int k = 0; k < in; ++k) acc += (double)be[k] * W[(size_t)k * outn + n];
       bf[n] = (float)acc;
     }
-    hipError_t e = hipMemcpyAsync(staging + hw, Wf.data(), Wf.size() * 4, hipMemcpyHostToDevice, s);
+    hipError_t e = hipMemcpyAsync(base + dev_b, bf.data(), bf.size() * 4, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return e;
+    if (f8) {
+      keep_q.emplace_back();
+      keep_s.emplace_back();
+      quantize_fp8(Wf.data(), in, outn, keep_q.back(), keep_s.back());
+      const std::vector<uint8_t>& q = keep_q.back();
+      const std::vector<float>& sc = keep_s.back();
+      keep_f.emplace_back(outn);
+      std::vector<float>& cs = keep_f.back();
+      for (int n = 0; n < outn; ++n) {
+        double acc = 0.0;
+        for (int k = 0; k < in; ++k) acc += e4m3_value(q[(size_t)n * in + k]);
+        cs[n] = (float)(acc * (double)sc[n]);
+      }
+      e = hipMemcpyAsync(base + dev_w, q.data(), q.size(), hipMemcpyHostToDevice, s);
+      if (e == hipSuccess) e = hipMemcpyAsync(base + scale_off, sc.data(), sc.size() * 4, hipMemcpyHostToDevice, s);
+      if (e == hipSuccess) e = hipMemcpyAsync(base + dev_c, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, s);
+      return e;
+    }
+    e = hipMemcpyAsync(staging + hw, Wf.data(), Wf.size() * 4, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = nt::pack_transpose(dt, staging + hw, base + dev_w, in, outn, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(base + dev_b, bf.data(), bf.size() * 4, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = nt::packed_row_sums(dt, base + dev_w, outn, in, reinterpret_cast<float*>(base + dev_c), s);
     return e;
   };
@@ -1340,18 +1347,9 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     NT_HIP(vec(D.ln1, Hh.ln1, 2 * d));
     NT_HIP(vec(D.ln2, Hh.ln2, 2 * d));
     NT_HIP(vec(D.ln3, Hh.ln3, 2 * d));
-    if (f8) {
-      NT_HIP(mat(D.Wqkv, Hh.Wqkv, d, 3 * d, D.sqkv));
-      NT_HIP(vec(D.bqkv, Hh.bqkv, 3 * d));
-      NT_HIP(mat(D.Wq, Hh.Wq, d, d, D.sq));
-      NT_HIP(vec(D.bq, Hh.bq, d));
-      NT_HIP(mat(D.W1, Hh.W1, d, F, D.s1));
-      NT_HIP(vec(D.b1, Hh.b1, F));
-    } else {
-      NT_HIP(folded(D.Wqkv, D.bqkv, D.cqkv, Hh.Wqkv, Hh.bqkv, Hh.ln1, d, 3 * d));
-      NT_HIP(folded(D.Wq, D.bq, D.cq, Hh.Wq, Hh.bq, Hh.ln2, d, d));
-      NT_HIP(folded(D.W1, D.b1, D.c1, Hh.W1, Hh.b1, Hh.ln3, d, F));
-    }
+    NT_HIP(folded(D.Wqkv, D.bqkv, D.cqkv, Hh.Wqkv, Hh.bqkv, Hh.ln1, d, 3 * d, D.sqkv));
+    NT_HIP(folded(D.Wq, D.bq, D.cq, Hh.Wq, Hh.bq, Hh.ln2, d, d, D.sq));
+    NT_HIP(folded(D.W1, D.b1, D.c1, Hh.W1, Hh.b1, Hh.ln3, d, F, D.s1));
     NT_HIP(mat(D.Wo, Hh.Wo, d, d, D.so));
     NT_HIP(vec(D.bo, Hh.bo, d));
     NT_HIP(mat(D.Woc, Hh.Woc, d, d, D.soc));
@@ -1410,7 +1408,7 @@ nt_status nt_load_weights(const nt_model_cfg* cfg, const float* host_weights, si
     const auto& D = Lo.dec[j];
     m->dec.push_back({fp(D.ln1), fp(D.bqkv), fp(D.bo), fp(D.ln2), fp(D.bq), fp(D.boc), fp(D.ln3), fp(D.b1), fp(D.b2),
                       base + D.Wqkv, base + D.Wo, base + D.Wq, base + D.Woc, base + D.W1, base + D.W2});
-    if (!f8) {
+    {
       DecLayerW& w = m->dec.back();
       w.cqkv = fp(D.cqkv);
       w.cq = fp(D.cq);
@@ -1809,7 +1807,7 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
 
 nt_status nt_op_gemm_ln(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N,
                         int32_t K, const float* d_colsum, float ln_eps, const float* d_bias, void* d_out,
-                        int32_t ldc, int32_t relu, int32_t tile, void* stream) {
+                        int32_t ldc, int32_t relu, int32_t tile, const float* d_bscale, void* stream) {
   g_err.clear();
   if (!d_A || !d_Bt || !d_out || !d_colsum) return fail(NT_E_INVALID, "null argument to nt_op_gemm_ln");
   if (dtype < NT_F32 || dtype > NT_BF16) return fail(NT_E_INVALID, "unknown dtype %d", dtype);
@@ -1819,7 +1817,9 @@ nt_status nt_op_gemm_ln(int32_t dtype, const void* d_A, int32_t lda, const void*
     return fail(NT_E_INVALID, "lda must be >= K with 16-byte rows, ldc >= N");
   if (tile < 0 || tile > 4) return fail(NT_E_INVALID, "tile must be 0..4");
   if (!(ln_eps > 0.f)) return fail(NT_E_INVALID, "ln_eps must be positive");
+  if (d_bscale && dtype != NT_F16) return fail(NT_E_UNSUPPORTED, "FP8 weights (d_bscale) need dtype NT_F16");
   nt::GemmEpi e{};
+  e.wscale = d_bscale;
   e.mode = relu ? nt::EPI_RELU : nt::EPI_STORE;
   e.bias = d_bias;
   e.out = d_out;

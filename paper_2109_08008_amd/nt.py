@@ -106,7 +106,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_op_gemm": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, P, P, c_int32, c_int32, c_int32,
                                  c_int32, P, P]),
         "nt_op_gemm_ln": (c_int32, [c_int32, P, c_int32, P, c_int32, c_int32, c_int32, P, c_float, P, P, c_int32,
-                                    c_int32, c_int32, P]),
+                                    c_int32, c_int32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -267,11 +267,11 @@ def nt_op_gemm(dtype: str, d_A: int, lda: int, d_Bt: int, M: int, N: int, K: int
 
 
 def nt_op_gemm_ln(dtype: str, d_A: int, lda: int, d_Bt: int, M: int, N: int, K: int, d_colsum: int, ln_eps: float,
-                  d_bias, d_out: int, ldc: int, relu: bool = False, tile: int = 0, stream=None):
+                  d_bias, d_out: int, ldc: int, relu: bool = False, tile: int = 0, d_bscale=None, stream=None):
     _check(load_library().nt_op_gemm_ln(DTYPES[dtype], c_void_p(d_A), lda, c_void_p(d_Bt), M, N, K,
                                         c_void_p(d_colsum), float(ln_eps),
                                         c_void_p(d_bias) if d_bias else None, c_void_p(d_out), ldc, int(relu),
-                                        tile, _stream(stream)))
+                                        tile, c_void_p(d_bscale) if d_bscale else None, _stream(stream)))
 
 
 def nt_quantize_fp8(w: np.ndarray):

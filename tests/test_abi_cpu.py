@@ -159,3 +159,27 @@ def test_fp8_weight_configs(nt):
     assert hf8 == hf16 and db16 - db8 >= mats - 4 * 2 * 1024 * 16
     lib = nt.load_library()
     assert lib.nt_quantize_fp8(None, 4, 4, None, None) == nt.NT_E_INVALID
+
+
+def test_library_e4m3_rounding_over_the_whole_range(nt):
+    """The E4M3 rounding the library shares between its weight quantizer and its FP8
+    key/value cache, reached through the quantizer with columns whose largest magnitude is
+    448 (scale exactly 1): every midpoint between neighbouring E4M3 values (ties to even),
+    every E4M3 value, and random magnitudes from 2^-14 to 448 of both signs, against
+    torch's float8_e4m3fn cast."""
+    import torch
+    grid = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    grid = np.unique(grid[np.isfinite(grid)])
+    mids = (grid[1:] + grid[:-1]) / 2
+    rng = np.random.default_rng(9)
+    rand = np.ldexp(rng.uniform(1.0, 2.0, 3000), rng.integers(-14, 9, 3000)) * rng.choice([-1.0, 1.0], 3000)
+    vals = np.concatenate([grid, mids, rand[np.abs(rand) <= 448.0]]).astype(np.float32)
+    w = np.zeros((len(vals), 2), dtype=np.float32)
+    w[:, 0] = vals
+    w[:, 1] = -vals
+    w[0, :] = 448.0   # the column maximum: scale 1
+    q, sc = nt.nt_quantize_fp8(w)
+    np.testing.assert_array_equal(sc, [1.0, 1.0])
+    decoded = torch.from_numpy(q).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    want = torch.from_numpy(w.T.copy()).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(decoded, want)

@@ -26,16 +26,18 @@ def _rows(M, K, seed, tdt):
     return (torch.randn(M, K, generator=g) * scale + mean).to(tdt)
 
 
-def _run(dtype, A, Bt, colsum, bias=None, relu=False, tile=0):
+def _run(dtype, A, Bt, colsum, bias=None, relu=False, tile=0, bscale=None):
     import torch
     from paper_2109_08008_amd import nt
     M, K = A.shape
     N = Bt.shape[0]
     dA, dB, dc = A.cuda(), Bt.cuda(), colsum.float().cuda()
     db = bias.float().cuda() if bias is not None else None
+    ds = bscale.float().cuda() if bscale is not None else None
     out = torch.full((M, N), float("nan"), dtype=A.dtype, device="cuda")
     nt.nt_op_gemm_ln(dtype, dA.data_ptr(), K, dB.data_ptr(), M, N, K, dc.data_ptr(), EPS,
-                     db.data_ptr() if db is not None else 0, out.data_ptr(), N, relu, tile)
+                     db.data_ptr() if db is not None else 0, out.data_ptr(), N, relu, tile,
+                     ds.data_ptr() if ds is not None else None)
     torch.cuda.synchronize()
     return out.cpu()
 
@@ -140,5 +142,31 @@ def test_folded_ln_large_mean_rows(dtype, tile, M, N, K):
     got = _run(dtype, A, Bt, colsum, bias=bias, tile=tile)
     assert not torch.isnan(got).any()
     tol = want.abs().max().item() * ULP[dtype] + 8 * 2.0 ** -24 * K * np.sqrt(K)
+    err = (got.double() - want).abs().max().item()
+    assert err <= tol, (err, tol)
+
+
+@pytest.mark.parametrize("tile", [1, 3, 4])
+@pytest.mark.parametrize("M,N,K", [(1, 8, 64), (37, 100, 512), (200, 520, 128), (300, 1000, 1024), (129, 136, 576)])
+def test_fp8_folded_ln_gemm_matches_fp64(tile, M, N, K):
+    """FP8 E4M3 weights with the LayerNorm gain folded in, as an fp8_weights model's decoder
+    projections run: codes and column scales of diag(gamma) W from the library's quantizer,
+    colsum of the dequantized columns; the result is LN0(A) Q + bias, Q the dequantized
+    matrix, to the folded fp16 projection's bound."""
+    import torch
+    from paper_2109_08008_amd import nt
+    g = torch.Generator().manual_seed(M + 11 * N + K)
+    A = _rows(M, K, M + 3 * N + K, torch.float16)
+    W = torch.randn(K, N, generator=g, dtype=torch.float64) * 0.05
+    gamma = 1.0 + 0.3 * torch.randn(K, generator=g, dtype=torch.float64)
+    q, sc = nt.nt_quantize_fp8((gamma[:, None] * W).float().numpy())
+    qt, sct = torch.from_numpy(q), torch.from_numpy(sc)
+    deq = qt.view(torch.float8_e4m3fn).double() * sct.double()[:, None]   # [N][K]
+    bias = torch.randn(N, generator=g)
+    want = _ln64(A) @ deq.T + bias.double()
+    got = _run("f16", A, qt, deq.sum(dim=1), bias=bias, tile=tile, bscale=sct)
+    assert not torch.isnan(got).any()
+    mu = A.double().mean(dim=1).abs().max().item()
+    tol = want.abs().max().item() * ULP["f16"] + 64 * 2.0 ** -24 * K * np.sqrt(K) * (1 + mu)
     err = (got.double() - want).abs().max().item()
     assert err <= tol, (err, tol)

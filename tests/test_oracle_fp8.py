@@ -137,3 +137,58 @@ def test_fp8_decoder_projection_folds_the_layernorm_gain(torch_cpu64, ln, w, b):
     # and it is not the unfolded quantization: Q / gamma differs from fp8(W)
     plain = _torch_fp8_columns(W.astype(np.float32))
     assert np.abs(r[p + w] - plain).max() > 1e-4
+
+
+def _torch_decoder_fp8_kv(torch, shape, blob, enc, tgt):
+    """Reference decoder in torch (fp64) whose self-attention keys and values go through
+    torch's float8_e4m3fn cast before scaled_dot_product_attention (causal): the FP8 cache."""
+    F = torch.nn.functional
+    d, H = shape.d_model, shape.n_heads
+    dh = d // H
+    P = {k: torch.tensor(v.astype(np.float64)) for k, v in synth.unpack(shape, blob).items()}
+    enc = torch.tensor(enc)
+
+    def ln(x, p):
+        return F.layer_norm(x, (d,), P[p + ".gamma"], P[p + ".beta"], eps=1e-5)
+
+    def heads(x):
+        return x.reshape(x.shape[0], H, dh).transpose(0, 1)
+
+    inp = torch.tensor([synth.BOS_ID] + list(tgt))
+    n = len(inp)
+    z = math.sqrt(d) * P["E"][inp] + torch.tensor(oracle.positional_encoding(np.arange(n), d))
+    for j in range(shape.n_dec):
+        p = f"dec.{j}."
+        qkv = ln(z, p + "ln1") @ P[p + "W_qkv"] + P[p + "b_qkv"]
+        q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+        k8 = k.float().to(torch.float8_e4m3fn).to(torch.float64)
+        v8 = v.float().to(torch.float8_e4m3fn).to(torch.float64)
+        att = F.scaled_dot_product_attention(heads(q), heads(k8), heads(v8), is_causal=True)
+        z = z + att.transpose(0, 1).reshape(n, d) @ P[p + "W_o"] + P[p + "b_o"]
+        qc = ln(z, p + "ln2") @ P[p + "W_q"] + P[p + "b_q"]
+        kv = enc @ P[p + "W_kv"] + P[p + "b_kv"]
+        att = F.scaled_dot_product_attention(heads(qc), heads(kv[:, :d]), heads(kv[:, d:]))
+        z = z + att.transpose(0, 1).reshape(n, d) @ P[p + "W_oc"] + P[p + "b_oc"]
+        f = torch.relu(ln(z, p + "ln3") @ P[p + "W_1"] + P[p + "b_1"])
+        z = z + f @ P[p + "W_2"] + P[p + "b_2"]
+    return (ln(z, "dec_out_ln") @ P["E"].T).numpy()
+
+
+def test_fp8_kv_cache_matches_torch_float8_decoder(torch_cpu64):
+    """The oracle's FP8 key/value cache against torch's float8 cast and attention, on a
+    model with large self-attention keys and values (lively weights) so that the rounding
+    matters; incremental decoding equals full recomputation with the cache quantized; and
+    the quantization moves the logits."""
+    torch = torch_cpu64
+    shape = synth.ModelShape(32, 4, 128, 2, 2, 23)
+    blob = synth.make_weights(shape, seed=12, lively=True)
+    src, tgt = [5, 9, 17, 4, 22, 8], [7, 3, 19, 2, 11, 6]
+    om = oracle.OracleModel(shape, blob, np.float64, kv_fp8=True)
+    want = _torch_decoder_fp8_kv(torch, shape, blob, om.encode(src), tgt)
+    inc = om.teacher_forced_logits(src, tgt)
+    full = om.teacher_forced_logits(src, tgt, incremental=False)
+    np.testing.assert_allclose(inc, want, rtol=0, atol=1e-10)
+    np.testing.assert_allclose(inc, full, rtol=0, atol=1e-12)
+    plain = oracle.OracleModel(shape, blob, np.float64).teacher_forced_logits(src, tgt)
+    assert np.abs(plain - inc).max() > 1e-3
+    assert oracle.OracleModel(shape, blob, np.float64, precision="f8").kv_fp8
