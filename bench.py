@@ -39,7 +39,7 @@ import synth  # noqa: E402
 PEAK = {  # MI355X published peaks (dense)
     "hbm_GBps": 8000.0,
     # FP8 weights are widened to fp16 inside the GEMM, whose contraction runs on the fp16 MFMA
-    "mfma_TFLOPs": {"f16": 2500.0, "bf16": 2500.0, "f8": 2500.0, "f32": 157.3},
+    "mfma_TFLOPs": {"f16": 2500.0, "bf16": 2500.0, "f8": 2500.0, "f8w": 2500.0, "f32": 157.3},
 }
 GEMM_CLASSES = (0, 1, 2)
 

@@ -72,7 +72,15 @@ typedef struct nt_dec_state nt_dec_state;
  *    nearest (ties to even) to W[k,n] / scale_n, both computed in fp32 by
  *    nt_load_weights.  The projections multiply fp16 activations by q exactly (every
  *    E4M3 value is an fp16 value) and scale the fp32 sums.  E (embedding and output
- *    projection) stays fp16; activations and every reduction are as for NT_F16. */
+ *    projection) stays fp16; activations and every reduction are as for NT_F16.  The
+ *    decoder projections that take a pre-norm LayerNorm's output (QKV, cross-Q, FFN1)
+ *    quantize the gain-scaled weights diag(gamma) W instead and normalise their input
+ *    rows themselves.
+ *  fp8_kv: 0, or 1 with dtype NT_F16: the decoder's self-attention key/value cache holds
+ *    OCP FP8 E4M3 values, each the E4M3 value nearest (ties to even, saturating at 448)
+ *    to the fp32 key or value the QKV projection computes; attention widens them exactly.
+ *    Halves the bytes the self-attention streams every step (Sec. 6 leaves lower
+ *    precision to future work; this is one reading of it). */
 typedef struct {
   int32_t d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_positions;
   int32_t pad_id, bos_id, eos_id;
@@ -81,6 +89,7 @@ typedef struct {
   float ln_eps;
   int32_t rel_pos_k;
   int32_t fp8_weights;
+  int32_t fp8_kv;
 } nt_model_cfg;
 
 /* Search and batching options.

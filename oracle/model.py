@@ -139,7 +139,7 @@ def quantize_fp8_columns(w):
 def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> np.ndarray:
     """Return a copy of the fp32 blob whose *matrices* (E and every W_*) are rounded as
     the GPU stores them and widened back.  "f16" / "bf16": round to nearest even.
-    "f8": the projection matrices W_* become q * scale of :func:`quantize_fp8_columns`
+    "f8" (and "f8w", the same weights): the projection matrices W_* become q * scale of :func:`quantize_fp8_columns`
     (exact in float64, which is then the returned dtype) and E is rounded to fp16, as
     an FP8-weight model with fp16 activations stores them; the decoder projections fed by
     a pre-norm LayerNorm quantize the gain-scaled weights instead (see
@@ -148,7 +148,7 @@ def round_weights(blob: np.ndarray, shape: synth.ModelShape, precision: str) -> 
     """
     if precision == "f32":
         return blob.copy()
-    if precision == "f8":
+    if precision in ("f8", "f8w"):
         out = blob.astype(np.float64)
         off = 0
         where = {}
@@ -220,7 +220,7 @@ class OracleModel:
     ``blob`` is the canonical fp32 weight vector; ``precision`` rounds its matrices as
     the GPU stores them ("f32", "f16", "bf16", "f8"); arithmetic is done in ``dtype``.
     ``kv_fp8`` keeps the decoder's self-attention keys and values as E4M3 values (by
-    default with precision "f8", the FP8 mode).
+    default with precision "f8", the FP8 mode; "f8w" is FP8 weights alone).
     """
 
     def __init__(self, shape: synth.ModelShape, blob: np.ndarray, dtype=np.float64,

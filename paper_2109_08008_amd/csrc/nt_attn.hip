@@ -12,6 +12,8 @@
 // ancestor hypothesis (anc table), so beams never copy caches when they reorder.  With
 // a single query per row this is a streaming kernel, not a contraction, so it stays on
 // the vector units.
+#include <type_traits>
+
 #include "nt_common.h"
 #include "nt_kernels.h"
 
@@ -313,9 +315,37 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
 // softmax is online across chunks, in fp32.  No LDS, so occupancy is set by registers:
 // four keys a lane (80 VGPRs at fp16, six waves a SIMD) measured 4% faster on base-6-6
 // than eight (91 VGPRs, five waves), and two (66 VGPRs) no faster than four.
-template <typename T, int DH>
+//
+// KV is the cache's element type: the model dtype, or E4M3 bytes (uint8_t) in FP8 mode,
+// where a 16-byte chunk carries 16 channels (64-byte keys at d_head 64 on 4 lanes), the
+// query and the output stay fp16, and the codes are widened exactly (through fp16).
+template <typename KV> struct KvChunk {
+  static __device__ __forceinline__ void get(const uint4& r, float* out) {
+    const KV* e = reinterpret_cast<const KV*>(&r);
+#pragma unroll
+    for (int i = 0; i < 16 / (int)sizeof(KV); ++i) out[i] = to_f32(e[i]);
+  }
+};
+template <> struct KvChunk<uint8_t> {
+  static __device__ __forceinline__ void get(const uint4& r, float* out) {
+    const unsigned w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const auto lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w[i], 1.0f, false);   // bytes 0, 1
+      const auto hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w[i], 1.0f, true);    // bytes 2, 3
+      out[4 * i] = (float)lo[0];
+      out[4 * i + 1] = (float)lo[1];
+      out[4 * i + 2] = (float)hi[0];
+      out[4 * i + 3] = (float)hi[1];
+    }
+  }
+};
+template <typename T, int DH, typename KV>
 __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
-  constexpr int VEC = Vec<T>::N, CPR = DH / VEC, GPW = kWave / CPR, KPL = 4, KCH = GPW * KPL;
+  // KPL keys a lane: 4 of 2-byte (or wider) elements, 2 of E4M3 bytes -- the same 128 bytes
+  // of keys and values in flight per lane and 32 keys per wave (118 VGPRs with 4 E4M3 keys)
+  constexpr int VEC = 16 / (int)sizeof(KV), CPR = DH / VEC, GPW = kWave / CPR;
+  constexpr int KPL = sizeof(KV) == 1 ? 2 : 4, KCH = GPW * KPL;
   static_assert(CPR >= 1 && CPR <= kWave && (CPR & (CPR - 1)) == 0, "a key's chunks fit in a wave");
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   // every argument the wave uses, named at entry: their scalar-cache misses overlap
@@ -330,7 +360,7 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   // waits for the live-row check.
   const int sent = a.sent_list[row / a.beam];
   float q[VEC];
-  load16(static_cast<const T*>(a.q) + (size_t)row * a.H * DH + h * DH + c * VEC, q);
+  load_row<T, VEC>(static_cast<const T*>(a.q) + (size_t)row * a.H * DH + h * DH + c * VEC, q);
   const int nlive = a.ctl[CTL_NLIVE], t = a.ctl[CTL_T], asel = a.ctl[CTL_ANC];
   asm volatile("" ::"v"(sent), "s"(nlive), "s"(t), "s"(asel));
   if (row >= min(a.rows, nlive * a.beam)) return;   // whole wave exits; no block barrier below
@@ -340,8 +370,8 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   const int n = t + 1;
   const int* anc = a.anc ? a.anc + (size_t)asel * a.anc_stride + (size_t)p * a.Tcap : nullptr;
   const size_t head = (size_t)h * a.Tcap * DH + c * VEC;
-  const T* K = static_cast<const T*>(a.kcache) + head;
-  const T* Vc = static_cast<const T*>(a.vcache) + head;
+  const KV* K = static_cast<const KV*>(a.kcache) + head;
+  const KV* Vc = static_cast<const KV*>(a.vcache) + head;
   const size_t row_stride = (size_t)a.H * a.Tcap * DH;
   float m = -INFINITY, lsum = 0.f, o[VEC];
 #pragma unroll
@@ -366,10 +396,11 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
     float sc[KPL], cmax = -INFINITY;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
-      const T* ke = reinterpret_cast<const T*>(&kr[j]);
+      float ke[VEC];
+      KvChunk<KV>::get(kr[j], ke);
       float dot = 0.f;
 #pragma unroll
-      for (int x = 0; x < VEC; ++x) dot += q[x] * to_f32(ke[x]);
+      for (int x = 0; x < VEC; ++x) dot += q[x] * ke[x];
       if constexpr (CPR <= 16) {
         dot = group_sum<CPR>(dot);
       } else {
@@ -387,10 +418,11 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
       const float pj = __expf(sc[j] - mn);
-      const T* ve = reinterpret_cast<const T*>(&vr[j]);
+      float ve[VEC];
+      KvChunk<KV>::get(vr[j], ve);
       ps += pj;
 #pragma unroll
-      for (int x = 0; x < VEC; ++x) o[x] += pj * to_f32(ve[x]);
+      for (int x = 0; x < VEC; ++x) o[x] += pj * ve[x];
     }
     lsum = lsum * alpha + (c == 0 ? ps : 0.f);   // one lane per key group counts its keys
     m = mn;
@@ -403,7 +435,7 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   if (g == 0) {
 #pragma unroll
     for (int x = 0; x < VEC; ++x) o[x] *= inv;
-    store16(static_cast<T*>(a.out) + (size_t)row * a.H * DH + h * DH + c * VEC, o);
+    store_row<T, VEC>(static_cast<T*>(a.out) + (size_t)row * a.H * DH + h * DH + c * VEC, o);
   }
 }
 
@@ -432,7 +464,13 @@ hipError_t mha_t(const MhaArgs& a, hipStream_t s) {
 template <typename T, int DH>
 void self_launch(const SelfAttnArgs& a, hipStream_t s) {
   const dim3 grid((a.rows * a.H + 3) / 4);
-  NT_LAUNCH((self_attn_kernel<T, DH>), grid, dim3(4 * kWave), 0, s, a);
+  if constexpr (std::is_same<T, f16>::value) {
+    if (a.kv_f8) {
+      NT_LAUNCH((self_attn_kernel<T, DH, uint8_t>), grid, dim3(4 * kWave), 0, s, a);
+      return;
+    }
+  }
+  NT_LAUNCH((self_attn_kernel<T, DH, T>), grid, dim3(4 * kWave), 0, s, a);
 }
 
 template <typename T>
@@ -460,6 +498,7 @@ hipError_t mha(DT dt, const MhaArgs& a, hipStream_t s, int role) {
 
 hipError_t self_attn(DT dt, const SelfAttnArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
+  if (a.kv_f8 && dt != DT::F16) return hipErrorInvalidValue;   // the FP8 cache pairs with fp16
   switch (dt) {
     case DT::F32: return self_t<float>(a, s);
     case DT::F16: return self_t<f16>(a, s);

@@ -158,7 +158,20 @@ __device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N,
       c -= kv * e.d;
       const int h = c / e.dh, x = c - h * e.dh;
       const int p = e.sent_list[m / e.beam] * e.beam + m % e.beam;
-      o = static_cast<T*>(kv ? e.vcache : e.kcache) + ((size_t)(p * e.H + h) * e.Tcap + t_slot) * e.dh + x;
+      const size_t idx = ((size_t)(p * e.H + h) * e.Tcap + t_slot) * e.dh + x;
+      if (e.kv_f8) {   // E4M3 cache: the 4 columns as 4 bytes, one 32-bit store (idx % 4 == 0)
+        uint8_t* o8 = static_cast<uint8_t*>(kv ? e.vcache : e.kcache) + idx;
+        if (cnt == 4) {
+          *reinterpret_cast<uint32_t*>(o8) = (uint32_t)e4m3_rne(v[0]) | ((uint32_t)e4m3_rne(v[1]) << 8) |
+                                             ((uint32_t)e4m3_rne(v[2]) << 16) | ((uint32_t)e4m3_rne(v[3]) << 24);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (k < cnt) o8[k] = e4m3_rne(v[k]);
+        }
+        return;
+      }
+      o = static_cast<T*>(kv ? e.vcache : e.kcache) + idx;
     }
   } else {
     static_assert(MODE == EPI_CROSS_KV, "epilogue mode");

@@ -76,6 +76,7 @@ struct GemmEpi {
   int beam = 1;
   void* kcache = nullptr;          // [R][H][Tcap][dh] of this layer
   void* vcache = nullptr;
+  int kv_f8 = 0;                   // 1: the caches hold E4M3 bytes (e4m3_rne of the fp32 value)
   int t = 0, Tcap = 0;
   // EPI_SELF_QKV / EPI_CROSS_KV
   int d = 0, H = 0, dh = 0;
@@ -207,6 +208,7 @@ struct SelfAttnArgs {
   int rows, H, dh, Tcap;      // rows: launch maximum; live rows = ctl[CTL_NLIVE] * beam
   float scale;
   const int* ctl;             // step t = ctl[CTL_T]
+  int kv_f8;                  // 1: the caches hold E4M3 bytes (q and out stay fp16)
 };
 hipError_t self_attn(DT dt, const SelfAttnArgs& a, hipStream_t s);
 

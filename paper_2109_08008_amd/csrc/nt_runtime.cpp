@@ -211,6 +211,8 @@ nt_status validate_cfg(const nt_model_cfg* c) {
   if (c->rel_pos_k < 0 || c->rel_pos_k > 16) return fail(NT_E_UNSUPPORTED, "rel_pos_k %d outside [0, 16]", c->rel_pos_k);
   if (c->fp8_weights != 0 && c->fp8_weights != 1) return fail(NT_E_INVALID, "fp8_weights must be 0 or 1");
   if (c->fp8_weights && c->dtype != NT_F16) return fail(NT_E_UNSUPPORTED, "fp8_weights needs dtype NT_F16");
+  if (c->fp8_kv != 0 && c->fp8_kv != 1) return fail(NT_E_INVALID, "fp8_kv must be 0 or 1");
+  if (c->fp8_kv && c->dtype != NT_F16) return fail(NT_E_UNSUPPORTED, "fp8_kv needs dtype NT_F16");
   return NT_OK;
 }
 
@@ -464,8 +466,9 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
     const size_t di = mi.d;
     p.mem[i].enc_out = take(T * di * eb);
     p.mem[i].cross = take((size_t)mi.Ld * 2 * T * di * eb);
-    p.mem[i].kself = take((size_t)mi.Ld * R * Tcap * di * eb);
-    p.mem[i].vself = take((size_t)mi.Ld * R * Tcap * di * eb);
+    const size_t kvb = mi.cfg.fp8_kv ? 1 : eb;   // E4M3 keys and values, or the model dtype
+    p.mem[i].kself = take((size_t)mi.Ld * R * Tcap * di * kvb);
+    p.mem[i].vself = take((size_t)mi.Ld * R * Tcap * di * kvb);
   }
   p.score = take(R * 4);
   p.cur_tok = take(R * 4);
@@ -750,6 +753,8 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
     const int d = m.d;
     const double eb = (double)m.eb;
     const float eps = m.cfg.ln_eps;
+    const int kv8 = m.cfg.fp8_kv ? 1 : 0;     // the self-attention cache holds E4M3 bytes
+    const size_t kvb = kv8 ? 1 : m.eb;
 
     // Algorithmic bytes of a decode-step launch count what the step must move: the
     // weights (read once per step, shared by every row) and, for the vocabulary
@@ -779,8 +784,8 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
 
     for (int j = 0; j < m.Ld; ++j) {
       const DecLayerW& w = m.dec[j];
-      char* kc = at(mp.kself) + (size_t)j * Rp * st->Tcap * d * m.eb;
-      char* vc = at(mp.vself) + (size_t)j * Rp * st->Tcap * d * m.eb;
+      char* kc = at(mp.kself) + (size_t)j * Rp * st->Tcap * d * kvb;
+      char* vc = at(mp.vself) + (size_t)j * Rp * st->Tcap * d * kvb;
 
       nt::GemmEpi e{};
       e.mode = nt::EPI_SELF_QKV;
@@ -792,6 +797,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       e.beam = K;
       e.kcache = kc;
       e.vcache = vc;
+      e.kv_f8 = kv8;
       e.Tcap = st->Tcap;
       e.d = d;
       e.H = m.H;
@@ -818,7 +824,8 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       sa.Tcap = st->Tcap;
       sa.scale = 1.0f / std::sqrt((float)m.dh);
       sa.ctl = ctl;
-      NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * eb * 2.0 * (t + 1), 4.0 * R * (t + 1) * (double)d,
+      sa.kv_f8 = kv8;
+      NT_HIP(timed(NT_K_ATTN_SELF, s, (double)R * d * (double)kvb * 2.0 * (t + 1), 4.0 * R * (t + 1) * (double)d,
                    [&] { return nt::self_attn(m.dt, sa, s); }));
 
       e = nt::GemmEpi{};

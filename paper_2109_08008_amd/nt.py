@@ -41,7 +41,7 @@ class nt_model_cfg(ctypes.Structure):
     _fields_ = [("d_model", c_int32), ("n_heads", c_int32), ("d_ffn", c_int32), ("n_enc", c_int32),
                 ("n_dec", c_int32), ("vocab", c_int32), ("max_positions", c_int32), ("pad_id", c_int32),
                 ("bos_id", c_int32), ("eos_id", c_int32), ("dtype", c_int32), ("dlcl_hist_norm", c_int32),
-                ("ln_eps", c_float), ("rel_pos_k", c_int32), ("fp8_weights", c_int32)]
+                ("ln_eps", c_float), ("rel_pos_k", c_int32), ("fp8_weights", c_int32), ("fp8_kv", c_int32)]
 
 
 class nt_search_cfg(ctypes.Structure):
@@ -135,11 +135,12 @@ def _stream(stream):
 def model_cfg(shape, dtype: str = "f16", hist_norm: bool = True, ln_eps: float = 1e-5,
               pad_id: int = 0, bos_id: int = 1, eos_id: int = 2) -> nt_model_cfg:
     """nt_model_cfg from any object with d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_positions
-    (and optionally rel_k).  dtype "f8" is fp16 activations with FP8 projection weights."""
-    f8 = dtype == "f8"
+    (and optionally rel_k).  dtype "f8" is the FP8 mode: fp16 activations, FP8 projection
+    weights and an FP8 self-attention key/value cache; "f8w" is FP8 weights alone."""
+    f8 = dtype in ("f8", "f8w")
     return nt_model_cfg(shape.d_model, shape.n_heads, shape.d_ffn, shape.n_enc, shape.n_dec, shape.vocab,
                         getattr(shape, "max_positions", 1024), pad_id, bos_id, eos_id, DTYPES["f16" if f8 else dtype],
-                        1 if hist_norm else 0, ln_eps, int(getattr(shape, "rel_k", 0)), int(f8))
+                        1 if hist_norm else 0, ln_eps, int(getattr(shape, "rel_k", 0)), int(f8), int(dtype == "f8"))
 
 
 def search_cfg(s) -> nt_search_cfg:

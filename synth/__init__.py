@@ -81,7 +81,8 @@ class Workload:
     model: ModelShape
     data: DataSetup
     search: SearchSetup
-    dtype: str                # "f32" | "f16" | "bf16" | "f8" (fp16 activations, FP8 E4M3 weights)
+    dtype: str                # "f32" | "f16" | "bf16" | "f8" (fp16 activations, FP8 E4M3 weights and
+                              # self-attention key/value cache) | "f8w" (FP8 weights alone)
     description: str = ""
     weights_seed: int = 0
     data_seed: int = 1
@@ -160,7 +161,8 @@ WORKLOADS = {
         DataSetup(2048, "lognormal", 25.0, 100, "zipf"),
         SearchSetup(beam=4, len_penalty=0.0, max_len_a=1.5, max_len_b=10, token_budget=8192),
         "f8",
-        "Base 6-6 with FP8 E4M3 projection weights (column scales) and fp16 activations; otherwise base-6-6",
+        "Base 6-6 with FP8 E4M3 projection weights (column scales), an FP8 E4M3 self-attention key/value "
+        "cache and fp16 activations; otherwise base-6-6",
     ),
     "wide-30-6-fp8": Workload(
         "wide-30-6-fp8",
@@ -168,7 +170,8 @@ WORKLOADS = {
         DataSetup(4096, "lognormal", 30.0, 200, "zipf"),
         SearchSetup(beam=4, len_penalty=0.0, max_len_a=1.5, max_len_b=10, token_budget=16384),
         "f8",
-        "Wide 30-6 with FP8 E4M3 projection weights (column scales) and fp16 activations; otherwise wide-30-6",
+        "Wide 30-6 with FP8 E4M3 projection weights (column scales), an FP8 E4M3 self-attention key/value "
+        "cache and fp16 activations; otherwise wide-30-6",
     ),
     "wide-30-6": Workload(
         "wide-30-6",

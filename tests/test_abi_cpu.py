@@ -153,6 +153,20 @@ def test_fp8_weight_configs(nt):
     with pytest.raises(nt.NTError) as e:
         nt.nt_weights_size(cfg)
     assert e.value.status == nt.NT_E_INVALID
+    for dt in ("f32", "bf16"):
+        cfg = nt.model_cfg(shape, dt)
+        cfg.fp8_kv = 1
+        with pytest.raises(nt.NTError) as e:
+            nt.nt_weights_size(cfg)
+        assert e.value.status == nt.NT_E_UNSUPPORTED
+    cfg = nt.model_cfg(shape, "f16")
+    cfg.fp8_kv = -1
+    with pytest.raises(nt.NTError) as e:
+        nt.nt_weights_size(cfg)
+    assert e.value.status == nt.NT_E_INVALID
+    assert (nt.model_cfg(shape, "f8").fp8_kv, nt.model_cfg(shape, "f8w").fp8_kv) == (1, 0)
+    assert nt.model_cfg(shape, "f8w").fp8_weights == 1
+    assert nt.nt_weights_size(nt.model_cfg(shape, "f8w")) == nt.nt_weights_size(nt.model_cfg(shape, "f8"))
     hf8, db8 = nt.nt_weights_size(nt.model_cfg(shape, "f8"))
     hf16, db16 = nt.nt_weights_size(nt.model_cfg(shape, "f16"))
     mats = sum(e.size for e in synth.weight_layout(shape) if ".W_" in e.name)

@@ -8,8 +8,10 @@ and 1024, 35- and 30-layer encoders), against the fp64 oracle spread over host p
   output respects the length limit, never contains EOS (generation is not masked
   otherwise), and the score is finite.  On a length-stratified sample of 64 sentences
   the oracle (fp64 on the GPU's rounded weights) is teacher-forced on the GPU's output:
-  every per-token log-prob must agree within the fp16 bound (1e-2), and the reported
-  score must be the length-normalised sum of those log-probs within 1e-2 per token.
+  every per-token log-prob must agree within the fp16 bound (1e-2; 2e-2 for the FP8
+  workloads, whose key/value cache the two sides can round one E4M3 step apart where a
+  value lies next to a rounding midpoint), and the reported score must be the
+  length-normalised sum of those log-probs within 1e-2 per token.
 * fp32 at full shape (test_fp32_full_shape): each of the five configurations -- Tiny's
   full set, and a 64-sentence length-stratified subset of the others -- with the test
   weights ("lively": source-dependent tokens and varied finishing) and the workload's
@@ -108,7 +110,7 @@ def test_full_workload_sampled_against_oracle(name):
     worst_score = max(r[1] / max(1, r[2] + 1) for r in res)
     print(f"{name}: {len(srcs)} sentences; {len(sample)} sampled: per-token log-prob max abs err {worst:.3g}, "
           f"score err per token {worst_score:.3g}")
-    assert worst <= 1e-2
+    assert worst <= (2e-2 if w.dtype == "f8" else 1e-2)
     assert worst_score <= 1e-2
 
 

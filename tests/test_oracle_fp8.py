@@ -192,3 +192,6 @@ def test_fp8_kv_cache_matches_torch_float8_decoder(torch_cpu64):
     plain = oracle.OracleModel(shape, blob, np.float64).teacher_forced_logits(src, tgt)
     assert np.abs(plain - inc).max() > 1e-3
     assert oracle.OracleModel(shape, blob, np.float64, precision="f8").kv_fp8
+    weights_only = oracle.OracleModel(shape, blob, np.float64, precision="f8w")
+    assert not weights_only.kv_fp8
+    np.testing.assert_array_equal(oracle.round_weights(blob, shape, "f8w"), oracle.round_weights(blob, shape, "f8"))
