@@ -92,6 +92,8 @@ def parse_args():
     ap.add_argument("--workload", default="wide-30-6", choices=sorted(synth.WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graphs", action="store_true", help="launch decoder steps kernel by kernel")
+    ap.add_argument("--no-beam-fused", action="store_true",
+                    help="beam search stores the fp32 logits and scans them (the default keeps them out of HBM)")
     ap.add_argument("--streams", type=int, default=0, help="batches decoded concurrently (0: library default)")
     ap.add_argument("--samples", type=int, default=40,
                     help="timing samples (isolated units) in the timed region, at most 2 per timed step")
@@ -270,6 +272,7 @@ def main():
     blobs = synth.member_weights(w) if w.members else [synth.make_weights(w.model, seed=w.weights_seed)]
     ids, offs = synth.make_sentences(w.data, w.model.vocab, seed=w.data_seed)
     nt.nt_set_graphs(not args.no_graphs)
+    nt.nt_set_beam_fused(not args.no_beam_fused)
     if args.streams:
         nt.nt_set_streams(args.streams)
     if w.members:   # ensemble decoding: every member scores each step
@@ -357,7 +360,7 @@ def main():
             "source_tokens": int(offs[-1]), "target_tokens_per_step": n_tokens,
             "beam": w.search.beam, "token_budget": w.search.token_budget,
             "d_model": w.model.d_model, "n_enc": w.model.n_enc, "n_dec": w.model.n_dec, "vocab": w.model.vocab,
-            "decode_step_graphs": not args.no_graphs, "concurrent_batches": args.streams or 4,
+            "decode_step_graphs": not args.no_graphs, "beam_logits_in_hbm": bool(args.no_beam_fused), "concurrent_batches": args.streams or 4,
             "workspace_GB": round(ws_bytes / 1e9, 2),
         },
         "roofline": rl,

@@ -372,6 +372,17 @@ nt_status nt_op_select_tiled_noalloc(const float* d_logits, int32_t rows, int32_
  * with 0, every step is launched kernel by kernel). */
 nt_status nt_set_graphs(int32_t enable);
 
+/* Process-wide choice of the beam selection (default 1).  With 1 the output projection
+ * keeps only per-tile records (max, sum of exp, best entry) of each row's 128-column
+ * tiles; the 2K tiles whose best entries rank first hold the row's 2K largest logits, and
+ * only their logits are formed again, bitwise equal, for the selection -- the R x V
+ * logits never reach device memory (Sec. 4.4 drops log_softmax, Sec. 6 names kernel
+ * fusion as the way on).  With 0 the projection stores the fp32 logits and the selection
+ * scans every row.  Both give bitwise identical results.  It takes effect for workspaces
+ * sized and states encoded after the call (the two need different buffers), so set it
+ * before nt_workspace_size. */
+nt_status nt_set_beam_fused(int32_t enable);
+
 /* Process-wide number of batches nt_translate decodes concurrently, 1..8 (default 4: on
  * MI355X with HIP's default of four hardware queues per process, 4 measured best with
  * graph replay; 3 without it). */

@@ -123,7 +123,8 @@ __device__ __forceinline__ void epilogue4(const GemmEpi& e, int m, int n, int N,
   const bool vec = cnt == 4 && (e.ldc & 3) == 0;
   if constexpr (MODE == EPI_STORE) {
     if (e.out_f32) {
-      float* o = static_cast<float*>(e.out) + (size_t)m * e.ldc + n;
+      const int mo = e.out_map ? e.sent_list[m / e.beam] * e.beam + m % e.beam : m;
+      float* o = static_cast<float*>(e.out) + (size_t)mo * e.ldc + n;
       if (vec) {
         *reinterpret_cast<float4*>(o) = make_float4(v[0], v[1], v[2], v[3]);
       } else {
@@ -304,8 +305,8 @@ template <> struct LdsWait<4, 4> {
 // row stride CS) are reduced to one record per row: the max, the sum of exp(x - max),
 // and for K2 = 1 the best (value, column) -- the max at its lowest column.  TPR
 // consecutive lanes share a row; each scans its columns in increasing order.  Two
-// passes: the max (and its column), then one exponential per logit.  K2 = 0 serves beam
-// search, which reads its candidates back from the stored logits; K2 = 1 serves greedy.
+// passes: the max (and its column), then one exponential per logit.  Both searches take
+// K2 = 1: greedy needs nothing else, beam ranks the tiles by their best entries.
 __device__ __forceinline__ bool topk_better(float v1, int i1, float v2, int i2) {
   return v1 > v2 || (v1 == v2 && i1 < i2);
 }
@@ -399,19 +400,29 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
     tiles_m = (M + BM_ - 1) / BM_;
   }
   // --- tile assignment: XCD-contiguous, then grouped by 8 tile-rows ---
-  const int ntiles = tiles_m * tiles_n;
+  // (role 3: block pid of the pair list; its rows are pairs of one 128-column tile)
+  const int ntiles = ROLE == 3 ? *epi.gnblk : tiles_m * tiles_n;
   int pid = blockIdx.x;
   if (pid >= ntiles) return;
   {
     const int q = ntiles / 8, r = ntiles % 8, xcd = pid % 8, idx = pid / 8;
     pid = xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
   }
-  constexpr int GROUP = 8;
-  const int per_group = GROUP * tiles_n;
-  const int first_m = (pid / per_group) * GROUP;
-  const int gsize = min(tiles_m - first_m, GROUP);
-  const int tm = first_m + (pid % per_group) % gsize;
-  const int tn = (pid % per_group) / gsize;
+  const int* prow = nullptr;   // role 3: the block's pair ids
+  int tm = 0, tn = 0;
+  if constexpr (ROLE == 3) {
+    static_assert(BN_ == 128, "a pair block covers one 128-column tile");
+    tn = epi.gblk[3 * pid];
+    prow = epi.sorted + epi.gblk[3 * pid + 1];
+    M = epi.gblk[3 * pid + 2];
+  } else {
+    constexpr int GROUP = 8;
+    const int per_group = GROUP * tiles_n;
+    const int first_m = (pid / per_group) * GROUP;
+    const int gsize = min(tiles_m - first_m, GROUP);
+    tm = first_m + (pid % per_group) % gsize;
+    tn = (pid % per_group) / gsize;
+  }
   const int m0 = tm * BM_, n0 = tn * BN_;
   const int t_slot = epi.ctl ? epi.ctl[CTL_T] : epi.t;
 
@@ -428,6 +439,20 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   const int brow8 = lane >> 2, bchunk8 = (lane & 3) ^ (lane >> 4);
   const char* Ab = reinterpret_cast<const char*>(A) + lchunk * 16;
   const char* Bb = reinterpret_cast<const char*>(Bt) + (F8 ? bchunk8 : lchunk) * 16;
+  // byte offset of A row `row_` of the tile (load i_ of this wave): role 3 gathers the
+  // rows of its pairs, read once here
+  size_t aoff3[ROLE == 3 ? LPW : 1];
+  if constexpr (ROLE == 3) {
+#pragma unroll
+    for (int i_ = 0; i_ < LPW; ++i_) {
+      const int g_ = wave * LPW + i_;
+      aoff3[i_] = g_ < GROUPS_A ? (size_t)(prow[min(g_ * 8 + lrow, M - 1)] / epi.pair_k) * lda_b : 0;
+    }
+  }
+  auto a_off = [&](int i_, int row_) -> size_t {
+    if constexpr (ROLE == 3) return aoff3[i_];
+    else return (size_t)min(m0 + row_, M - 1) * lda_b;
+  };
 #define NT_ISSUE(kt, SL)                                                                          \
   {                                                                                               \
     unsigned char* sb_ = lds + (SL) * STAGE_BYTES;                                                \
@@ -438,7 +463,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       if (!F8 || g_ < GROUPS_A) {                                                                 \
         const int row_ = g_ * 8 + lrow;                                                           \
         const size_t kb_ = (size_t)(kt) * ROWB;                                                   \
-        src_ = row_ < BM_ ? Ab + (size_t)min(m0 + row_, M - 1) * lda_b + kb_                      \
+        src_ = row_ < BM_ ? Ab + a_off(i_, row_) + kb_                                            \
                           : Bb + (size_t)min(n0 + row_ - BM_, N - 1) * ldb_b + kb_;               \
         dst_ = sb_ + g_ * 1024;                                                                   \
       } else {                                                                                    \
@@ -474,7 +499,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   // vector-aligned reads the (16-byte aligned) base of A instead and is left to the
   // epilogue's own loads.  The epilogue adds them in its own order (bias, then residual),
   // so results are bitwise unchanged.
-  constexpr bool PRE = ROLE != 2 && EPG % NTHR == 0 && PASSES * (EPG / NTHR) <= 4;
+  constexpr bool PRE = ROLE < 2 && EPG % NTHR == 0 && PASSES * (EPG / NTHR) <= 4;
   constexpr int NPRE = PRE ? PASSES * (EPG / NTHR) : 1;
   using R4 = typename Raw4<T>::type;
   float4 pre_b[NPRE];
@@ -614,7 +639,7 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
   // residual), one round trip per group.  Groups are disjoint between threads, and each
   // residual element is read by the thread that overwrites it, so reading them all first
   // is the same computation.
-  constexpr bool BATCH = !PRE && EPG % NTHR == 0 && ROLE != 2;   // the projection has no operands to fetch
+  constexpr bool BATCH = !PRE && EPG % NTHR == 0 && ROLE < 2;   // the projection has no operands to fetch
   constexpr int GPT = BATCH ? EPG / NTHR : 1;
 #pragma unroll
   for (int pass = 0; pass < PASSES; ++pass) {
@@ -653,12 +678,24 @@ __global__ __launch_bounds__(NTHR) void gemm_kernel(const T* __restrict__ A, int
       }
     }
     __syncthreads();
-    if (ROLE == 2 && epi.mode == EPI_TOPK) {
-      if (!epi.out) {   // greedy: the records are all its selection needs
-        topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
-        continue;
+    if constexpr (ROLE == 3) {   // the pairs' logits, row = pair id
+      for (int g = tid; g < EPG; g += NTHR) {
+        const int row = g / (BN_ / 4), c4 = g % (BN_ / 4);
+        if (pass * ER + row < M) {
+          float4 v = *reinterpret_cast<const float4*>(&cs[row * CS + c4 * 4]);
+          const int n = n0 + c4 * 4;
+          if (n + 0 >= N) v.x = -INFINITY;
+          if (n + 1 >= N) v.y = -INFINITY;
+          if (n + 2 >= N) v.z = -INFINITY;
+          if (n + 3 >= N) v.w = -INFINITY;
+          *reinterpret_cast<float4*>(static_cast<float*>(epi.out) + (size_t)prow[pass * ER + row] * BN_ + c4 * 4) = v;
+        }
       }
-      topk_tile_rows<ER, BN_, 0>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);   // beam also stores the logits
+      continue;
+    }
+    if (ROLE == 2 && epi.mode == EPI_TOPK) {
+      topk_tile_rows<ER, BN_, 1>(cs, CS, m0 + pass * ER, n0, M, N, tn, epi);
+      if (!epi.out) continue;   // the records are all the selection needs; else the logits too
     }
     // The mode is the same for every thread: one branch per pass, then that mode's groups.
     auto finish_pass = [&](auto mode_c) {
@@ -796,7 +833,29 @@ hipError_t launch_role(const void* A, int lda, const void* Bt, int M, int N, int
   }
 }
 
+template <typename T>
+hipError_t launch_pairs(const void* A, int lda, const void* Bt, int N, int K, const GemmEpi& epi, int max_blocks,
+                        hipStream_t s) {
+  NT_LAUNCH((gemm_kernel<T, PAIR_BM, 128, 2, 3>), dim3(max_blocks), dim3(NTHR), 0, s, static_cast<const T*>(A), lda,
+            Bt, PAIR_BM, N, K, epi, 1, 1);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t gemm_pairs(DT dt, const void* A, int lda, const void* Bt, int N, int K, const GemmEpi& epi,
+                      int max_blocks, hipStream_t s) {
+  if (max_blocks <= 0) return hipSuccess;
+  if (!epi.gblk || !epi.gnblk || !epi.sorted || !epi.out || epi.wscale || epi.lnf_colsum || epi.pair_k < 1)
+    return hipErrorInvalidValue;
+  if (((reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(Bt)) & 15) != 0) return hipErrorInvalidValue;
+  switch (dt) {
+    case DT::F32: return launch_pairs<float>(A, lda, Bt, N, K, epi, max_blocks, s);
+    case DT::F16: return launch_pairs<f16>(A, lda, Bt, N, K, epi, max_blocks, s);
+    case DT::BF16: return launch_pairs<bf16>(A, lda, Bt, N, K, epi, max_blocks, s);
+  }
+  return hipErrorInvalidValue;
+}
 
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                 hipStream_t s, int role, int tile) {

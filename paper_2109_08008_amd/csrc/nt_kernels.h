@@ -57,8 +57,8 @@ enum EpiMode : int {
   EPI_SELF_QKV = 3,   // decoder: cols [0,d) -> q out; [d,3d) -> K/V cache slot t of phys row
   EPI_CROSS_KV = 4,   // encoder: cols of [Ld][K|V][d] -> cross cache [Ld][2][B][H][S][dh]
   EPI_TOPK = 5,       // output projection: per row and 128-column tile, the (max, sum exp,
-                      // largest (value, index)) partials -- instead of the logits (greedy),
-                      // or with out set, as well as the fp32 logits (beam)
+                      // largest (value, index)) partials -- instead of the logits, or with
+                      // out set, as well as the fp32 logits
 };
 __host__ __device__ inline int topk_record(int k2) { return 2 + 2 * k2; }   // floats per partial record
 
@@ -71,6 +71,7 @@ struct GemmEpi {
   void* out = nullptr;           // [M][ldc]
   int ldc = 0;
   int out_f32 = 0;               // 1: out is fp32 (logits); else the model dtype
+  int out_map = 0;               // fp32 out: row m goes to row sent_list[m / beam] * beam + m % beam
   // EPI_SELF_QKV
   const int* sent_list = nullptr;  // logical sentence -> batch sentence
   int beam = 1;
@@ -96,17 +97,33 @@ struct GemmEpi {
   float lnf_eps = 0.f;
   // EPI_TOPK (the launch uses 128x128 tiles, so n_tiles = ceil(N / 128))
   float* part = nullptr;           // [M][n_tiles][topk_record(k2)]
-  int k2 = 1;                      // record layout: 1 (max, sum, best value, best column); the
-                                   //   projection fills the best entry for greedy only
+  int k2 = 1;                      // record layout: 1 (max, sum, best value, best column)
   int n_tiles = 0;
+  // Candidate-tile recompute (gemm_pairs): workgroup b takes block gblk[b] = {tile, first,
+  // count} (b < *gnblk): the pairs sorted[first + i], i < count, all of that 128-column
+  // tile, pair p belonging to row p / pair_k.
+  const int* gblk = nullptr;
+  const int* gnblk = nullptr;
+  const int* sorted = nullptr;
+  int pair_k = 1;
 };
 
 // role: 0 encoder, 1 decoder step, 2 output projection.  Only the kernel's symbol name
-// depends on it, so profiles separate the three uses.
+// depends on it, so profiles separate the three uses.  (Role 3 is gemm_pairs below.)
 // tile: 0 = chosen by shape, 1 = 64x32, 2 = 128x128, 3 = 128x64, 4 = 64x128 (never changes
 // a result).
 hipError_t gemm(DT dt, const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi,
                 hipStream_t s, int role = 0, int tile = 0);
+
+// The output projection's logits of chosen (row, 128-column tile) pairs, recomputed: for
+// every block of epi.gblk, the rows of its pairs times the tile's columns of Bt (N = V
+// columns in all, K = the row width), written as fp32 to out[pair][128] (columns past N
+// get -inf).  The product runs through the same kernel and k-order as gemm(), so each
+// value is bitwise the one the projection's EPI_TOPK records were formed from.  The
+// grid covers max_blocks blocks; those past *epi.gnblk return.
+constexpr int PAIR_BM = 64;      // pair rows per block
+hipError_t gemm_pairs(DT dt, const void* A, int lda, const void* Bt, int N, int K, const GemmEpi& epi,
+                      int max_blocks, hipStream_t s);
 
 // ---------------------------------------------------------------------------------
 // Normalisation / embedding kernels (one wave per row of d = 64*EPL elements).
@@ -266,6 +283,23 @@ hipError_t beam_update(const float* topv, const int* topi, const float* lse, con
 // results as beam_select (the log-sum-exp merged from the records).
 hipError_t beam_select_tiles(const float* part, int n_tiles, const float* logits, const int* ctl, int beam, int rows,
                              int V, int k2, float* topv, int* topi, float* lse, hipStream_t s);
+// Beam selection with the logits never stored (three launches around gemm_pairs).
+// beam_pick_tiles: per live row, the log-sum-exp merged from its records (lse) and the k2
+//   tiles whose best entries rank first under (value desc, column asc); every one of the
+//   row's k2 largest logits lies in them.  Pair p = r * k2 + j names the row's j-th tile,
+//   ptile[p] (-1 past the row's tiles).  tau[r] is the k2-th best tile maximum, a lower
+//   bound of the row's k2-th largest logit.
+// pair_bucket (one workgroup, n_tiles <= 512): sorts the live pairs by tile into sorted[]
+//   (R * k2 entries) and cuts each tile's run into blocks of at most PAIR_BM pairs,
+//   gblk[b] = {tile, first position in sorted, count}, *gnblk = their number.
+// beam_select_pairs: per live row, its k2 largest logits (value desc, index asc) from the
+//   recomputed tiles logp[p][128] -- the same result as beam_select over the whole row.
+hipError_t beam_pick_tiles(const float* part, int n_tiles, const int* ctl, int beam, int rows, int k2, int* ptile,
+                           float* tau, float* lse, hipStream_t s);
+hipError_t pair_bucket(const int* ptile, const int* ctl, int beam, int rows, int k2, int n_tiles, int* sorted,
+                       int* gblk, int* gnblk, hipStream_t s);
+hipError_t beam_select_pairs(const float* logp, const int* ptile, const float* tau, const int* ctl, int beam,
+                             int rows, int V, int k2, float* topv, int* topi, hipStream_t s);
 // Per-tile records of a logits matrix in the projection epilogue's layout (for tests).
 hipError_t tile_records(const float* logits, int rows, int V, float* part, hipStream_t s);
 // The current device's copy of the library's static records array (room for

@@ -96,6 +96,7 @@ enum ProfMode { PROF_STRIDE = 0, PROF_NONE = 1, PROF_ALL = 2 };
 thread_local int g_prof_mode = PROF_STRIDE;
 int64_t g_prof_enc_units = 0, g_prof_step_units = 0;   // nt_translate units seen while profiling
 std::atomic<bool> g_use_graphs{true};   // nt_translate replays a captured decode step
+std::atomic<bool> g_beam_fused{true};   // beam selection without stored logits (nt_set_beam_fused)
 std::atomic<int> g_streams{4};          // batches nt_translate decodes concurrently
 
 struct ProfModeScope {
@@ -436,13 +437,21 @@ struct WsPlan {
   size_t hist, x, u, qkv, att, a, f, y, dlcl_part;
   // decoder buffers (comb: an ensemble's combined scores)
   size_t z, du, dq, datt, df, logits, comb, topv, topi, lse;
-  size_t tparts;   // beam: the projection's per-tile records, beside the logits
+  size_t tparts;   // beam: the projection's per-tile records
+  // beam without stored logits: each pair's tile, the pairs sorted by tile, the rows'
+  // thresholds, the recomputed tiles and the blocks of the recompute
+  bool beam_pairs = false;
+  int pair_blocks = 0;
+  size_t gptile, gsorted, gtau, glog, gblk, gnblk;
 };
 
 WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   WsPlan p;
   const int M = n_members(m);
   const size_t T = (size_t)B * S, R = (size_t)B * K, eb = m.eb;
+  const size_t n_tiles = (m.V + 127) / 128, k2 = 2 * (size_t)K;
+  p.beam_pairs = K > 1 && M == 1 && g_beam_fused.load();
+  p.pair_blocks = p.beam_pairs ? (int)((R * k2 + nt::PAIR_BM - 1) / nt::PAIR_BM + n_tiles) : 0;
   size_t d = 0, F = 0, hist = 0, dlcl_part = 0;
   for (int i = 0; i < M; ++i) {
     const nt_model& mi = member(m, i);
@@ -507,13 +516,21 @@ WsPlan ws_plan(const nt_model& m, int B, int S, int K, int Tcap) {
   p.dq = take(R * d * eb);
   p.datt = take(R * d * eb);
   p.df = take(R * F * eb);
-  // fp32 logits, or (fused selection) the per-tile partial records, whichever is larger
-  p.logits = take(std::max(R * m.V * 4, R * (size_t)((m.V + 127) / 128) * nt::topk_record(1) * 4));
+  // fp32 logits, or (fused greedy selection) the per-tile partial records, whichever is
+  // larger; beam without stored logits needs neither
+  const size_t recs = R * n_tiles * nt::topk_record(1) * 4;
+  p.logits = take(p.beam_pairs ? 0 : std::max(R * m.V * 4, recs));
   p.comb = M > 1 ? take(R * m.V * 4) : 0;
   p.topv = take(R * 2 * K * 4);
   p.topi = take(R * 2 * K * 4);
   p.lse = take(R * 4);
-  p.tparts = take(K > 1 ? R * (size_t)((m.V + 127) / 128) * nt::topk_record(1) * 4 : 0);
+  p.tparts = take(K > 1 ? recs : 0);
+  p.gptile = take(p.beam_pairs ? R * k2 * 4 : 0);
+  p.gsorted = take(p.beam_pairs ? R * k2 * 4 : 0);
+  p.gtau = take(p.beam_pairs ? R * 4 : 0);
+  p.glog = take(p.beam_pairs ? R * k2 * 128 * 4 : 0);
+  p.gblk = take((size_t)p.pair_blocks * 3 * 4);
+  p.gnblk = take(p.beam_pairs ? 4 : 0);
   p.total = std::max(enc_end, off);
   return p;
 }
@@ -914,12 +931,12 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
     }
 
     // Tied output projection.  Its epilogue reduces each row to per-tile (max, sum exp,
-    // best) records: greedy needs nothing else, so its logits never reach HBM; beam also
-    // stores the logits and reads back only the tiles that can hold a row's 2K largest.
-    // Teacher forcing and the logits copy-out use the plain path that writes fp32 logits.
-    // (measured: a top-8 per tile row in the epilogue costs more than the (max, sum)
-    // records and the targeted re-read.)  An ensemble member writes its logits and folds
-    // them into the combined scores.
+    // best) records.  Greedy needs nothing else, so its logits never reach HBM.  Beam
+    // ranks each row's tiles by their best entries, forms the logits of the first 2K
+    // tiles again (the same kernel and k-order, so the same bits), and selects from
+    // those: its logits never reach HBM either.  Teacher forcing, greedy copy-out and
+    // the plain beam path (nt_set_beam_fused(0)) store the fp32 logits and scan them.
+    // An ensemble member writes its logits and folds them into the combined scores.
     if (M > 1) {
       nt::GemmEpi e{};
       e.mode = nt::EPI_STORE;
@@ -930,7 +947,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       NT_HIP(timed(NT_K_SELECT, s, (double)R * m.V * 4 * (mi == 0 ? 2 : 3), 5.0 * R * m.V, [&] {
         return nt::ens_combine(st->at<float>(p.logits), st->at<float>(p.comb), ctl, K, Rp, m.V, mi, M, top.rule, s);
       }));
-    } else if (!d_logits && !d_forced && K == 1) {
+    } else if (K == 1 && !d_logits && !d_forced) {
       const int n_tiles = (m.V + 127) / 128;
       nt::GemmEpi e{};
       e.mode = nt::EPI_TOPK;
@@ -941,7 +958,7 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
       const float* part = st->at<float>(p.logits);
       const double pbytes = (double)R * n_tiles * nt::topk_record(1) * 4;
       NT_HIP(timed(NT_K_SELECT, s, pbytes, 0.0, [&] { return nt::greedy_step_fused(part, n_tiles, ss, s); }));
-    } else if (d_logits || d_forced) {   // teacher forcing, or the caller wants the logits
+    } else if (!p.beam_pairs) {   // stored logits: teacher forcing, greedy copy-out, plain beam
       nt::GemmEpi e{};
       e.mode = nt::EPI_STORE;
       e.out = at(p.logits);
@@ -962,22 +979,45 @@ nt_status enqueue_step(nt_dec_state* st, const int32_t* d_forced, float* d_logit
         }));
       }
     } else {
-      // Beam: the projection also leaves per-tile (max, sum exp) records, so the selection
-      // reads them and only the few tiles that can hold a row's 2K largest logits.
-      const int n_tiles = (m.V + 127) / 128;
+      // Beam without stored logits: records (and, when the caller asks, the logits copied
+      // straight to its buffer), the 2K tiles of every row, their blocks, the tiles'
+      // logits formed again, the row's 2K largest from them, the update.
+      const int n_tiles = (m.V + 127) / 128, k2 = 2 * K;
       nt::GemmEpi e{};
       e.mode = nt::EPI_TOPK;
       e.part = st->at<float>(p.tparts);
       e.k2 = 1;
       e.n_tiles = n_tiles;
-      e.out = at(p.logits);
-      e.ldc = m.V;
-      e.out_f32 = 1;
+      if (d_logits) {
+        e.out = d_logits;
+        e.ldc = m.V;
+        e.out_f32 = 1;
+        e.out_map = 1;
+        e.sent_list = list;
+        e.beam = K;
+      }
       NT_HIP(gemm_dec(NT_K_GEMM_VOCAB, at(p.du), d, m.E, m.V, d, e));
-      const double sbytes = (double)R * (n_tiles * nt::topk_record(1) * 4.0 + 2.0 * K * 128 * 4);
-      NT_HIP(timed(NT_K_SELECT, s, sbytes, 0.0, [&] {
-        return nt::beam_select_tiles(st->at<float>(p.tparts), n_tiles, st->at<float>(p.logits), ctl, K, Rp, m.V,
-                                     2 * K, st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), s);
+      const double rec_bytes = (double)R * n_tiles * nt::topk_record(1) * 4;
+      const double pair_bytes = (double)R * k2 * 128 * 4;   // the recomputed tiles' logits
+      NT_HIP(timed(NT_K_SELECT, s, rec_bytes, 0.0, [&] {
+        return nt::beam_pick_tiles(st->at<float>(p.tparts), n_tiles, ctl, K, Rp, k2, st->at<int>(p.gptile),
+                                   st->at<float>(p.gtau), st->at<float>(p.lse), s);
+      }));
+      NT_HIP(timed(NT_K_SELECT, s, (double)R * k2 * 4 * 3, 0.0, [&] {
+        return nt::pair_bucket(st->at<int>(p.gptile), ctl, K, Rp, k2, n_tiles, st->at<int>(p.gsorted),
+                               st->at<int>(p.gblk), st->at<int>(p.gnblk), s);
+      }));
+      nt::GemmEpi g{};
+      g.gblk = st->at<int>(p.gblk);
+      g.gnblk = st->at<int>(p.gnblk);
+      g.sorted = st->at<int>(p.gsorted);
+      g.pair_k = k2;
+      g.out = st->at<float>(p.glog);
+      NT_HIP(timed(NT_K_GEMM_VOCAB, s, pair_bytes, 2.0 * R * k2 * 128 * d,
+                   [&] { return nt::gemm_pairs(m.dt, at(p.du), d, m.E, m.V, d, g, p.pair_blocks, s); }));
+      NT_HIP(timed(NT_K_SELECT, s, pair_bytes, 0.0, [&] {
+        return nt::beam_select_pairs(st->at<float>(p.glog), st->at<int>(p.gptile), st->at<float>(p.gtau), ctl, K,
+                                     Rp, m.V, k2, st->at<float>(p.topv), st->at<int>(p.topi), s);
       }));
       NT_HIP(timed(NT_K_SEARCH, s, (double)R * 2 * K * 8 + (double)R * t * 8, 0.0, [&] {
         return nt::beam_update(st->at<float>(p.topv), st->at<int>(p.topi), st->at<float>(p.lse), ss, s);
@@ -1925,6 +1965,12 @@ nt_status nt_prof_units(int64_t* encodes, int64_t* steps) {
 nt_status nt_set_graphs(int32_t enable) {
   g_err.clear();
   g_use_graphs = enable != 0;
+  return NT_OK;
+}
+
+nt_status nt_set_beam_fused(int32_t enable) {
+  g_err.clear();
+  g_beam_fused = enable != 0;
   return NT_OK;
 }
 

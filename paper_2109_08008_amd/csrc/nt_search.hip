@@ -655,6 +655,182 @@ __global__ __launch_bounds__(256) void beam_select_tiles_kernel(const float* __r
   if (lane == 0) lse_out[r] = acc.m + logf(acc.s);
 }
 
+// Beam selection without stored logits.  The projection leaves only the per-tile records
+// (max, sum of exp(x - max), best value, best column).  Order a row's tiles by their best
+// entries under (value desc, column asc) and take the first k2: the j-th largest logit x
+// of the row (same order) lies in some tile T, and every tile ranked before T has a best
+// entry ranked before T's, which is at or before x -- j - 1 entries at most -- so T is
+// among the first k2.  Only those tiles' logits are formed again (gemm_pairs, bitwise the
+// projection's values), and the row's k2 largest come from them.
+template <int TPL>
+__global__ __launch_bounds__(256) void beam_pick_tiles_kernel(const float* __restrict__ part, int n_tiles,
+                                                              const int* __restrict__ ctl, int beam, int rows,
+                                                              int k2, int* __restrict__ ptile,
+                                                              float* __restrict__ tau_out,
+                                                              float* __restrict__ lse_out) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  asm volatile("" ::"s"(part), "s"(n_tiles), "s"(ctl), "s"(beam), "s"(rows), "s"(k2));
+  const int r = blockIdx.x * 4 + wave;
+  if (r >= rows) return;            // grid tail
+  const float* rec = part + (size_t)r * n_tiles * 4;
+  float4 rq[TPL];
+#pragma unroll
+  for (int j = 0; j < TPL; ++j)
+    rq[j] = *reinterpret_cast<const float4*>(rec + (size_t)min(lane + j * kWave, n_tiles - 1) * 4);
+  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
+#pragma unroll
+  for (int j = 0; j < TPL; ++j) asm volatile("" ::"v"(rq[j].x), "v"(rq[j].y), "v"(rq[j].z), "v"(rq[j].w));
+  asm volatile("" ::"s"(live));
+  if (r >= live) return;            // whole wave; no block barrier below
+  float tv[TPL];                    // the lane's tiles' best entries; taken ones become empty
+  int tc[TPL];
+  MaxSum acc{-INFINITY, 0.f};
+#pragma unroll
+  for (int j = 0; j < TPL; ++j) {
+    const bool ok = lane + j * kWave < n_tiles;
+    tv[j] = ok ? rq[j].z : -INFINITY;
+    tc[j] = ok ? __float_as_int(rq[j].w) : INT_MAX;
+    if (ok) acc = ms_merge(acc, MaxSum{rq[j].x, rq[j].y});
+  }
+  acc = wave_ms(acc);
+  float tau = -INFINITY;
+  int mine = -1;                    // lane j2 keeps the row's j2-th tile
+  for (int j2 = 0; j2 < k2; ++j2) {
+    float bv = -INFINITY;
+    int bc = INT_MAX;
+#pragma unroll
+    for (int j = 0; j < TPL; ++j)
+      if (takes(tv[j], tc[j], bv, bc)) { bv = tv[j]; bc = tc[j]; }
+    wave_best(bv, bc);
+    const int tile = bc == INT_MAX ? -1 : bc / TILE_COLS;
+    tau = bv;                       // -inf once the row has fewer than k2 tiles
+    if (lane == j2) mine = tile;
+    if (tile >= 0 && lane == (tile & (kWave - 1))) {   // the owner gives the tile up
+#pragma unroll
+      for (int j = 0; j < TPL; ++j)
+        if (j == tile / kWave) { tv[j] = -INFINITY; tc[j] = INT_MAX; }
+    }
+  }
+  if (lane < k2) ptile[(size_t)r * k2 + lane] = mine;
+  if (lane == 0) {
+    tau_out[r] = tau;
+    lse_out[r] = acc.m + logf(acc.s);
+  }
+}
+
+// Counting sort of the live rows' pairs by tile in one workgroup, in LDS: the counts, an
+// exclusive scan for each tile's first position, the blocks, then every pair written to
+// its tile's run of `sorted`.  Consecutive pairs belong to one row's distinct tiles, so
+// the lanes of one LDS atomic meet on an address only across rows (64 / k2 at most).
+// Global memory sees no atomics: device-wide atomics on one address serialise.
+constexpr int BUCKET_THREADS = 1024;
+__global__ __launch_bounds__(BUCKET_THREADS) void pair_bucket_kernel(const int* __restrict__ ptile,
+                                                                     const int* __restrict__ ctl, int beam,
+                                                                     int rows, int k2, int n_tiles,
+                                                                     int* __restrict__ sorted,
+                                                                     int* __restrict__ gblk,
+                                                                     int* __restrict__ gnblk) {
+  __shared__ int cnt[512], cur[512], nbs[512];
+  const int t = threadIdx.x;
+  if (t < 512) cnt[t] = 0;
+  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
+  const int np = live * k2;
+  __syncthreads();
+  for (int i = t; i < np; i += BUCKET_THREADS) {
+    const int tl = ptile[i];
+    if (tl >= 0) atomicAdd(&cnt[tl], 1);
+  }
+  __syncthreads();
+  // exclusive scans of the counts (positions) and of the blocks per tile
+  const int c = t < n_tiles ? cnt[t] : 0;
+  const int nb = (c + PAIR_BM - 1) / PAIR_BM;
+  if (t < 512) { cur[t] = c; nbs[t] = nb; }
+  __syncthreads();
+  for (int o = 1; o < 512; o <<= 1) {   // inclusive, Hillis-Steele
+    const int v1 = t < 512 && t >= o ? cur[t - o] : 0;
+    const int v2 = t < 512 && t >= o ? nbs[t - o] : 0;
+    __syncthreads();
+    if (t < 512) { cur[t] += v1; nbs[t] += v2; }
+    __syncthreads();
+  }
+  if (t < n_tiles) {
+    const int first = cur[t] - c, fb = nbs[t] - nb;
+    for (int b = 0; b < nb; ++b) {
+      int* g = gblk + 3 * (size_t)(fb + b);
+      g[0] = t;
+      g[1] = first + b * PAIR_BM;
+      g[2] = min(PAIR_BM, c - b * PAIR_BM);
+    }
+  }
+  if (t == 0) *gnblk = nbs[511];
+  __syncthreads();
+  if (t < n_tiles) cur[t] -= c;          // each tile's next free position
+  __syncthreads();
+  for (int i = t; i < np; i += BUCKET_THREADS) {
+    const int tl = ptile[i];
+    if (tl >= 0) sorted[atomicAdd(&cur[tl], 1)] = i;
+  }
+}
+
+// One wave per live row: the lanes scan the row's recomputed tiles (column h*64 + lane of
+// each, both halves), keep the logits at or above tau in sorted lists, and k2 rounds of a
+// wave argmax under (value desc, index asc) emit them in order.
+template <int K2>
+__global__ __launch_bounds__(256) void beam_select_pairs_kernel(const float* __restrict__ logp,
+                                                                const int* __restrict__ ptile,
+                                                                const float* __restrict__ tau_in,
+                                                                const int* __restrict__ ctl, int beam, int rows,
+                                                                int V, int k2, float* __restrict__ topv,
+                                                                int* __restrict__ topi) {
+  constexpr int CB = 8;             // tiles read per batch, every load issued before any use
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  asm volatile("" ::"s"(logp), "s"(ptile), "s"(tau_in), "s"(ctl), "s"(beam), "s"(rows), "s"(V), "s"(k2));
+  const int r = blockIdx.x * 4 + wave;
+  if (r >= rows) return;
+  const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
+  if (r >= live) return;
+  const float tau = tau_in[r];
+  float v[K2];
+  int ix[K2];
+#pragma unroll
+  for (int j = 0; j < K2; ++j) { v[j] = -INFINITY; ix[j] = INT_MAX; }
+  for (int c0 = 0; c0 < k2; c0 += CB) {
+    int tl[CB];
+    float xs[CB][2];
+#pragma unroll
+    for (int c = 0; c < CB; ++c) tl[c] = c0 + c < k2 ? ptile[(size_t)r * k2 + c0 + c] : -1;
+#pragma unroll
+    for (int c = 0; c < CB; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float* src = logp + ((size_t)r * k2 + (tl[c] >= 0 ? c0 + c : 0)) * TILE_COLS + h * kWave + lane;
+        xs[c][h] = *src;
+      }
+#pragma unroll
+    for (int c = 0; c < CB; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int n = tl[c] * TILE_COLS + h * kWave + lane;
+        if (tl[c] >= 0 && n < V && xs[c][h] >= tau) list_insert<K2>(v, ix, xs[c][h], n);
+      }
+  }
+  for (int round = 0; round < k2; ++round) {
+    float bv = v[0];
+    int bi = ix[0];
+    wave_best(bv, bi);
+    if (lane == 0) {
+      topv[(size_t)r * k2 + round] = bi == INT_MAX ? -INFINITY : bv;
+      topi[(size_t)r * k2 + round] = bi;
+    }
+    if (ix[0] == bi && bi != INT_MAX) {
+#pragma unroll
+      for (int q = 0; q < K2 - 1; ++q) { v[q] = v[q + 1]; ix[q] = ix[q + 1]; }
+      v[K2 - 1] = -INFINITY;
+      ix[K2 - 1] = INT_MAX;
+    }
+  }
+}
+
 // The per-tile records of a logits matrix, as the projection's epilogue forms them: one
 // wave per (row, tile), (max, sum of exp(x - max)) over the tile's columns.  For tests.
 __global__ __launch_bounds__(256) void tile_records_kernel(const float* __restrict__ logits, int rows, int V,
@@ -1025,6 +1201,43 @@ hipError_t beam_select_tiles(const float* part, int n_tiles, const float* logits
   const dim3 grid((rows + 3) / 4);
 #define NT_SEL(K2) \
   NT_LAUNCH(beam_select_tiles_kernel<K2>, grid, dim3(256), 0, s, part, n_tiles, logits, ctl, beam, rows, V, k2, topv, topi, lse)
+  if (k2 <= 4) NT_SEL(4);
+  else if (k2 <= 8) NT_SEL(8);
+  else if (k2 <= 16) NT_SEL(16);
+  else NT_SEL(32);
+#undef NT_SEL
+  return hipGetLastError();
+}
+
+hipError_t beam_pick_tiles(const float* part, int n_tiles, const int* ctl, int beam, int rows, int k2, int* ptile,
+                           float* tau, float* lse, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (n_tiles < 1 || n_tiles > SEL_TPL * kWave || k2 < 1 || k2 > 32) return hipErrorInvalidValue;
+  const dim3 grid((rows + 3) / 4);
+  if (n_tiles <= 4 * kWave)
+    NT_LAUNCH(beam_pick_tiles_kernel<4>, grid, dim3(256), 0, s, part, n_tiles, ctl, beam, rows, k2, ptile, tau, lse);
+  else
+    NT_LAUNCH(beam_pick_tiles_kernel<SEL_TPL>, grid, dim3(256), 0, s, part, n_tiles, ctl, beam, rows, k2, ptile, tau,
+              lse);
+  return hipGetLastError();
+}
+
+hipError_t pair_bucket(const int* ptile, const int* ctl, int beam, int rows, int k2, int n_tiles, int* sorted,
+                       int* gblk, int* gnblk, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (n_tiles < 1 || n_tiles > 512 || k2 < 1 || k2 > 32) return hipErrorInvalidValue;
+  NT_LAUNCH(pair_bucket_kernel, dim3(1), dim3(BUCKET_THREADS), 0, s, ptile, ctl, beam, rows, k2, n_tiles, sorted,
+            gblk, gnblk);
+  return hipGetLastError();
+}
+
+hipError_t beam_select_pairs(const float* logp, const int* ptile, const float* tau, const int* ctl, int beam,
+                             int rows, int V, int k2, float* topv, int* topi, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (k2 < 1 || k2 > 32) return hipErrorInvalidValue;
+  const dim3 grid((rows + 3) / 4);
+#define NT_SEL(K2) \
+  NT_LAUNCH(beam_select_pairs_kernel<K2>, grid, dim3(256), 0, s, logp, ptile, tau, ctl, beam, rows, V, k2, topv, topi)
   if (k2 <= 4) NT_SEL(4);
   else if (k2 <= 8) NT_SEL(8);
   else if (k2 <= 16) NT_SEL(16);

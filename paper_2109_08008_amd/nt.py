@@ -29,7 +29,7 @@ EXPORTS = [
     "nt_weights_size", "nt_load_weights", "nt_free_model", "nt_workspace_size", "nt_translate_workspace_size",
     "nt_encode", "nt_decode_step", "nt_dec_state_read", "nt_dec_state_info", "nt_dec_state_encoder_out",
     "nt_free_state", "nt_translate", "nt_last_error", "nt_prof_enable", "nt_prof_reset", "nt_prof_get",
-    "nt_op_gemm", "nt_op_gemm_ln", "nt_prof_config", "nt_set_graphs", "nt_set_streams", "nt_prof_units", "nt_op_select",
+    "nt_op_gemm", "nt_op_gemm_ln", "nt_prof_config", "nt_set_graphs", "nt_set_beam_fused", "nt_set_streams", "nt_prof_units", "nt_op_select",
     "nt_op_select_tiled", "nt_op_select_tiled_noalloc",
     "nt_ensemble", "nt_quantize_fp8",
 ]
@@ -96,6 +96,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "nt_prof_enable": (c_int32, [c_uint32]),
         "nt_prof_config": (c_int32, [c_uint32, c_int32]),
         "nt_set_graphs": (c_int32, [c_int32]),
+        "nt_set_beam_fused": (c_int32, [c_int32]),
         "nt_set_streams": (c_int32, [c_int32]),
         "nt_op_select": (c_int32, [P, c_int32, c_int32, c_int32, P, P, P, P]),
         "nt_op_select_tiled": (c_int32, [P, c_int32, c_int32, c_int32, P, P, P, P]),
@@ -313,6 +314,10 @@ def nt_prof_config(mask: int, stride: int):
 
 def nt_set_graphs(enable: bool):
     _check(load_library().nt_set_graphs(int(bool(enable))))
+
+
+def nt_set_beam_fused(enable: bool):
+    _check(load_library().nt_set_beam_fused(int(bool(enable))))
 
 
 def nt_set_streams(n: int):
