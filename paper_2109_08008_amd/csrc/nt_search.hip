@@ -719,11 +719,13 @@ __global__ __launch_bounds__(256) void beam_pick_tiles_kernel(const float* __res
 }
 
 // Counting sort of the live rows' pairs by tile in one workgroup, in LDS: the counts, an
-// exclusive scan for each tile's first position, the blocks, then every pair written to
-// its tile's run of `sorted`.  Consecutive pairs belong to one row's distinct tiles, so
-// the lanes of one LDS atomic meet on an address only across rows (64 / k2 at most).
-// Global memory sees no atomics: device-wide atomics on one address serialise.
-constexpr int BUCKET_THREADS = 1024;
+// exclusive scan for each tile's first position, the blocks, then every pair placed in
+// its tile's run.  Consecutive pairs belong to one row's distinct tiles, so the lanes of
+// one LDS atomic meet on an address only across rows (64 / k2 at most).  Up to
+// BUCKET_LDS pairs the runs are assembled in LDS and copied out in order (coalesced);
+// beyond, each pair is stored to its place directly.  Global memory sees no atomics:
+// device-wide atomics on one address serialise.
+constexpr int BUCKET_THREADS = 1024, BUCKET_BATCH = 8, BUCKET_LDS = 36864;
 __global__ __launch_bounds__(BUCKET_THREADS) void pair_bucket_kernel(const int* __restrict__ ptile,
                                                                      const int* __restrict__ ctl, int beam,
                                                                      int rows, int k2, int n_tiles,
@@ -731,14 +733,23 @@ __global__ __launch_bounds__(BUCKET_THREADS) void pair_bucket_kernel(const int* 
                                                                      int* __restrict__ gblk,
                                                                      int* __restrict__ gnblk) {
   __shared__ int cnt[512], cur[512], nbs[512];
+  __shared__ int runs[BUCKET_LDS];
   const int t = threadIdx.x;
   if (t < 512) cnt[t] = 0;
   const int live = ctl ? min(rows, ctl[CTL_NLIVE] * beam) : rows;
   const int np = live * k2;
   __syncthreads();
-  for (int i = t; i < np; i += BUCKET_THREADS) {
-    const int tl = ptile[i];
-    if (tl >= 0) atomicAdd(&cnt[tl], 1);
+  // each pass reads BUCKET_BATCH entries a thread before using any: one load round trip per batch
+  for (int i0 = t; i0 < np; i0 += BUCKET_THREADS * BUCKET_BATCH) {
+    int tl[BUCKET_BATCH];
+#pragma unroll
+    for (int b = 0; b < BUCKET_BATCH; ++b) {
+      const int i = i0 + b * BUCKET_THREADS;
+      tl[b] = i < np ? ptile[i] : -1;
+    }
+#pragma unroll
+    for (int b = 0; b < BUCKET_BATCH; ++b)
+      if (tl[b] >= 0) atomicAdd(&cnt[tl[b]], 1);
   }
   __syncthreads();
   // exclusive scans of the counts (positions) and of the blocks per tile
@@ -753,6 +764,7 @@ __global__ __launch_bounds__(BUCKET_THREADS) void pair_bucket_kernel(const int* 
     if (t < 512) { cur[t] += v1; nbs[t] += v2; }
     __syncthreads();
   }
+  const int total = cur[511];
   if (t < n_tiles) {
     const int first = cur[t] - c, fb = nbs[t] - nb;
     for (int b = 0; b < nb; ++b) {
@@ -766,9 +778,25 @@ __global__ __launch_bounds__(BUCKET_THREADS) void pair_bucket_kernel(const int* 
   __syncthreads();
   if (t < n_tiles) cur[t] -= c;          // each tile's next free position
   __syncthreads();
-  for (int i = t; i < np; i += BUCKET_THREADS) {
-    const int tl = ptile[i];
-    if (tl >= 0) sorted[atomicAdd(&cur[tl], 1)] = i;
+  const bool in_lds = total <= BUCKET_LDS;   // the same in every thread
+  for (int i0 = t; i0 < np; i0 += BUCKET_THREADS * BUCKET_BATCH) {
+    int tl[BUCKET_BATCH];
+#pragma unroll
+    for (int b = 0; b < BUCKET_BATCH; ++b) {
+      const int i = i0 + b * BUCKET_THREADS;
+      tl[b] = i < np ? ptile[i] : -1;
+    }
+#pragma unroll
+    for (int b = 0; b < BUCKET_BATCH; ++b)
+      if (tl[b] >= 0) {
+        const int pos = atomicAdd(&cur[tl[b]], 1);
+        if (in_lds) runs[pos] = i0 + b * BUCKET_THREADS;
+        else sorted[pos] = i0 + b * BUCKET_THREADS;
+      }
+  }
+  if (in_lds) {
+    __syncthreads();
+    for (int i = t; i < total; i += BUCKET_THREADS) sorted[i] = runs[i];
   }
 }
 
