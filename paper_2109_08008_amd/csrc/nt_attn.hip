@@ -376,16 +376,20 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
   float m = -INFINITY, lsum = 0.f, o[VEC];
 #pragma unroll
   for (int x = 0; x < VEC; ++x) o[x] = 0.f;
-  for (int c0 = 0; c0 < n; c0 += KCH) {
-    // every ancestor row first, then all key/value loads with no branch between them, so
-    // the wave has one dependent round trip per chunk; slots past the end re-read the
-    // last one (their scores are masked)
-    int ph[KPL];
+  // the physical row of each of the lane's slots of a chunk (slot t was just written by
+  // this row; slots past the end re-read the last one, their scores are masked)
+  int ph[KPL];
+  auto anc_rows = [&](int c0) {
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
       const int s = min(c0 + g * KPL + j, t);
-      ph[j] = (anc && s < t) ? anc[s] : p;        // slot t was just written by this row
+      ph[j] = (anc && s < t) ? anc[s] : p;
     }
+  };
+  anc_rows(0);
+  for (int c0 = 0; c0 < n; c0 += KCH) {
+    // all key/value loads with no branch between them, then the next chunk's ancestor
+    // rows, in flight with them: one dependent round trip per chunk
     uint4 kr[KPL], vr[KPL];
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
@@ -393,6 +397,7 @@ __global__ __launch_bounds__(256) void self_attn_kernel(SelfAttnArgs a) {
       kr[j] = *reinterpret_cast<const uint4*>(K + off);
       vr[j] = *reinterpret_cast<const uint4*>(Vc + off);
     }
+    if (anc && c0 + KCH < n) anc_rows(c0 + KCH);
     float sc[KPL], cmax = -INFINITY;
 #pragma unroll
     for (int j = 0; j < KPL; ++j) {
