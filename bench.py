@@ -51,20 +51,52 @@ GEMM_CLASSES = (0, 1, 2)
 GEMM_FILES = ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"]
 TRAFFIC = {
     ("gemm_dec", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
-        "fetch_kib": 12672.25, "write_kib": 4063.63, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 12692.34, "write_kib": 4063.63, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_enc", "wide-30-6"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 136800.32, "write_kib": 74738.12, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_vocab", "wide-30-6"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 44593.14, "write_kib": 5091.22, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
-        "fetch_kib": 3920.85, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 3931.38, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_enc", "base-6-6"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 15491.40, "write_kib": 19806.60, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_vocab", "base-6-6"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 14001.81, "write_kib": 3142.06, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
-        "fetch_kib": 15269.18, "write_kib": 17941.88, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 15285.63, "write_kib": 17941.84, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_dec", "deep-shallow-greedy"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 2063.38, "write_kib": 411.51, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_vocab", "deep-shallow-greedy"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 17058.41, "write_kib": 946.58, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_enc", "deep-shallow-beam"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 34549.06, "write_kib": 36548.92, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "205ea6cae8a7289c9cd86ffdb11b7fded1cdc0e84efe1e2f1cb063c0ebcfec40",
-        "fetch_kib": 52133.48, "write_kib": 204231.26, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 22426.87, "write_kib": 6909.66, "fetch_scale": 2.0, "write_scale": 1.0,
+    },
+    ("gemm_dec", "deep-shallow-beam"): {
+        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
+        "fetch_kib": 5923.69, "write_kib": 2873.08, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 
