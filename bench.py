@@ -340,9 +340,14 @@ def main():
     # (the other batches' streams drained first) so that they time the kernel by itself
     # A sample drains the other batches' streams and runs alone, which stalls the pipeline
     # for about one unit: at most 2 per timed step keeps that near 1% of the timed run.
+    # The stride advances the sampled position within a translation by units / samples
+    # from one timed step to the next, so the samples spread over the whole translation
+    # (its long-sentence first batches and short-sentence last ones, early and late steps)
+    # instead of landing on the same units in every timed step.
     units = enc_units if dominant in ENCODE_ONLY_CLASSES else step_units
     samples = max(1, min(args.samples, 2 * args.steps))
-    stride = max(1, (units * args.steps) // samples)
+    per_step = max(1, samples // args.steps)
+    stride = max(1, units // per_step + units // samples)
     nt.nt_prof_reset()
     nt.nt_prof_config(1 << dominant, stride)
     torch.cuda.synchronize()
