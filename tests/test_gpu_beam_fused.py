@@ -90,3 +90,20 @@ def test_logits_copy_out_is_the_same_on_both_paths():
     for a, b in zip(fo[0], po[0]):
         np.testing.assert_array_equal(a, b)
     np.testing.assert_allclose(fo[1], po[1], rtol=1e-6, atol=1e-6)
+
+
+def test_fused_beam_with_more_pairs_than_the_sort_holds_in_lds():
+    """80 sentences at beam 16 over 33 tiles: 1280 rows x 32 tiles = 40960 (row, tile)
+    pairs, more than the sort assembles in LDS (36864), so each pair is stored to its
+    place directly; the result must still equal the plain scan."""
+    shape = synth.ModelShape(64, 2, 256, 1, 1, 4200)
+    blob = synth.make_weights(shape, seed=95, lively=True, eos_boost=1.5)
+    ids, offs = synth.make_sentences(synth.DataSetup(80, "uniform", 2, 8, "uniform"), shape.vocab, seed=96)
+    search = synth.SearchSetup(beam=16, len_penalty=0.6, max_len_a=1.0, max_len_b=3, token_budget=8192, prune=1)
+    model = G.new_model(shape, blob, "f32")
+    fused = _translate(model, ids, offs, search, True)
+    plain = _translate(model, ids, offs, search, False)
+    model.close()
+    for a, b in zip(fused[0], plain[0]):
+        np.testing.assert_array_equal(a, b)
+    np.testing.assert_allclose(fused[1], plain[1], rtol=1e-6, atol=1e-6)
