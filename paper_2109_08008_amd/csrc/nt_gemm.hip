@@ -770,8 +770,9 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
   // FP8 weights (fp16 activations only).  A 64-byte weight row moves 16 rows per wave
   // load, so the narrow tiles change: measured at decode shapes with four GEMMs in flight,
   // 32x64 (3 stages) is the best small tile (650x512x512: 5.1 us against 6.2 at 64x64;
-  // 1300x512x2048: 13.0 against 15.9) and 64x64 the best middle one (1300x1536x512: 8.2
-  // against 9.1 at 64x128).
+  // 1300x512x2048: 13.0 against 15.9).  Alone, 64x64 is the faster middle tile
+  // (1300x1536x512: 8.2 against 9.1 us at 64x128), but inside whole translations the
+  // decoder's projections run best at 64x128 above the smallest shapes.
   // folded LayerNorm: decoder-step launches with weights in the model dtype
   if (epi.lnf_colsum) {
     if constexpr (ROLE != 1) {
@@ -782,11 +783,13 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
         if constexpr (!std::is_same<T, f16>::value) {
           return hipErrorInvalidValue;
         } else {
-          // (the unfolded map's 128x128 becomes 128x64: 164 VGPRs with the row statistics)
+          // 64x128 for every tile above the smallest, as for the decoder's FP8 residual
+          // projections below (measured on wide-30-6-fp8 with four batches in flight:
+          // 264.6k -> 278.4k tok/s against 128x64 / 64x64; base-6-6-fp8 648.9k -> 655.7k)
           switch (tile) {
             case 2:
-            case 3: return launch_tile<T, 128, 64, 2, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
-            case 4: return launch_tile<T, 64, 64, 3, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
+            case 3:
+            case 4: return launch_tile<T, 64, 128, 2, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
             default: return launch_tile<T, 32, 64, 3, ROLE, true, true>(A, lda, Bt, M, N, K, epi, s);
           }
         }
@@ -803,6 +806,8 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
     if constexpr (!std::is_same<T, f16>::value || ROLE == 2) {
       return hipErrorInvalidValue;
     } else {
+      if (ROLE == 1 && tile != 1)   // decoder steps: 64x128 (see the folded map above)
+        return launch_tile<T, 64, 128, 2, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
       switch (tile) {
         case 2: return launch_tile<T, 128, 128, 2, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
         case 3: return launch_tile<T, 128, 64, 2, ROLE, true>(A, lda, Bt, M, N, K, epi, s);
