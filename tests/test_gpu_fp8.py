@@ -129,15 +129,24 @@ def test_fp8_cache_beam_translation_per_token_logprobs():
     search = synth.SearchSetup(beam=4, len_penalty=0.6, max_len_a=1.5, max_len_b=5)
     toks, scores, logp = G.new_model(shape, blob, "f8").translate(ids, offs, search)
     om = G.oracle_model(shape, blob, "f8")
-    worst = 0.0
-    for s, tk, lp in zip(srcs, toks, logp):
-        ref = om.teacher_forced_logits(s, list(tk))
+    ow = G.oracle_model(shape, blob, "f8w")
+
+    def token_logp(model, s, tk):
+        ref = model.teacher_forced_logits(s, list(tk))
         lse = np.log(np.exp(ref - ref.max(1, keepdims=True)).sum(1)) + ref.max(1)
-        want = np.array([ref[t, tk[t]] - lse[t] for t in range(len(tk))])
+        return np.array([ref[t, tk[t]] - lse[t] for t in range(len(tk))])
+
+    worst = cache_effect = 0.0
+    for s, tk, lp in zip(srcs, toks, logp):
+        want = token_logp(om, s, tk)
         worst = max(worst, float(np.abs(np.asarray(lp) - want).max(initial=0)))
-    print("FP8 cache per-token log-prob max abs err", worst, "lengths", [len(t) for t in toks])
+        cache_effect = max(cache_effect, float(np.abs(token_logp(ow, s, tk) - want).max(initial=0)))
+    print("FP8 cache per-token log-prob max abs err", worst, "oracle with vs without the FP8 cache", cache_effect,
+          "lengths", [len(t) for t in toks])
     assert sum(len(t) for t in toks) > len(toks)
-    assert worst <= 2e-2
+    # the derived bound of the FP8 cache (values one E4M3 step apart for up to 2% of the
+    # cache: half the cache's own effect), as for the logits, and never above 5e-2
+    assert worst <= min(5e-2, 0.5 * cache_effect)
 
 
 @pytest.mark.parametrize("beam", [1, 4])
