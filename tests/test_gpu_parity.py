@@ -133,6 +133,7 @@ def test_tiny_greedy_fp32_token_ids():
 
 
 @pytest.mark.parametrize("beam,alpha,early", [(4, 0.0, 1), (4, 0.6, 1), (4, 0.6, 0), (2, 0.0, 1), (2, 0.6, 1),
+                                              (3, 0.6, 1), (5, 0.0, 1), (6, 0.6, 0), (7, 0.6, 1), (12, 0.6, 1),
                                               (8, 0.0, 1), (8, 0.6, 1), (16, 0.0, 1), (16, 0.6, 1), (16, 0.6, 0)])
 def test_beam_fp32_token_ids(beam, alpha, early):
     """Beam widths 2 to 16 (the widest the library accepts; 2K = 32 candidates a row).  The
