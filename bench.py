@@ -51,52 +51,52 @@ GEMM_CLASSES = (0, 1, 2)
 GEMM_FILES = ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"]
 TRAFFIC = {
     ("gemm_dec", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 12692.34, "write_kib": 4063.63, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 12662.23, "write_kib": 4063.62, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 136800.32, "write_kib": 74738.12, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 137203.78, "write_kib": 74738.14, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 44593.14, "write_kib": 5091.22, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 44469.27, "write_kib": 5095.09, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 3931.38, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 3929.49, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 15491.40, "write_kib": 19806.60, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 15483.54, "write_kib": 19806.60, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 14001.81, "write_kib": 3142.06, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 13998.59, "write_kib": 3142.18, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 15285.63, "write_kib": 17941.84, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 15289.07, "write_kib": 17941.82, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 2063.38, "write_kib": 411.51, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 2063.13, "write_kib": 411.51, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 17058.41, "write_kib": 946.58, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 17058.89, "write_kib": 945.56, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 34549.06, "write_kib": 36548.92, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 34636.35, "write_kib": 36548.98, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 22426.87, "write_kib": 6909.66, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 22423.03, "write_kib": 6898.18, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "ce93368d849332ed588677de3274b384557aec300bda0ff807c131d67a55734f",
-        "fetch_kib": 5923.69, "write_kib": 2873.08, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "fetch_kib": 5920.41, "write_kib": 2873.04, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 

@@ -756,7 +756,8 @@ hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int
 //                      decoder's K >= 2048);
 //   M*N < 3M outputs:  64x128, 2 stages (1300x1536: 5.6 us against 6.8 at 64x32;
 //                      2160x1024x1024: 8.6 against 12.0);
-//   larger:            128x128, 2 stages (2160x1024x4096: 27.8 us against 43.8 at 64x32).
+//   larger:            128x128, 2 stages (2160x1024x4096: 27.8 us against 43.8 at 64x32),
+//                      except in decoder steps, which take 64x128 there (below).
 // All reduce each output over K in the same order, so the choice never changes a result.
 template <typename T, int ROLE>
 hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, const GemmEpi& epi, hipStream_t s,
@@ -816,6 +817,10 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
       }
     }
   }
+  // decoder steps keep to 64-row tiles where the shape picks 128x128: alone, 3172x1024x4096
+  // takes 40.7 us at 64x128 against 47.5 us, 3172x1024x1024 13.2 against 18.3 (the
+  // 128x128 choice was measured against 64x32 only)
+  if (ROLE == 1 && tile == 2) tile = 4;
   switch (tile) {
     case 2: return launch_tile<T, 128, 128, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
     case 3: return launch_tile<T, 128, 64, 2, ROLE>(A, lda, Bt, M, N, K, epi, s);
