@@ -751,7 +751,10 @@ hipError_t launch_tile(const void* A, int lda, const void* Bt, int M, int N, int
 // Tile choice by problem size, measured on MI355X with four batches' GEMMs in flight at
 // once (how nt_translate runs them).  LDS footprint matters more than pipeline depth, so
 // the big tiles use two stages.
-//   M >= 4096 (encoder, big batches): 128x64 for N <= 2048, else 128x128;
+//   M >= 4096 (encoder, big batches): 128x64 for N <= 2048, else 128x128; and
+//                      128x128 for the FFN's second GEMM (K >= 2048) from 8M outputs up
+//                      (16384x512x2048: 40.6 us against 52.1; 16384x1024x4096: 135.4
+//                      against 161.4; 8192x512x2048 stays: 26.0 against 31.0);
 //   M*N < 1M outputs:  64x32, 3 stages (skinny decode-step shapes; 4 stages for the
 //                      decoder's K >= 2048);
 //   M*N < 3M outputs:  64x128, 2 stages (1300x1536: 5.6 us against 6.8 at 64x32;
@@ -765,7 +768,7 @@ hipError_t launch(const void* A, int lda, const void* Bt, int M, int N, int K, c
   if (M <= 0 || N <= 0) return hipSuccess;
   if (tile == 0) {
     const long long mn = (long long)M * N;
-    if (M >= 4096) tile = N <= 2048 ? 3 : 2;
+    if (M >= 4096) tile = N <= 2048 && (K < 2048 || mn < (8ll << 20)) ? 3 : 2;
     else tile = mn < (1ll << 20) ? 1 : mn < (3ll << 20) ? 4 : 2;
   }
   // FP8 weights (fp16 activations only).  A 64-byte weight row moves 16 rows per wave
