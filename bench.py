@@ -51,52 +51,52 @@ GEMM_CLASSES = (0, 1, 2)
 GEMM_FILES = ["paper_2109_08008_amd/csrc/nt_gemm.hip", "paper_2109_08008_amd/csrc/nt_common.h"]
 TRAFFIC = {
     ("gemm_dec", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 12662.23, "write_kib": 4063.62, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 12662.90, "write_kib": 4063.62, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 137203.78, "write_kib": 74738.14, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 111992.06, "write_kib": 74738.06, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "wide-30-6"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 44469.27, "write_kib": 5095.09, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 44495.21, "write_kib": 5086.86, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
         "fetch_kib": 3929.49, "write_kib": 1303.11, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 15483.54, "write_kib": 19806.60, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 15480.32, "write_kib": 19806.60, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "base-6-6"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 13998.59, "write_kib": 3142.18, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 13998.60, "write_kib": 3141.33, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 15289.07, "write_kib": 17941.82, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 15286.01, "write_kib": 17941.79, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
         "fetch_kib": 2063.13, "write_kib": 411.51, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "deep-shallow-greedy"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 17058.89, "write_kib": 945.56, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 17058.90, "write_kib": 945.94, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_enc", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 34636.35, "write_kib": 36548.98, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 34254.48, "write_kib": 36548.84, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_vocab", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 22423.03, "write_kib": 6898.18, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 22423.13, "write_kib": 6903.01, "fetch_scale": 2.0, "write_scale": 1.0,
     },
     ("gemm_dec", "deep-shallow-beam"): {
-        "files": GEMM_FILES, "sha256": "59a5038ce44cdca2bc630197dcd8b328f4ef20e393ee563f00324d2906313dd4",
-        "fetch_kib": 5920.41, "write_kib": 2873.04, "fetch_scale": 2.0, "write_scale": 1.0,
+        "files": GEMM_FILES, "sha256": "8696ca14961f0c4ac045848f028eeab73e938a62840b3e44679dde3faaf0af44",
+        "fetch_kib": 5920.51, "write_kib": 2873.06, "fetch_scale": 2.0, "write_scale": 1.0,
     },
 }
 
