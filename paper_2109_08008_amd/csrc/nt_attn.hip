@@ -56,6 +56,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
   constexpr int VPL = KSTEP * ROWP / kWave;   // 16-byte value pieces per lane per P.V step
   static_assert(DH % KSTEP == 0 && NSB % SB == 0, "head dim must fill whole MFMA steps");
   static_assert(KSTEP * ROWP % kWave == 0, "value rows of a P.V step split evenly over the lanes");
+  constexpr bool KALL = ROLE == 1;   // the chunk's key blocks all loaded before its scores
   __shared__ __attribute__((aligned(16))) unsigned Vs[4][KSTEP][VSTR];
   constexpr int RW = RPR ? 4 : 1;   // per-wave RPR buffers (1 placeholder when unused)
   constexpr int RQ = RPR ? 16 : 1;
@@ -149,15 +150,30 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(MhaArgs a) {
     load_v(c0, vcur);
     floatx4 sc[NSB];
     float cmax = -INFINITY;
+    // decoder: every key block of the chunk is fetched before the first score, so the
+    // blocks' loads are in flight together (rows past len re-read the last key, and
+    // their scores are masked below)
+    u32x4 kf[KALL ? NSB : 1][KALL ? QK : 1];
+    if constexpr (KALL) {
+#pragma unroll
+      for (int kb = 0; kb < NSB; ++kb) {
+        const char* krow = Kb + (size_t)min(c0 + kb * 16 + ln, len - 1) * ks_b;
+#pragma unroll
+        for (int st = 0; st < QK; ++st) kf[kb][st] = *reinterpret_cast<const u32x4*>(krow + st * 64 + grp * 16);
+      }
+      __builtin_amdgcn_sched_barrier(0);   // the value and key loads all issue before the scores
+    }
 #pragma unroll
     for (int kb = 0; kb < NSB; ++kb) {
       sc[kb] = floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-      if (kb < nb) {
+      if (KALL || kb < nb) {
         const char* krow = Kb + (size_t)min(c0 + kb * 16 + ln, len - 1) * ks_b;
         floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int st = 0; st < QK; ++st)
-          acc = Mfma<T>::step(*reinterpret_cast<const u32x4*>(krow + st * 64 + grp * 16), qf[st], acc);
+          acc = Mfma<T>::step(KALL ? kf[kb % (KALL ? NSB : 1)][st % (KALL ? QK : 1)]
+                                   : *reinterpret_cast<const u32x4*>(krow + st * 64 + grp * 16),
+                              qf[st], acc);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int key = c0 + kb * 16 + 4 * grp + r;
