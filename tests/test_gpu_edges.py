@@ -1,7 +1,8 @@
 """GPU edge cases of nt_translate: input it must reject (an empty sentence, a source past
 the position table, a token ID outside the vocabulary, a target limit past the position
 table), a model that keeps working after a rejected call, the longest source the
-position table allows, and one-step target limits.  Parity is against the oracle in
+position table allows, one-step target limits, and source lengths at the edges of the
+decoder cross-attention's key blocks and chunks.  Parity is against the oracle in
 fp32 (token IDs under the near-tie protocol, teacher-forced logits within 1e-3)."""
 import numpy as np
 import pytest
@@ -195,4 +196,33 @@ def test_target_length_cap(beam):
     with pytest.raises(nt.NTError) as err:
         model.translate(ids, offs, synth.replace(search, max_len_cap=-1))
     assert err.value.status == nt.NT_E_INVALID, err.value
+    model.close()
+
+
+def test_cross_attention_chunk_edges():
+    """Source lengths at and next to the decoder cross-attention's 16-key blocks and
+    64-key chunks, at d_head 64 (a chunk's key blocks past the source length re-read its
+    last key and are masked): fp32 teacher-forced logits within 1e-3 of the oracle, and
+    the per-token log-probs of beam-4 translations within 1e-3 of the oracle's logits on
+    the same tokens."""
+    shape = synth.ModelShape(128, 2, 256, 1, 1, 101)
+    blob = synth.make_weights(shape, seed=77, lively=True, eos_boost=2.0)
+    rng = np.random.default_rng(78)
+    lengths = [1, 15, 16, 17, 31, 32, 33, 47, 48, 49, 63, 64, 65, 127, 128, 129]
+    srcs = [list(rng.integers(3, shape.vocab, size=L)) for L in lengths]
+    tgts = [list(rng.integers(3, shape.vocab, size=3)) for _ in srcs]
+    model = G.new_model(shape, blob, "f32")
+    om = G.oracle_model(shape, blob, "f32")
+    got, _, _ = G.gpu_teacher_forced(model, srcs, tgts, shape.vocab)
+    for b, (s, tg) in enumerate(zip(srcs, tgts)):
+        np.testing.assert_allclose(got[b], om.teacher_forced_logits(s, tg), atol=1e-3, err_msg=f"length {len(s)}")
+    ids, offs = _csr(srcs)
+    search = synth.SearchSetup(beam=4, len_penalty=0.6, max_len_a=0.0, max_len_b=4)
+    toks, _, logp = model.translate(ids, offs, search)
+    assert sum(len(t) for t in toks) > len(toks)
+    for s, tk, lp in zip(srcs, toks, logp):
+        ref = om.teacher_forced_logits(s, list(tk))
+        lse = np.log(np.exp(ref - ref.max(1, keepdims=True)).sum(1)) + ref.max(1)
+        want = np.array([ref[t, tk[t]] - lse[t] for t in range(len(tk))])
+        np.testing.assert_allclose(np.asarray(lp), want, atol=1e-3, err_msg=f"length {len(s)}")
     model.close()
