@@ -319,8 +319,8 @@ nt_status nt_op_gemm(int32_t dtype, const void* d_A, int32_t lda, const void* d_
  * holds the row statistics at a higher occupancy).  d_bscale: NULL, or (dtype NT_F16
  * only) Bt holds FP8 E4M3 bytes and column n of A . Bt is multiplied by d_bscale[n] before
  * the normalisation, as for the decoder projections of an fp8_weights model (colsum then
- * holds the sums of the dequantized columns); tiles 1 and 4 are then 32x64 and 64x64.
- * Asynchronous. */
+ * holds the sums of the dequantized columns); tile 1 is then 32x64 and tiles 2-4 are
+ * 64x128.  Asynchronous. */
 nt_status nt_op_gemm_ln(int32_t dtype, const void* d_A, int32_t lda, const void* d_Bt, int32_t M, int32_t N,
                         int32_t K, const float* d_colsum, float ln_eps, const float* d_bias, void* d_out,
                         int32_t ldc, int32_t relu, int32_t tile, const float* d_bscale, void* stream);
