@@ -226,3 +226,31 @@ def test_cross_attention_chunk_edges():
         want = np.array([ref[t, tk[t]] - lse[t] for t in range(len(tk))])
         np.testing.assert_allclose(np.asarray(lp), want, atol=1e-3, err_msg=f"length {len(s)}")
     model.close()
+
+
+@pytest.mark.parametrize("beam", [1, 4])
+def test_long_k_decoder_projection_is_batch_invariant(beam):
+    """The decoder's K = 4096 projection (the second FFN GEMM at d_ff 4096, the longest
+    k-loop of a step, on its four-stage tile): fp16 translations are bitwise the same
+    whatever the batching, and the fp16 teacher-forced logits stay within 5e-2 of the
+    oracle."""
+    shape = synth.ModelShape(1024, 16, 4096, 1, 1, 101)
+    blob = synth.make_weights(shape, seed=79, lively=True, eos_boost=4.0)
+    ids, offs = synth.make_sentences(synth.DataSetup(24, "uniform", 1, 30, "uniform"), shape.vocab, seed=80)
+    model = G.new_model(shape, blob, "f16")
+    base = synth.SearchSetup(beam=beam, len_penalty=0.6, max_len_a=1.5, max_len_b=5, token_budget=8192, prune=1)
+    ref = model.translate(ids, offs, base)
+    assert sum(len(t) for t in ref[0]) > len(ref[0])
+    for kw in [dict(token_budget=64), dict(token_budget=0, max_batch_sents=1)]:
+        t, s, _ = model.translate(ids, offs, synth.replace(base, **kw))
+        for a, b in zip(ref[0], t):
+            np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(ref[1], s)
+    srcs = synth.sentence_list(ids, offs)[:6]
+    rng = np.random.default_rng(81)
+    tgts = [list(rng.integers(3, shape.vocab, size=4)) for _ in srcs]
+    got, _, _ = G.gpu_teacher_forced(model, srcs, tgts, shape.vocab)
+    om = G.oracle_model(shape, blob, "f16")
+    for b, (s, tg) in enumerate(zip(srcs, tgts)):
+        assert float(np.abs(got[b] - om.teacher_forced_logits(s, tg)).max()) <= 5e-2, len(s)
+    model.close()
